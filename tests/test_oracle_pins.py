@@ -1,0 +1,410 @@
+"""Pins the CPU oracle to what the paper and the mathematics fix.
+
+Each test checks the oracle against something other than itself: a closed
+form, a library routine (numpy's bit packing and norms, torch.optim.Adam and
+torch.optim.SGD), an identity the paper proves, a hand-worked example with
+exactly representable numbers, or a special case that reduces to a textbook
+method.  A plausible slip in the oracle (a dropped error term, a wrong sign,
+a transposed bit order, eps in the wrong place, a wrong chunk cut) fails at
+least one of them.
+"""
+import math
+
+import numpy as np
+import pytest
+
+import oracle
+import synth
+
+BETA1, BETA2, EPS, LR = 0.9, 0.999, 1e-8, 1e-4
+
+
+def assert_close_scaled(a, b, rel):
+    """|a - b| <= rel * (|b| + mean|b|): relative, with a floor at the typical
+    magnitude so that fp32 cancellation in tiny entries is not flagged."""
+    a = np.asarray(a, np.float64); b = np.asarray(b, np.float64)
+    tol = rel * (np.abs(b) + np.abs(b).mean())
+    bad = np.abs(a - b) > tol
+    assert not bad.any(), (int(bad.sum()), float(np.abs(a - b).max()))
+
+
+def ulp32(a):
+    a = np.abs(np.asarray(a, np.float32))
+    return np.spacing(a).astype(np.float64)
+
+
+# ---------------------------------------------------------------------------
+# Layout: chunk cut of each tensor into n chunks (64-aligned), segments
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("numel,n", [([1], 1), ([100, 1 << 20, 5], 4), ([64, 65, 128, 129, 4096], 8),
+                                     ([0, 7, 0, 1000], 3), ([10_000], 256)])
+def test_layout_brute_force(numel, n):
+    L = oracle.Layout(numel, n)
+    off = 0
+    for k, d in enumerate(numel):
+        assert L.tensor_off[k] == off
+        assert off % 64 == 0
+        c = L.chunk_len(k)
+        assert c % 64 == 0
+        if d:
+            # the smallest 64-multiple c with n*c >= d
+            assert n * c >= d and (c == 64 or n * (c - 64) < d)
+        # brute force: element r of tensor k belongs to chunk r // c
+        for j in range(n):
+            b, e = L.seg_begin[k * n + j], L.seg_end[k * n + j]
+            members = [r for r in range(d) if c and r // c == j] if d <= 20000 else None
+            if members is not None:
+                if members:
+                    assert (b, e) == (off + members[0], off + members[-1] + 1)
+                else:
+                    assert b == e
+            assert (b - off) % 64 == 0 or b == e
+        off += 64 * ((d + 63) // 64)
+    assert L.D == off and L.W * 64 == L.D
+
+
+def test_layout_bert_large_chunks():
+    wl = synth.get("bert_large")
+    L = oracle.Layout(wl.numel, wl.n)
+    assert wl.d == 334_088_192 and L.D == wl.d
+    assert L.chunk_len(0) == 10_440_256 == wl.d // 32
+    wb = synth.get("bert_base")
+    assert wb.d == 108_888_576
+    assert sum(int(np.prod(s)) for s, _ in synth.bert_tensor_shapes(24, 1024, 4096)) == wl.d
+    assert len(synth.bert_tensor_shapes(24, 1024, 4096)) == 386
+    assert len(synth.bert_tensor_shapes(12, 768, 3072)) == 194
+    s = synth.get("share256")
+    Ls = oracle.Layout(s.numel, s.n)
+    assert Ls.chunk_len(0) == 1_305_088
+    assert Ls.seg_end[255] - Ls.seg_begin[255] == 1_290_752
+
+
+# ---------------------------------------------------------------------------
+# The compression operator: bit order, sign convention, scale
+# ---------------------------------------------------------------------------
+
+def test_bits_match_numpy_packbits():
+    rng = np.random.default_rng(5)
+    for length in [1, 63, 64, 65, 200, 4096 + 17]:
+        z = rng.standard_normal(length).astype(np.float32)
+        z[:: 7] = 0.0
+        z[3 % length] = -0.0
+        bits, _ = oracle.compress(z)
+        ref = np.packbits(z >= 0, bitorder="little")
+        ref = np.concatenate([ref, np.zeros(len(bits) * 8 - len(ref), np.uint8)])
+        assert bits.view(np.uint8).tobytes() == ref.tobytes()
+
+
+def test_sign_convention_zero_nan_padding():
+    z = np.array([0.0, -0.0, np.nan, -1.0, 1.0], np.float32)
+    bits, s = oracle.compress(z)
+    assert int(bits[0]) == 0b10011  # +0 -> 1, -0 -> 1, NaN -> 0, -1 -> 0, 1 -> 1
+    assert np.isnan(s)
+    # padding bits beyond the segment are zero
+    z = np.ones(70, np.float32)
+    bits, _ = oracle.compress(z)
+    assert int(bits[1]) == (1 << 6) - 1
+
+
+def test_scale_same_l2_magnitude():
+    rng = np.random.default_rng(7)
+    for length in [1, 2, 3, 64, 1000, 262_144]:
+        z = (rng.standard_normal(length) * rng.uniform(1e-6, 10)).astype(np.float32)
+        bits, s = oracle.compress(z)
+        norm = np.linalg.norm(z.astype(np.float64))
+        # ||C[z]||_2 = s * sqrt(len) equals ||z||_2 up to fp32 rounding of s
+        assert abs(float(s) - norm / math.sqrt(length)) <= 0.5 * ulp32(s) * 1.0001
+    # an l1 (mean |z|) scale would differ on a non-constant vector
+    z = np.array([3.0, 4.0], np.float32)
+    _, s = oracle.compress(z)
+    assert s == np.float32(math.sqrt(12.5))
+
+
+def test_empty_segment_scale_zero():
+    z = np.ones(10, np.float32)
+    bits = np.zeros(1, np.uint64)
+    assert oracle.lib().orc_compress(5, 5, z, bits) == 0.0
+    assert int(bits[0]) == 0
+
+
+# ---------------------------------------------------------------------------
+# Hand-worked two-step example (Algorithm 1, exact dyadic arithmetic)
+# d = 2, n = 2, beta1 = 1/2, lr = 1/2, eps = 0, v = [4, 16], x0 = [1, 1], m0 = 0
+#  step 1: g0 = [28, -4], g1 = [48, 48]
+#    worker 0: z = [14, -2], s = sqrt(200/2) = 10, bits [1,0], m_hat [10,-10], delta0 = [4, 8]
+#    worker 1: z = [24, 24], s = 24, bits [1,1], m_hat [24, 24], delta1 = [0, 0]
+#    server : avg = [17, 7], z_bar = [17, 7], s_bar = sqrt(338/2) = 13, bits [1,1],
+#             m_bar = [13, 13], delta_bar = [4, -6]
+#    update : x = [1 - 0.5*13/2, 1 - 0.5*13/4] = [-2.25, -0.625], m = [13, 13]
+#  step 2: g0 = [-23, -15], g1 = [-27, -11]
+#    worker 0: z = 6.5 + g/2 + [4, 8] = [-1, 7], s = 5, bits [0,1], m_hat [-5, 5], delta0 = [4, 2]
+#    worker 1: z = 6.5 + g/2 + [0, 0] = [-7, 1], s = 5, bits [0,1], m_hat [-5, 5], delta1 = [-2, -4]
+#    server : avg = [-5, 5], z_bar = [-1, -1], s_bar = 1, bits [0,0], m_bar = [-1,-1], delta_bar = 0
+#    update : x = [-2.25 + 0.25, -0.625 + 0.125] = [-2, -0.5], m = [-1, -1]
+# ---------------------------------------------------------------------------
+
+def test_hand_worked_two_steps():
+    L = oracle.Layout([2], 2)
+    assert L.D == 64 and L.segments() == [(0, 2), (2, 2)]
+    x = np.zeros(64, np.float32); x[:2] = 1.0
+    v = np.zeros(64, np.float32); v[:2] = [4.0, 16.0]
+    st = oracle.State(L, x, np.zeros(64, np.float32), v)
+    g = np.zeros((2, 64), np.float32)
+    g[0, :2] = [28, -4]; g[1, :2] = [48, 48]
+    st.step(g, lr=0.5, beta1=0.5, eps=0.0)
+    np.testing.assert_array_equal(st.wscales[:, 0], [10, 24])
+    np.testing.assert_array_equal(st.wscales[:, 1], [0, 0])
+    assert [int(w) for w in st.wbits[:, 0]] == [0b01, 0b11]
+    np.testing.assert_array_equal(st.delta[:, :2], [[4, 8], [0, 0]])
+    assert st.sscales[0] == 13 and st.sscales[1] == 0 and int(st.sbits[0]) == 0b11
+    np.testing.assert_array_equal(st.delta_bar[:2], [4, -6])
+    np.testing.assert_array_equal(st.x[:2], [-2.25, -0.625])
+    np.testing.assert_array_equal(st.m[:2], [13, 13])
+    g[0, :2] = [-23, -15]; g[1, :2] = [-27, -11]
+    st.step(g, lr=0.5, beta1=0.5, eps=0.0)
+    np.testing.assert_array_equal(st.wscales[:, 0], [5, 5])
+    assert [int(w) for w in st.wbits[:, 0]] == [0b10, 0b10]
+    np.testing.assert_array_equal(st.delta[:, :2], [[4, 2], [-2, -4]])
+    assert st.sscales[0] == 1 and int(st.sbits[0]) == 0
+    np.testing.assert_array_equal(st.delta_bar[:2], [0, 0])
+    np.testing.assert_array_equal(st.x[:2], [-2.0, -0.5])
+    np.testing.assert_array_equal(st.m[:2], [-1, -1])
+    # padding untouched
+    assert not st.x[2:].any() and not st.delta[:, 2:].any()
+
+
+# ---------------------------------------------------------------------------
+# Error-feedback identity and telescoping (appendix "Proof to the updating form")
+# ---------------------------------------------------------------------------
+
+def _run_compression(numel, n, steps, seed=11, start_m=None):
+    wl = synth.Workload(name="t", numel=numel, n=n, warmup_steps=0, steps=steps, seed_grads=seed)
+    L = oracle.Layout(numel, n)
+    x = synth.host_params(wl, L.D)
+    m = synth.host_normal(L.D, 1e-4, seed, 99) if start_m is None else start_m
+    v = np.abs(synth.host_normal(L.D, 1e-6, seed, 98))
+    mask = L.real_mask()
+    x[~mask] = 0; m[~mask] = 0; v[~mask] = 0
+    return wl, L, oracle.State(L, x, m, v)
+
+
+def test_error_feedback_identity_worker_and_server():
+    wl, L, st = _run_compression([5000, 300], 4, 0)
+    z = np.zeros(L.D, np.float32)
+    for t in range(3):
+        g = synth.host_grads(wl, L.D, L.tensor_off, t)
+        for i in range(L.n):
+            for q, (b, e) in enumerate(L.segments()):
+                delta_prev = st.delta[i].copy()
+                s = oracle.worker_segment(b, e, BETA1, st.m, g[i], st.delta[i], st.wbits[i], z)
+                st.wscales[i, q] = s
+                dec = np.array([oracle.decode(st.wbits[i], idx, s) for idx in range(b, e)], np.float64)
+                zz = z[b:e].astype(np.float64)
+                # C[z] + delta_new == z, up to one rounding of the subtraction
+                err = np.abs(dec + st.delta[i, b:e] - zz)
+                assert np.all(err <= 0.5 * np.maximum(ulp32(zz), ulp32(s)))
+                assert not np.array_equal(delta_prev[b:e], st.delta[i, b:e]) or e == b
+        for q, (b, e) in enumerate(L.segments()):
+            s = oracle.server_segment(b, e, L.n, st.wbits.reshape(-1), L.W,
+                                      np.ascontiguousarray(st.wscales[:, q]), 1,
+                                      st.delta_bar, st.sbits, z)
+            dec = np.array([oracle.decode(st.sbits, idx, s) for idx in range(b, e)], np.float64)
+            err = np.abs(dec + st.delta_bar[b:e] - z[b:e].astype(np.float64))
+            assert np.all(err <= 0.5 * np.maximum(ulp32(z[b:e]), ulp32(s)))
+            st.sscales[q] = s
+            oracle.update_segment(b, e, st.sbits, s, LR, EPS, st.x, st.m, st.v)
+
+
+@pytest.mark.parametrize("n", [1, 3, 4])
+def test_telescoping_update_form(n):
+    """m_t = beta1 m_{t-1} + (1-beta1) g_avg_t + Delta_{t-1} - Delta_t with
+    Delta_t = mean_i delta_t^(i) + delta_bar_t, checked in float64."""
+    wl, L, st = _run_compression([3000, 130, 64], n, 6)
+    mask = L.real_mask()
+    Delta_prev = np.zeros(L.D)
+    for t in range(6):
+        g = synth.host_grads(wl, L.D, L.tensor_off, t)
+        m_prev = st.m.astype(np.float64)
+        st.step(g, LR, BETA1, EPS)
+        Delta = st.delta.astype(np.float64).mean(0) + st.delta_bar
+        rhs = BETA1 * m_prev + (1 - BETA1) * g.astype(np.float64).mean(0) + Delta_prev - Delta
+        mag = np.maximum.reduce([np.abs(m_prev), np.abs(st.m), np.abs(Delta), np.abs(Delta_prev),
+                                 np.abs(g).max(0) * (1 - BETA1)])
+        assert np.all(np.abs(st.m - rhs)[mask] <= 16 * 2.0 ** -24 * mag[mask] + 1e-30)
+        Delta_prev = Delta
+    # the errors carry real information: dropping them breaks the identity
+    assert np.abs(Delta_prev[mask]).max() > 1e-6
+
+
+# ---------------------------------------------------------------------------
+# Special cases
+# ---------------------------------------------------------------------------
+
+def test_identical_workers_server_is_passthrough():
+    """n identical workers: the server average equals one worker's decoded
+    message, server bits equal worker bits, the server error stays zero."""
+    wl, L, st = _run_compression([4096, 1000], 4, 0)
+    for t in range(4):
+        g1 = synth.host_grads(wl, L.D, L.tensor_off, t, workers=[0])
+        g = np.repeat(g1, L.n, axis=0)
+        st.step(g, LR, BETA1, EPS)
+        for i in range(1, L.n):
+            np.testing.assert_array_equal(st.wbits[i], st.wbits[0])
+            np.testing.assert_array_equal(st.wscales[i], st.wscales[0])
+        np.testing.assert_array_equal(st.sbits, st.wbits[0])
+        np.testing.assert_array_equal(st.sscales, st.wscales[0, :])
+        assert not st.delta_bar.any()
+
+
+def test_single_worker():
+    wl, L, st = _run_compression([777, 64], 1, 0)
+    for t in range(3):
+        st.step(synth.host_grads(wl, L.D, L.tensor_off, t), LR, BETA1, EPS)
+        np.testing.assert_array_equal(st.sbits, st.wbits[0])
+        np.testing.assert_array_equal(st.sscales, st.wscales[0])
+        assert not st.delta_bar.any()
+
+
+def test_chunk_independence():
+    """Each segment is an independent parameter-server problem: running the
+    per-segment pieces on a segment copied out alone gives the same bits."""
+    wl, L, st = _run_compression([3000, 200], 3, 0)
+    g = synth.host_grads(wl, L.D, L.tensor_off, 0)
+    before = (st.x.copy(), st.m.copy(), st.v.copy())
+    st.step(g, LR, BETA1, EPS)
+    z = np.zeros(L.D, np.float32)
+    for q, (b, e) in enumerate(L.segments()):
+        ln = e - b
+        if ln == 0:
+            continue
+        W = (ln + 63) // 64
+        wb = np.zeros((L.n, W), np.uint64)
+        ws = np.zeros(L.n, np.float32)
+        for i in range(L.n):
+            d_i = np.zeros(ln, np.float32)
+            ws[i] = oracle.worker_segment(0, ln, BETA1, np.ascontiguousarray(before[1][b:e]),
+                                          np.ascontiguousarray(g[i, b:e]), d_i, wb[i], z)
+            np.testing.assert_array_equal(d_i, st.delta[i, b:e])
+        assert np.array_equal(ws, st.wscales[:, q])
+        np.testing.assert_array_equal(wb, st.wbits[:, b // 64:b // 64 + W])
+        db = np.zeros(ln, np.float32)
+        sb = np.zeros(W, np.uint64)
+        s = oracle.server_segment(0, ln, L.n, wb.reshape(-1), W, ws, 1, db, sb, z)
+        assert s == st.sscales[q]
+        np.testing.assert_array_equal(sb, st.sbits[b // 64:b // 64 + W])
+        x = before[0][b:e].copy(); m = np.zeros(ln, np.float32)
+        oracle.update_segment(0, ln, sb, s, LR, EPS, x, m, np.ascontiguousarray(before[2][b:e]))
+        np.testing.assert_array_equal(x, st.x[b:e])
+
+
+def test_message_volume():
+    """One sign bit per element plus one fp32 scale per segment: about 1/32
+    of the fp32 volume (the paper's 97% reduction versus fp32)."""
+    wl = synth.get("bert_large")
+    L = oracle.Layout(wl.numel, wl.n)
+    packed = L.W * 8 + 4 * L.S
+    assert packed / (4 * wl.d) < 0.0313
+    assert 1 - packed / (4 * wl.d) > 0.968
+
+
+# ---------------------------------------------------------------------------
+# Warm-up: textbook Adam (library) and the paper's no-bias-correction form
+# ---------------------------------------------------------------------------
+
+def _torch_adam_trajectory(x0, gbar_steps, lr, b1, b2, eps, bias_correction):
+    import torch
+    p = torch.nn.Parameter(torch.from_numpy(x0.astype(np.float64)).clone())
+    opt = torch.optim.Adam([p], lr=lr, betas=(b1, b2), eps=eps, foreach=False)
+    for t, gb in enumerate(gbar_steps, start=1):
+        if not bias_correction:
+            # torch always divides by bc1 and bc2; undo it with per-step lr, eps
+            bc1, bc2 = 1 - b1 ** t, 1 - b2 ** t
+            opt.param_groups[0]["lr"] = lr * bc1 / math.sqrt(bc2)
+            opt.param_groups[0]["eps"] = eps / math.sqrt(bc2)
+        p.grad = torch.from_numpy(gb.astype(np.float64))
+        opt.step()
+    st = opt.state[p]
+    return p.detach().numpy(), st["exp_avg"].numpy(), st["exp_avg_sq"].numpy()
+
+
+@pytest.mark.parametrize("bias_correction", [1, 0])
+def test_warmup_matches_torch_adam(bias_correction):
+    wl = synth.get("tiny")
+    L = oracle.Layout([5000], 4)
+    x = synth.host_params(wl, L.D)
+    x0 = x.copy()
+    m = np.zeros(L.D, np.float32); v = np.zeros(L.D, np.float32)
+    gbars = []
+    for t in range(1, 11):
+        g = synth.host_grads(wl, L.D, L.tensor_off, t)
+        gbars.append(g.astype(np.float64).mean(0))
+        oracle.warmup_step(L, x, m, v, g, 4, LR, BETA1, BETA2, EPS, bias_correction, t)
+    # the oracle's hyperparameters are binary32; give torch the same values
+    f = lambda a: float(np.float32(a))
+    xr, mr, vr = _torch_adam_trajectory(x0[:5000], [gb[:5000] for gb in gbars],
+                                        f(LR), f(BETA1), f(BETA2), f(EPS), bias_correction)
+    assert_close_scaled(m[:5000], mr, 1e-5)
+    assert_close_scaled(v[:5000], vr, 1e-5)
+    assert_close_scaled(x[:5000] - x0[:5000], xr - x0[:5000], 1e-4)
+    # the update is not negligible relative to the tolerance
+    assert np.abs(x[:5000] - x0[:5000]).max() > 1e-4
+
+
+def test_warmup_constant_gradient_closed_form():
+    """Constant gradient g: m_t = (1-beta1^t) g, v_t = (1-beta2^t) g^2 and
+    x_t = x_0 - lr sum_s m_s / (sqrt(v_s) + eps) (no bias correction)."""
+    L = oracle.Layout([256], 1)
+    gc = np.linspace(-2e-3, 2e-3, 256).astype(np.float32)
+    x = np.ones(256, np.float32); m = np.zeros(256, np.float32); v = np.zeros(256, np.float32)
+    g64 = gc.astype(np.float64)
+    b1, b2, lr, eps = (float(np.float32(a)) for a in (BETA1, BETA2, LR, EPS))
+    acc = np.zeros(256)
+    for t in range(1, 9):
+        oracle.warmup_step(L, x, m, v, gc[None, :].copy(), 1, LR, BETA1, BETA2, EPS, 0, t)
+        mt = (1 - b1 ** t) * g64
+        vt = (1 - b2 ** t) * g64 ** 2
+        acc += mt / (np.sqrt(vt) + eps)
+        np.testing.assert_allclose(m, mt, rtol=4e-6, atol=1e-30)
+        np.testing.assert_allclose(v, vt, rtol=4e-6, atol=1e-30)
+        np.testing.assert_allclose(x, 1 - lr * acc, rtol=1e-6, atol=1e-7)
+
+
+def test_warmup_gradient_average_over_workers():
+    """n identical gradient rows average to that row exactly."""
+    L = oracle.Layout([300], 5)
+    g = synth.host_normal(320, 1e-3, 4)
+    g[300:] = 0
+    xa, ma, va = (np.ones(320, np.float32), np.zeros(320, np.float32), np.zeros(320, np.float32))
+    xb, mb, vb = xa.copy(), ma.copy(), va.copy()
+    oracle.warmup_step(L, xa, ma, va, np.repeat(g[None], 5, 0), 5, LR, BETA1, BETA2, EPS, 0, 1)
+    oracle.warmup_step(L, xb, mb, vb, g[None].copy(), 1, LR, BETA1, BETA2, EPS, 0, 1)
+    np.testing.assert_array_equal(xa, xb)
+    np.testing.assert_array_equal(ma, mb)
+
+
+# ---------------------------------------------------------------------------
+# Identity compressor: momentum SGD with the frozen preconditioner
+# ---------------------------------------------------------------------------
+
+def test_identity_compressor_is_preconditioned_momentum_sgd():
+    import torch
+    n = 3
+    L = oracle.Layout([4000], n)
+    wl = synth.Workload(name="t", numel=[4000], n=n, warmup_steps=0, steps=5, seed_grads=21)
+    x = synth.host_params(wl, L.D)
+    m = synth.host_normal(L.D, 1e-4, 21, 1)
+    v = np.abs(synth.host_normal(L.D, 1e-6, 21, 2))
+    p = 1.0 / np.sqrt(v[:4000].astype(np.float64) + EPS)
+    # change of variables y = x / p turns the preconditioned step into plain SGD
+    y = torch.nn.Parameter(torch.from_numpy(x[:4000].astype(np.float64) / p))
+    f = lambda a: float(np.float32(a))
+    opt = torch.optim.SGD([y], lr=f(LR), momentum=f(BETA1), dampening=f(BETA1), foreach=False)
+    opt.state[y]["momentum_buffer"] = torch.from_numpy(m[:4000].astype(np.float64)).clone()
+    for t in range(5):
+        g = synth.host_grads(wl, L.D, L.tensor_off, t)
+        oracle.step_uncompressed(L, x, m, v, g, LR, BETA1, EPS)
+        y.grad = torch.from_numpy(g[:, :4000].astype(np.float64).mean(0))
+        opt.step()
+    assert_close_scaled(m[:4000], opt.state[y]["momentum_buffer"].numpy(), 1e-5)
+    assert_close_scaled(x[:4000], y.detach().numpy() * p, 1e-6)
