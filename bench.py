@@ -1,0 +1,222 @@
+#!/usr/bin/env python3
+"""Throughput of 1-bit Adam's compression-stage step on one MI355X.
+
+One step = the whole hot path over one batch of synthetic gradients: the
+worker pass of all n simulated workers (momentum, error compensation, sign
+packing, per-segment scales), the chunk owners' average + recompression, and
+the decompress + preconditioned update.  Inputs are resident in HBM before the
+timed region.  The Adam warm-up steps that produce the frozen variance run
+(untimed) during set-up.  Prints one JSON line.
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBPS = 8000.0  # MI355X HBM3E, published
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def algorithmic_bytes_per_param(n):
+    """Bytes the method must move per parameter, each input read once and each
+    output written once (fp32 state, 1-bit messages):
+      worker pass: m read once for all n workers, then per worker g read,
+                   error state read and written, one sign bit written;
+      server pass: n incoming sign bits, server error state read and written,
+                   one sign bit written;
+      update     : one sign bit read, x read and written, v read, m written."""
+    worker = 4 + n * (4 + 4 + 4 + 1 / 8)
+    server = n / 8 + 4 + 4 + 1 / 8
+    update = 1 / 8 + 4 + 4 + 4 + 4
+    return worker, server, update
+
+
+def cpu_baseline(st, plan, wl, target_s=12.0, max_segments=3):
+    """Times the oracle (single thread) on whole segments of the workload:
+    every worker's pass over the segment, the owner's average and
+    recompression, and the update.  The oracle gets host copies of the
+    segment's device state."""
+    import numpy as np
+
+    import oracle
+    segs = [0, plan.S - 1, plan.S // 2][:max_segments]
+    n = st.n_local
+    done, spent, used = 0, 0.0, []
+    for q in segs:
+        b, e = int(plan.seg_begin[q]), int(plan.seg_end[q])
+        ln = e - b
+        if ln == 0:
+            continue
+        nw = (ln + 63) // 64
+        m = st.m[b:e].cpu().numpy().copy()
+        x = st.x[b:e].cpu().numpy().copy()
+        v = st.v[b:e].cpu().numpy().copy()
+        dbar = st.server_err[b:e].cpu().numpy().copy()
+        g = st.grads[:, b:e].cpu().numpy().copy()
+        delta = st.worker_err[:, b:e].cpu().numpy().copy()
+        wbits = np.zeros((n, nw), np.uint64)
+        wscales = np.zeros(n, np.float32)
+        sbits = np.zeros(nw, np.uint64)
+        z = np.zeros(ln, np.float32)
+        t0 = time.perf_counter()
+        for i in range(n):
+            wscales[i] = oracle.worker_segment(0, ln, wl.beta1, m, g[i], delta[i], wbits[i], z)
+        s = oracle.server_segment(0, ln, n, wbits.reshape(-1), nw, wscales, 1, dbar, sbits, z)
+        oracle.update_segment(0, ln, sbits, s, wl.lr, wl.eps, x, m, v)
+        spent += time.perf_counter() - t0
+        done += ln
+        used.append(q)
+        del g, delta
+        if spent >= target_s:
+            break
+    return {"value": done / spent, "unit": "params/s", "cores": 1, "kind": "oracle",
+            "sample": "%d whole segment(s) %s of %d (%d params, all %d workers' passes, the "
+                      "chunk owner's average and recompression, and the update), %.1f s"
+                      % (len(used), used, plan.S, done, n, spent)}
+
+
+def hbm_copy_probe(dev, nbytes=4 << 30, reps=10):
+    """Achievable HBM bandwidth of a plain device copy (read + write)."""
+    import torch
+    a = torch.empty(nbytes // 4, dtype=torch.float32, device=dev)
+    b = torch.empty_like(a)
+    a.fill_(1.0)
+    b.copy_(a)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        b.copy_(a)
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / reps
+    del a, b
+    return 2 * nbytes / (ms * 1e-3) / 1e9
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="bert_large",
+                    choices=["tiny", "bert_base", "bert_large", "stress"])
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-probe", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print("bench.py measures one GPU: the compressed exchange is simulated in one GPU's "
+              "HBM and no collective is called, so --gpus %d is not supported (use --gpus 1)"
+              % args.gpus, file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    import paper_2102_02888_amd as ob
+    import synth
+
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    wl = synth.get(args.workload)
+    n = wl.n
+    plan = ob.Plan(wl.numel, n)
+    log("workload %s: d=%d D=%d n=%d segments=%d tiles=%d" % (wl.name, plan.d, plan.D, n,
+                                                              plan.S, plan.T))
+    st = ob.State(plan, dev)
+    scale_vec = torch.from_numpy(synth.grad_scale_per_element(wl, plan.D, plan.tensor_off)).to(dev)
+    st.x.copy_(synth.device_params(wl, plan.D, dev))
+
+    # Adam warm-up (untimed set-up): produces m and the frozen variance v.
+    warm_ms = []
+    for t in range(1, wl.warmup_steps + 1):
+        synth.device_grads(wl, plan.D, plan.tensor_off, t, st.grads, scale_vec)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        st.warmup(wl.lr, wl.beta1, wl.beta2, wl.eps, t)
+        e1.record()
+        torch.cuda.synchronize()
+        warm_ms.append(e0.elapsed_time(e1))
+    synth.device_grads(wl, plan.D, plan.tensor_off, wl.warmup_steps + 1, st.grads, scale_vec)
+    torch.cuda.synchronize()
+
+    def one_step(ev=None):
+        if ev:
+            ev[0].record()
+        ob.onebit_worker_compress(plan, st.m, st.grads, st.worker_err, st.worker_bits,
+                                  st.worker_scales, wl.beta1, st.workspace)
+        if ev:
+            ev[1].record()
+        ob.onebit_server_reduce_compress(plan, 0, n, st.worker_bits, st.worker_scales,
+                                         st.server_err, st.server_bits, st.server_scales,
+                                         st.workspace)
+        if ev:
+            ev[2].record()
+        ob.onebit_decompress_update(plan, st.server_bits, st.server_scales, st.x, st.m, st.v,
+                                    wl.lr, wl.eps)
+        if ev:
+            ev[3].record()
+
+    for _ in range(args.warmup):
+        one_step()
+    torch.cuda.synchronize()
+    events = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for k in range(args.steps):
+        one_step(events[k])
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ms_step = wall * 1e3 / args.steps
+    part_ms = [sum(ev[j].elapsed_time(ev[j + 1]) for ev in events) / args.steps
+               for j in range(3)]
+    gpu_step_ms = sum(part_ms)
+
+    bw, bs, bu = algorithmic_bytes_per_param(n)
+    d = plan.d
+    step_bytes = d * (bw + bs + bu)
+    worker_bytes = d * bw
+    achieved = worker_bytes / (part_ms[0] * 1e-3) / 1e9
+    result = {
+        "metric": "compression-phase step params/sec (1-bit Adam, BERT-Large-shaped)",
+        "value": d / (ms_step * 1e-3),
+        "unit": "params/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": wl.name, "d": d, "n_workers": n, "segments": plan.S,
+                   "tensors_shaped": len(wl.grad_scale_ranges or wl.numel),
+                   "adam_warmup_steps": wl.warmup_steps, "description": wl.description},
+        "step_hbm_gbps_algorithmic": step_bytes / (ms_step * 1e-3) / 1e9,
+        "step_frac_of_peak": step_bytes / (ms_step * 1e-3) / 1e9 / HBM_PEAK_GBPS,
+        "bytes_per_param": {"worker": bw, "server": bs, "update": bu},
+        "kernel_ms": {"worker_compress": part_ms[0], "server_reduce_compress": part_ms[1],
+                      "decompress_update": part_ms[2], "sum": gpu_step_ms},
+        "warmup_adam_step_ms": sum(warm_ms[1:]) / max(1, len(warm_ms) - 1) if warm_ms else None,
+        "roofline": {"bound": "hbm", "kernel": "worker_compress (k_worker_pass)",
+                     "achieved": achieved, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                     "frac": achieved / HBM_PEAK_GBPS, "traffic": None},
+    }
+    if not args.no_probe:
+        del events
+        result["hbm_copy_probe_gbps"] = hbm_copy_probe(dev, nbytes=2 << 30)
+    if not args.no_cpu_baseline:
+        log("timing the oracle on sampled segments ...")
+        result["cpu_baseline"] = cpu_baseline(st, plan, wl)
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

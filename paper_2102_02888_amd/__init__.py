@@ -1,0 +1,11 @@
+"""1-bit Adam's compression-stage hot path on AMD MI355X (gfx950).
+
+The kernels and their C ABI live in ``libonebit.so`` (sources in ``csrc/``,
+header ``include/onebit.h``); this package is the Python binding.
+"""
+from .onebit import (  # noqa: F401
+    Plan, State, onebit_decompress_update, onebit_error_materialize, onebit_plan_create,
+    onebit_server_reduce_compress, onebit_step, onebit_warmup_adam_step,
+    onebit_worker_compress,
+)
+from ._native import OnebitError, lib  # noqa: F401

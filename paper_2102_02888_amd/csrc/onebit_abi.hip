@@ -1,0 +1,472 @@
+// C ABI of the 1-bit Adam hot path: plans (layout and tile tables), argument
+// validation, and stream-ordered kernel launches.  See include/onebit.h for
+// the contract of every entry point.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdarg>
+#include <cstdint>
+#include <cstdio>
+#include <cstring>
+#include <new>
+#include <vector>
+
+#include "../../include/onebit.h"
+#include "onebit_internal.h"
+
+using onebit::DeviceTables;
+using onebit::kTileElems;
+using onebit::Tile;
+
+struct onebit_plan_s {
+    int device = 0;
+    int32_t K = 0, n = 0;
+    int64_t d = 0, D = 0, W = 0, S = 0, T = 0;
+    std::vector<int64_t> tensor_off, seg_begin, seg_end;
+    std::vector<int64_t> seg_tile_begin, seg_tile_end;  // [S]
+    std::vector<int64_t> chunk_tile_begin;              // [n+1]
+    std::vector<int64_t> chunk_word_lo, chunk_word_hi;  // [n], words touched by chunk j
+    void *dev_mem = nullptr;                            // one allocation for all tables
+    DeviceTables tb{};
+    size_t workspace_bytes = 0;
+};
+
+namespace {
+
+thread_local char g_last_error[512] = "";
+
+int fail(int status, const char *fmt, ...) __attribute__((format(printf, 2, 3)));
+int fail(int status, const char *fmt, ...)
+{
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(g_last_error, sizeof g_last_error, fmt, ap);
+    va_end(ap);
+    return status;
+}
+
+int hip_fail(hipError_t e, const char *where)
+{
+    return fail(ONEBIT_EHIP, "%s: %s", where, hipGetErrorString(e));
+}
+
+bool aligned(const void *p, size_t a) { return ((uintptr_t)p % a) == 0; }
+
+size_t round_up(size_t a, size_t m) { return (a + m - 1) / m * m; }
+
+// Workspace: per-tile fp64 partial sums, n rows for the workers then one row
+// for the chunk owners.
+size_t worker_partial_offset(const onebit_plan_s *) { return 0; }
+size_t server_partial_offset(const onebit_plan_s *p)
+{
+    return round_up((size_t)p->n * (size_t)p->T * sizeof(double), 256);
+}
+
+int check_plan(const onebit_plan_s *p)
+{
+    if (!p) return fail(ONEBIT_EINVAL, "plan is NULL");
+    int dev = -1;
+    if (hipGetDevice(&dev) != hipSuccess || dev != p->device)
+        return fail(ONEBIT_EINVAL, "plan was created on device %d, current device is %d",
+                    p->device, dev);
+    return ONEBIT_OK;
+}
+
+int check_f32(const void *ptr, const char *name)
+{
+    if (!ptr) return fail(ONEBIT_EINVAL, "%s is NULL", name);
+    if (!aligned(ptr, 16)) return fail(ONEBIT_EALIGN, "%s is not 16-byte aligned", name);
+    return ONEBIT_OK;
+}
+
+int check_u64(const void *ptr, const char *name)
+{
+    if (!ptr) return fail(ONEBIT_EINVAL, "%s is NULL", name);
+    if (!aligned(ptr, 8)) return fail(ONEBIT_EALIGN, "%s is not 8-byte aligned", name);
+    return ONEBIT_OK;
+}
+
+int check_ld(int64_t ld, int64_t need, bool mult4, const char *name)
+{
+    if (ld < need) return fail(ONEBIT_EINVAL, "%s = %lld is below %lld", name, (long long)ld,
+                               (long long)need);
+    if (mult4 && ld % 4 != 0) return fail(ONEBIT_EALIGN, "%s = %lld is not a multiple of 4",
+                                          name, (long long)ld);
+    return ONEBIT_OK;
+}
+
+#define TRY(expr)                         \
+    do {                                  \
+        int _st = (expr);                 \
+        if (_st != ONEBIT_OK) return _st; \
+    } while (0)
+
+#define TRY_HIP(expr, where)                       \
+    do {                                           \
+        hipError_t _e = (expr);                    \
+        if (_e != hipSuccess) return hip_fail(_e, where); \
+    } while (0)
+
+int64_t chunk_len(int64_t d, int32_t n)
+{
+    if (d <= 0) return 0;
+    const int64_t per = (d + (int64_t)n * 64 - 1) / ((int64_t)n * 64);
+    return per * 64;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char *onebit_status_str(int32_t status)
+{
+    switch (status) {
+    case ONEBIT_OK: return "ONEBIT_OK";
+    case ONEBIT_EINVAL: return "ONEBIT_EINVAL";
+    case ONEBIT_EALIGN: return "ONEBIT_EALIGN";
+    case ONEBIT_EHIP: return "ONEBIT_EHIP";
+    case ONEBIT_ENOMEM: return "ONEBIT_ENOMEM";
+    default: return "ONEBIT_UNKNOWN";
+    }
+}
+
+const char *onebit_last_error(void) { return g_last_error; }
+
+int onebit_plan_create(const int64_t *tensor_numel, int32_t num_tensors, int32_t n_workers,
+                       onebit_plan *out)
+{
+    if (!out) return fail(ONEBIT_EINVAL, "out is NULL");
+    *out = nullptr;
+    if (!tensor_numel) return fail(ONEBIT_EINVAL, "tensor_numel is NULL");
+    if (num_tensors < 1) return fail(ONEBIT_EINVAL, "num_tensors < 1");
+    if (n_workers < 1) return fail(ONEBIT_EINVAL, "n_workers < 1");
+    for (int32_t k = 0; k < num_tensors; ++k)
+        if (tensor_numel[k] < 0) return fail(ONEBIT_EINVAL, "tensor_numel[%d] < 0", k);
+
+    onebit_plan_s *p = new (std::nothrow) onebit_plan_s;
+    if (!p) return fail(ONEBIT_ENOMEM, "host allocation failed");
+    hipError_t e = hipGetDevice(&p->device);
+    if (e != hipSuccess) {
+        delete p;
+        return hip_fail(e, "hipGetDevice");
+    }
+    const int32_t K = num_tensors, n = n_workers;
+    p->K = K;
+    p->n = n;
+    p->S = (int64_t)K * n;
+    p->tensor_off.resize(K);
+    p->seg_begin.resize(p->S);
+    p->seg_end.resize(p->S);
+    int64_t off = 0, d = 0;
+    for (int32_t k = 0; k < K; ++k) {
+        const int64_t dk = tensor_numel[k];
+        const int64_t c = chunk_len(dk, n);
+        p->tensor_off[k] = off;
+        for (int32_t j = 0; j < n; ++j) {
+            const int64_t b = std::min<int64_t>((int64_t)j * c, dk);
+            const int64_t en = std::min<int64_t>((int64_t)(j + 1) * c, dk);
+            p->seg_begin[(int64_t)k * n + j] = off + b;
+            p->seg_end[(int64_t)k * n + j] = off + en;
+        }
+        off += (dk + 63) / 64 * 64;
+        d += dk;
+        if (off >= ((int64_t)1 << 40)) {
+            delete p;
+            return fail(ONEBIT_EINVAL, "padded length exceeds 2^40 elements");
+        }
+    }
+    p->d = d;
+    p->D = off;
+    p->W = off / 64;
+
+    // Tiles in chunk-major order, so that the tiles of chunk owner j are one
+    // contiguous range.
+    std::vector<Tile> tiles;
+    p->seg_tile_begin.assign(p->S, 0);
+    p->seg_tile_end.assign(p->S, 0);
+    p->chunk_tile_begin.assign(n + 1, 0);
+    p->chunk_word_lo.assign(n, INT64_MAX);
+    p->chunk_word_hi.assign(n, -1);
+    std::vector<int64_t> seg_len(p->S);
+    for (int32_t j = 0; j < n; ++j) {
+        p->chunk_tile_begin[j] = (int64_t)tiles.size();
+        for (int32_t k = 0; k < K; ++k) {
+            const int64_t q = (int64_t)k * n + j;
+            const int64_t b = p->seg_begin[q], en = p->seg_end[q];
+            seg_len[q] = en - b;
+            p->seg_tile_begin[q] = (int64_t)tiles.size();
+            for (int64_t s = b; s < en; s += kTileElems) {
+                Tile t;
+                t.start = s;
+                t.len = (int32_t)std::min<int64_t>(kTileElems, en - s);
+                t.seg = (int32_t)q;
+                tiles.push_back(t);
+            }
+            p->seg_tile_end[q] = (int64_t)tiles.size();
+            if (en > b) {
+                p->chunk_word_lo[j] = std::min(p->chunk_word_lo[j], b / 64);
+                p->chunk_word_hi[j] = std::max(p->chunk_word_hi[j], (en - 1) / 64);
+            }
+        }
+    }
+    p->chunk_tile_begin[n] = (int64_t)tiles.size();
+    p->T = (int64_t)tiles.size();
+    if (p->S > INT32_MAX) {
+        delete p;
+        return fail(ONEBIT_EINVAL, "too many segments");
+    }
+
+    const size_t tiles_bytes = round_up(tiles.size() * sizeof(Tile) + 1, 256);
+    const size_t seg_bytes = round_up((size_t)p->S * sizeof(int64_t), 256);
+    const size_t total = tiles_bytes + 3 * seg_bytes;
+    e = hipMalloc(&p->dev_mem, total);
+    if (e != hipSuccess) {
+        delete p;
+        return fail(ONEBIT_ENOMEM, "hipMalloc of %zu bytes of plan tables: %s", total,
+                    hipGetErrorString(e));
+    }
+    char *base = (char *)p->dev_mem;
+    Tile *d_tiles = (Tile *)base;
+    int64_t *d_stb = (int64_t *)(base + tiles_bytes);
+    int64_t *d_ste = (int64_t *)(base + tiles_bytes + seg_bytes);
+    int64_t *d_sl = (int64_t *)(base + tiles_bytes + 2 * seg_bytes);
+    std::vector<char> host(total, 0);
+    if (!tiles.empty()) std::memcpy(host.data(), tiles.data(), tiles.size() * sizeof(Tile));
+    std::memcpy(host.data() + tiles_bytes, p->seg_tile_begin.data(), p->S * sizeof(int64_t));
+    std::memcpy(host.data() + tiles_bytes + seg_bytes, p->seg_tile_end.data(),
+                p->S * sizeof(int64_t));
+    std::memcpy(host.data() + tiles_bytes + 2 * seg_bytes, seg_len.data(),
+                p->S * sizeof(int64_t));
+    e = hipMemcpy(p->dev_mem, host.data(), total, hipMemcpyHostToDevice);
+    if (e != hipSuccess) {
+        (void)hipFree(p->dev_mem);
+        delete p;
+        return hip_fail(e, "hipMemcpy of plan tables");
+    }
+    p->tb.tiles = d_tiles;
+    p->tb.seg_tile_begin = d_stb;
+    p->tb.seg_tile_end = d_ste;
+    p->tb.seg_len = d_sl;
+    p->workspace_bytes = server_partial_offset(p) + round_up((size_t)p->T * sizeof(double) + 1, 256);
+    *out = p;
+    return ONEBIT_OK;
+}
+
+int onebit_plan_destroy(onebit_plan p)
+{
+    if (!p) return fail(ONEBIT_EINVAL, "plan is NULL");
+    int prev = -1;
+    (void)hipGetDevice(&prev);
+    if (prev != p->device) (void)hipSetDevice(p->device);
+    hipError_t e = hipFree(p->dev_mem);
+    if (prev >= 0 && prev != p->device) (void)hipSetDevice(prev);
+    delete p;
+    if (e != hipSuccess) return hip_fail(e, "hipFree of plan tables");
+    return ONEBIT_OK;
+}
+
+int onebit_plan_get_info(onebit_plan p, onebit_plan_info *info)
+{
+    if (!p) return fail(ONEBIT_EINVAL, "plan is NULL");
+    if (!info) return fail(ONEBIT_EINVAL, "info is NULL");
+    info->d = p->d;
+    info->padded_len = p->D;
+    info->words = p->W;
+    info->num_tensors = p->K;
+    info->num_segments = p->S;
+    info->num_tiles = p->T;
+    info->n_workers = p->n;
+    info->tile_elems = kTileElems;
+    info->workspace_bytes = p->workspace_bytes;
+    return ONEBIT_OK;
+}
+
+int onebit_plan_get_layout(onebit_plan p, int64_t *tensor_offset, int64_t *seg_begin,
+                           int64_t *seg_end)
+{
+    if (!p) return fail(ONEBIT_EINVAL, "plan is NULL");
+    if (tensor_offset) std::memcpy(tensor_offset, p->tensor_off.data(), p->K * sizeof(int64_t));
+    if (seg_begin) std::memcpy(seg_begin, p->seg_begin.data(), p->S * sizeof(int64_t));
+    if (seg_end) std::memcpy(seg_end, p->seg_end.data(), p->S * sizeof(int64_t));
+    return ONEBIT_OK;
+}
+
+int onebit_warmup_adam_step(onebit_plan p, float *x, float *m, float *v, const float *grads,
+                            int64_t grad_ld, int32_t n_grads, float lr, float beta1,
+                            float beta2, float eps, int32_t bias_correction, int64_t step,
+                            onebit_stream stream)
+{
+    TRY(check_plan(p));
+    TRY(check_f32(x, "x"));
+    TRY(check_f32(m, "m"));
+    TRY(check_f32(v, "v"));
+    TRY(check_f32(grads, "grads"));
+    if (n_grads < 1) return fail(ONEBIT_EINVAL, "n_grads < 1");
+    if (step < 1) return fail(ONEBIT_EINVAL, "step < 1 (steps are 1-based)");
+    TRY(check_ld(grad_ld, p->D, n_grads > 1, "grad_ld"));
+    if (p->T == 0) return ONEBIT_OK;
+    float bc1 = 1.0f, bc2 = 1.0f;
+    if (bias_correction) {
+        bc1 = (float)(1.0 - std::pow((double)beta1, (double)step));
+        bc2 = (float)(1.0 - std::pow((double)beta2, (double)step));
+    }
+    TRY_HIP(onebit::launch_warmup(p->tb, p->T, x, m, v, grads, grad_ld, n_grads, lr, beta1,
+                                  beta2, eps, bias_correction ? 1 : 0, bc1, bc2,
+                                  (hipStream_t)stream),
+            "warm-up kernel launch");
+    return ONEBIT_OK;
+}
+
+int onebit_worker_compress(onebit_plan p, const float *m, const float *grads, int64_t grad_ld,
+                           int32_t n_local, float *worker_err, int64_t err_ld,
+                           uint64_t *worker_bits, int64_t bits_ld, float *worker_scales,
+                           int64_t scales_ld, float beta1, void *workspace,
+                           onebit_stream stream)
+{
+    TRY(check_plan(p));
+    TRY(check_f32(m, "m"));
+    TRY(check_f32(grads, "grads"));
+    TRY(check_f32(worker_err, "worker_err"));
+    TRY(check_u64(worker_bits, "worker_bits"));
+    if (!worker_scales) return fail(ONEBIT_EINVAL, "worker_scales is NULL");
+    if (!aligned(worker_scales, 4)) return fail(ONEBIT_EALIGN, "worker_scales misaligned");
+    if (!workspace) return fail(ONEBIT_EINVAL, "workspace is NULL");
+    if (!aligned(workspace, 256)) return fail(ONEBIT_EALIGN, "workspace is not 256-byte aligned");
+    if (n_local < 1 || n_local > p->n)
+        return fail(ONEBIT_EINVAL, "n_local = %d outside [1, %d]", n_local, p->n);
+    TRY(check_ld(grad_ld, p->D, n_local > 1, "grad_ld"));
+    TRY(check_ld(err_ld, p->D, n_local > 1, "err_ld"));
+    TRY(check_ld(bits_ld, p->W, false, "bits_ld"));
+    TRY(check_ld(scales_ld, p->S, false, "scales_ld"));
+    if (p->T == 0) return ONEBIT_OK;
+    double *part = (double *)((char *)workspace + worker_partial_offset(p));
+    hipStream_t s = (hipStream_t)stream;
+    TRY_HIP(onebit::launch_worker_pass(p->tb, p->T, m, grads, grad_ld, worker_err, err_ld,
+                                       worker_scales, scales_ld, worker_bits, bits_ld, part,
+                                       n_local, beta1, s),
+            "worker kernel launch");
+    TRY_HIP(onebit::launch_worker_finalize(p->tb, p->S, n_local, part, p->T, worker_scales,
+                                           scales_ld, s),
+            "worker scale kernel launch");
+    return ONEBIT_OK;
+}
+
+int onebit_server_reduce_compress(onebit_plan p, int32_t server_begin, int32_t server_end,
+                                  const uint64_t *worker_bits, int64_t bits_ld,
+                                  int64_t bits_word_base, const float *worker_scales,
+                                  int64_t scales_ld, int64_t scales_seg_base, float *server_err,
+                                  uint64_t *server_bits, float *server_scales, void *workspace,
+                                  onebit_stream stream)
+{
+    TRY(check_plan(p));
+    TRY(check_u64(worker_bits, "worker_bits"));
+    if (!worker_scales) return fail(ONEBIT_EINVAL, "worker_scales is NULL");
+    if (!aligned(worker_scales, 4)) return fail(ONEBIT_EALIGN, "worker_scales misaligned");
+    TRY(check_f32(server_err, "server_err"));
+    TRY(check_u64(server_bits, "server_bits"));
+    if (!server_scales) return fail(ONEBIT_EINVAL, "server_scales is NULL");
+    if (!aligned(server_scales, 4)) return fail(ONEBIT_EALIGN, "server_scales misaligned");
+    if (!workspace) return fail(ONEBIT_EINVAL, "workspace is NULL");
+    if (!aligned(workspace, 256)) return fail(ONEBIT_EALIGN, "workspace is not 256-byte aligned");
+    if (server_begin < 0 || server_end > p->n || server_begin >= server_end)
+        return fail(ONEBIT_EINVAL, "chunk range [%d, %d) is empty or outside [0, %d)",
+                    server_begin, server_end, p->n);
+    // Incoming words and scales must cover every owned segment.
+    int64_t wlo = INT64_MAX, whi = -1;
+    for (int32_t j = server_begin; j < server_end; ++j) {
+        if (p->chunk_word_hi[j] < 0) continue;
+        wlo = std::min(wlo, p->chunk_word_lo[j]);
+        whi = std::max(whi, p->chunk_word_hi[j]);
+    }
+    if (whi >= 0) {
+        if (bits_word_base < 0 || bits_word_base > wlo)
+            return fail(ONEBIT_EINVAL, "bits_word_base %lld is not in [0, %lld]",
+                        (long long)bits_word_base, (long long)wlo);
+        TRY(check_ld(bits_ld, whi + 1 - bits_word_base, false, "bits_ld"));
+    }
+    const int64_t qlo = server_begin, qhi = (int64_t)(p->K - 1) * p->n + (server_end - 1);
+    if (scales_seg_base < 0 || scales_seg_base > qlo)
+        return fail(ONEBIT_EINVAL, "scales_seg_base %lld is not in [0, %lld]",
+                    (long long)scales_seg_base, (long long)qlo);
+    TRY(check_ld(scales_ld, qhi + 1 - scales_seg_base, false, "scales_ld"));
+    const int64_t tb = p->chunk_tile_begin[server_begin];
+    const int64_t tc = p->chunk_tile_begin[server_end] - tb;
+    double *part = (double *)((char *)workspace + server_partial_offset(p));
+    hipStream_t s = (hipStream_t)stream;
+    if (tc > 0)
+        TRY_HIP(onebit::launch_server_pass(p->tb, tb, tc, p->n, worker_bits, bits_ld,
+                                           bits_word_base, worker_scales, scales_ld,
+                                           scales_seg_base, server_err, server_scales,
+                                           server_bits, part, s),
+                "server kernel launch");
+    TRY_HIP(onebit::launch_server_finalize(p->tb, p->K, p->n, server_begin, server_end, part,
+                                           server_scales, s),
+            "server scale kernel launch");
+    return ONEBIT_OK;
+}
+
+int onebit_decompress_update(onebit_plan p, const uint64_t *server_bits,
+                             const float *server_scales, float *x, float *m_out,
+                             const float *v_frozen, float lr, float eps, onebit_stream stream)
+{
+    TRY(check_plan(p));
+    TRY(check_u64(server_bits, "server_bits"));
+    if (!server_scales) return fail(ONEBIT_EINVAL, "server_scales is NULL");
+    if (!aligned(server_scales, 4)) return fail(ONEBIT_EALIGN, "server_scales misaligned");
+    TRY(check_f32(x, "x"));
+    if (m_out) TRY(check_f32(m_out, "m_out"));
+    TRY(check_f32(v_frozen, "v_frozen"));
+    if (p->T == 0) return ONEBIT_OK;
+    TRY_HIP(onebit::launch_update(p->tb, p->T, server_bits, server_scales, x, m_out, v_frozen,
+                                  lr, eps, (hipStream_t)stream),
+            "update kernel launch");
+    return ONEBIT_OK;
+}
+
+int onebit_step(onebit_plan p, float *x, float *m, const float *v_frozen, const float *grads,
+                int64_t grad_ld, float *worker_err, int64_t err_ld, float *server_err,
+                uint64_t *worker_bits, float *worker_scales, uint64_t *server_bits,
+                float *server_scales, float lr, float beta1, float eps, void *workspace,
+                onebit_stream stream)
+{
+    TRY(check_plan(p));
+    // Validate everything before the first launch so that an error writes nothing.
+    TRY(check_f32(x, "x"));
+    TRY(check_f32(m, "m"));
+    TRY(check_f32(v_frozen, "v_frozen"));
+    TRY(check_f32(server_err, "server_err"));
+    TRY(check_u64(server_bits, "server_bits"));
+    if (!server_scales) return fail(ONEBIT_EINVAL, "server_scales is NULL");
+    TRY(onebit_worker_compress(p, m, grads, grad_ld, p->n, worker_err, err_ld, worker_bits,
+                               p->W, worker_scales, p->S, beta1, workspace, stream));
+    TRY(onebit_server_reduce_compress(p, 0, p->n, worker_bits, p->W, 0, worker_scales, p->S, 0,
+                                      server_err, server_bits, server_scales, workspace,
+                                      stream));
+    return onebit_decompress_update(p, server_bits, server_scales, x, m, v_frozen, lr, eps,
+                                    stream);
+}
+
+int onebit_error_materialize(onebit_plan p, const float *err_state, int64_t err_ld,
+                             const float *scales, int64_t scales_ld, int32_t rows,
+                             float *delta_out, int64_t out_ld, onebit_stream stream)
+{
+    TRY(check_plan(p));
+    TRY(check_f32(err_state, "err_state"));
+    TRY(check_f32(delta_out, "delta_out"));
+    if (!scales) return fail(ONEBIT_EINVAL, "scales is NULL");
+    if (!aligned(scales, 4)) return fail(ONEBIT_EALIGN, "scales misaligned");
+    if (rows < 1) return fail(ONEBIT_EINVAL, "rows < 1");
+    TRY(check_ld(err_ld, p->D, rows > 1, "err_ld"));
+    TRY(check_ld(out_ld, p->D, rows > 1, "out_ld"));
+    TRY(check_ld(scales_ld, rows > 1 ? p->S : 0, false, "scales_ld"));
+    if (delta_out == err_state && out_ld != err_ld)
+        return fail(ONEBIT_EINVAL, "in-place materialize needs out_ld == err_ld");
+    if (p->T == 0) return ONEBIT_OK;
+    TRY_HIP(onebit::launch_materialize(p->tb, p->T, rows, err_state, err_ld, scales, scales_ld,
+                                       delta_out, out_ld, (hipStream_t)stream),
+            "materialize kernel launch");
+    return ONEBIT_OK;
+}
+
+}  // extern "C"

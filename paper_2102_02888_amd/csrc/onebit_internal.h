@@ -1,0 +1,68 @@
+// Internal interface between the C-ABI layer and the gfx950 kernels.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace onebit {
+
+// A unit of work: up to kTileElems consecutive elements of one segment,
+// starting on a 64-element (one sign word) boundary.  One wavefront owns one
+// tile; a 256-thread workgroup runs four consecutive tiles.
+struct Tile {
+    int64_t start;  // first flat element (multiple of 64)
+    int32_t len;    // elements in the tile, 1..kTileElems
+    int32_t seg;    // segment q = k*n + j
+};
+
+constexpr int kWave = 64;
+constexpr int kWavesPerBlock = 4;
+constexpr int kBlock = kWave * kWavesPerBlock;
+constexpr int kSubBlocks = 4;                       // float4 loads per lane per array
+constexpr int kTileElems = kWave * 4 * kSubBlocks;  // 1024 elements = 16 sign words
+constexpr int kTileWords = kTileElems / 64;
+constexpr int kServerRowBatch = 32;                 // worker rows staged in LDS at a time
+
+// Device-side layout tables owned by a plan.
+struct DeviceTables {
+    const Tile *tiles;             // [T], chunk-major order
+    const int64_t *seg_tile_begin; // [S]
+    const int64_t *seg_tile_end;   // [S]
+    const int64_t *seg_len;        // [S]
+};
+
+hipError_t launch_warmup(const DeviceTables &tb, int64_t num_tiles, float *x, float *m,
+                         float *v, const float *g, int64_t g_ld, int n_grads, float lr,
+                         float beta1, float beta2, float eps, int use_bc, float bc1,
+                         float bc2, hipStream_t s);
+
+hipError_t launch_worker_pass(const DeviceTables &tb, int64_t num_tiles, const float *m,
+                              const float *g, int64_t g_ld, float *err, int64_t err_ld,
+                              const float *scales, int64_t scales_ld, uint64_t *bits,
+                              int64_t bits_ld, double *partial, int n_local, float beta1,
+                              hipStream_t s);
+
+// Worker scales: rows x S pairs; scale[i*scales_ld + q] from partial[i*part_ld + tiles of q].
+hipError_t launch_worker_finalize(const DeviceTables &tb, int64_t num_segments, int rows,
+                                  const double *partial, int64_t part_ld, float *scales,
+                                  int64_t scales_ld, hipStream_t s);
+
+hipError_t launch_server_pass(const DeviceTables &tb, int64_t tile_begin, int64_t tile_count,
+                              int n, const uint64_t *wbits, int64_t bits_ld,
+                              int64_t bits_word_base, const float *wscales, int64_t scales_ld,
+                              int64_t scales_seg_base, float *serr, float *sscales,
+                              uint64_t *sbits, double *partial, hipStream_t s);
+
+// Server scales for segments k*n + j, j in [jb, je), all k < K.
+hipError_t launch_server_finalize(const DeviceTables &tb, int K, int n, int jb, int je,
+                                  const double *partial, float *sscales, hipStream_t s);
+
+hipError_t launch_update(const DeviceTables &tb, int64_t num_tiles, const uint64_t *sbits,
+                         const float *sscales, float *x, float *m_out, const float *v,
+                         float lr, float eps, hipStream_t s);
+
+hipError_t launch_materialize(const DeviceTables &tb, int64_t num_tiles, int rows,
+                              const float *err, int64_t err_ld, const float *scales,
+                              int64_t scales_ld, float *out, int64_t out_ld, hipStream_t s);
+
+}  // namespace onebit

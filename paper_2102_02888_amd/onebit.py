@@ -1,0 +1,217 @@
+"""Python binding of the C ABI in include/onebit.h.
+
+Argument marshalling only: every step of the method runs in the gfx950
+kernels of libonebit.so.  Tensors must live on the plan's GPU; float buffers
+are torch.float32, sign-bit buffers torch.int64 (the bytes of uint64 words).
+Row-major 2-D buffers pass their row stride as the leading dimension.  Calls
+are asynchronous on torch's current stream unless a stream is given.
+"""
+import ctypes
+
+import numpy as np
+import torch
+
+from ._native import PlanInfo, call, lib
+
+__all__ = [
+    "Plan", "onebit_plan_create", "onebit_warmup_adam_step", "onebit_worker_compress",
+    "onebit_server_reduce_compress", "onebit_decompress_update", "onebit_step",
+    "onebit_error_materialize", "State",
+]
+
+
+def _stream(stream):
+    s = torch.cuda.current_stream() if stream is None else stream
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+def _ptr(t, dtype, name):
+    if t is None:
+        return None
+    if not isinstance(t, torch.Tensor):
+        raise TypeError("%s must be a torch.Tensor" % name)
+    if t.dtype != dtype:
+        raise TypeError("%s must be %s, got %s" % (name, dtype, t.dtype))
+    if t.device.type != "cuda":
+        raise ValueError("%s must be a GPU tensor" % name)
+    if t.dim() >= 1 and t.stride(-1) != 1:
+        raise ValueError("%s must have unit stride in its last dimension" % name)
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def _ld(t):
+    return t.stride(0) if t.dim() == 2 else t.numel()
+
+
+def _rows(t):
+    return t.shape[0] if t.dim() == 2 else 1
+
+
+class Plan:
+    """Layout of K tensors cut into n chunks, with its device tile tables."""
+
+    def __init__(self, tensor_numel, n_workers):
+        numel = np.ascontiguousarray(np.asarray(tensor_numel, dtype=np.int64))
+        h = ctypes.c_void_p()
+        call("onebit_plan_create", numel.ctypes.data_as(ctypes.c_void_p), len(numel),
+             int(n_workers), ctypes.byref(h))
+        self._h = h
+        info = PlanInfo()
+        call("onebit_plan_get_info", h, ctypes.byref(info))
+        self.d = info.d
+        self.D = info.padded_len
+        self.W = info.words
+        self.K = info.num_tensors
+        self.S = info.num_segments
+        self.T = info.num_tiles
+        self.n = info.n_workers
+        self.tile_elems = info.tile_elems
+        self.workspace_bytes = info.workspace_bytes
+        self.tensor_off = np.zeros(self.K, np.int64)
+        self.seg_begin = np.zeros(self.S, np.int64)
+        self.seg_end = np.zeros(self.S, np.int64)
+        call("onebit_plan_get_layout", h, self.tensor_off.ctypes.data_as(ctypes.c_void_p),
+             self.seg_begin.ctypes.data_as(ctypes.c_void_p),
+             self.seg_end.ctypes.data_as(ctypes.c_void_p))
+        self.numel = numel
+
+    @property
+    def handle(self):
+        if self._h is None:
+            raise ValueError("plan is closed")
+        return self._h
+
+    def workspace(self, device):
+        nbytes = max(self.workspace_bytes, 256)
+        return torch.empty(nbytes // 8 + 32, dtype=torch.float64, device=device)
+
+    def close(self):
+        if self._h is not None:
+            call("onebit_plan_destroy", self._h)
+            self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+def onebit_plan_create(tensor_numel, n_workers):
+    return Plan(tensor_numel, n_workers)
+
+
+def onebit_warmup_adam_step(plan, x, m, v, grads, lr, beta1, beta2, eps,
+                            bias_correction, step, n_grads=None, stream=None):
+    n = _rows(grads) if n_grads is None else n_grads
+    if _rows(grads) < n:
+        raise ValueError("grads has fewer than %d rows" % n)
+    call("onebit_warmup_adam_step", plan.handle, _ptr(x, torch.float32, "x"),
+         _ptr(m, torch.float32, "m"), _ptr(v, torch.float32, "v"),
+         _ptr(grads, torch.float32, "grads"), _ld(grads), n, lr, beta1, beta2, eps,
+         int(bias_correction), int(step), _stream(stream))
+
+
+def onebit_worker_compress(plan, m, grads, worker_err, worker_bits, worker_scales, beta1,
+                           workspace, n_local=None, stream=None):
+    n = _rows(grads) if n_local is None else n_local
+    if min(_rows(grads), _rows(worker_err), _rows(worker_bits), _rows(worker_scales)) < n:
+        raise ValueError("grads, worker_err, worker_bits, worker_scales need %d rows" % n)
+    call("onebit_worker_compress", plan.handle, _ptr(m, torch.float32, "m"),
+         _ptr(grads, torch.float32, "grads"), _ld(grads), n,
+         _ptr(worker_err, torch.float32, "worker_err"), _ld(worker_err),
+         _ptr(worker_bits, torch.int64, "worker_bits"), _ld(worker_bits),
+         _ptr(worker_scales, torch.float32, "worker_scales"), _ld(worker_scales),
+         beta1, _ptr(workspace, torch.float64, "workspace"), _stream(stream))
+
+
+def onebit_server_reduce_compress(plan, server_begin, server_end, worker_bits, worker_scales,
+                                  server_err, server_bits, server_scales, workspace,
+                                  bits_word_base=0, scales_seg_base=0, bits_ld=None,
+                                  scales_ld=None, stream=None):
+    if _rows(worker_bits) < plan.n or (scales_ld is None and _rows(worker_scales) < plan.n):
+        raise ValueError("incoming bits and scales need one row per worker (%d)" % plan.n)
+    if scales_ld is not None and worker_scales.numel() < (plan.n - 1) * scales_ld + 1:
+        raise ValueError("worker_scales too small for %d rows of stride %d" % (plan.n, scales_ld))
+    call("onebit_server_reduce_compress", plan.handle, int(server_begin), int(server_end),
+         _ptr(worker_bits, torch.int64, "worker_bits"),
+         _ld(worker_bits) if bits_ld is None else bits_ld, int(bits_word_base),
+         _ptr(worker_scales, torch.float32, "worker_scales"),
+         _ld(worker_scales) if scales_ld is None else scales_ld, int(scales_seg_base),
+         _ptr(server_err, torch.float32, "server_err"),
+         _ptr(server_bits, torch.int64, "server_bits"),
+         _ptr(server_scales, torch.float32, "server_scales"),
+         _ptr(workspace, torch.float64, "workspace"), _stream(stream))
+
+
+def onebit_decompress_update(plan, server_bits, server_scales, x, m_out, v_frozen, lr, eps,
+                             stream=None):
+    call("onebit_decompress_update", plan.handle, _ptr(server_bits, torch.int64, "server_bits"),
+         _ptr(server_scales, torch.float32, "server_scales"), _ptr(x, torch.float32, "x"),
+         _ptr(m_out, torch.float32, "m_out"), _ptr(v_frozen, torch.float32, "v_frozen"),
+         lr, eps, _stream(stream))
+
+
+def onebit_step(plan, x, m, v_frozen, grads, worker_err, server_err, worker_bits,
+                worker_scales, server_bits, server_scales, lr, beta1, eps, workspace,
+                stream=None):
+    call("onebit_step", plan.handle, _ptr(x, torch.float32, "x"), _ptr(m, torch.float32, "m"),
+         _ptr(v_frozen, torch.float32, "v_frozen"), _ptr(grads, torch.float32, "grads"),
+         _ld(grads), _ptr(worker_err, torch.float32, "worker_err"), _ld(worker_err),
+         _ptr(server_err, torch.float32, "server_err"),
+         _ptr(worker_bits, torch.int64, "worker_bits"),
+         _ptr(worker_scales, torch.float32, "worker_scales"),
+         _ptr(server_bits, torch.int64, "server_bits"),
+         _ptr(server_scales, torch.float32, "server_scales"), lr, beta1, eps,
+         _ptr(workspace, torch.float64, "workspace"), _stream(stream))
+
+
+def onebit_error_materialize(plan, err_state, scales, delta_out, rows=None, stream=None):
+    r = _rows(err_state) if rows is None else rows
+    if _rows(scales) < r or _rows(delta_out) < r or _rows(err_state) < r:
+        raise ValueError("err_state, scales and delta_out need %d rows" % r)
+    call("onebit_error_materialize", plan.handle, _ptr(err_state, torch.float32, "err_state"),
+         _ld(err_state), _ptr(scales, torch.float32, "scales"), _ld(scales), r,
+         _ptr(delta_out, torch.float32, "delta_out"), _ld(delta_out), _stream(stream))
+
+
+class State:
+    """Device buffers of one compression-stage run with n_local simulated
+    workers (all zero-initialised except x, m, v which the caller fills)."""
+
+    def __init__(self, plan, device, n_local=None, grad_rows=None):
+        n = plan.n if n_local is None else n_local
+        D, W, S = plan.D, plan.W, plan.S
+        f = dict(dtype=torch.float32, device=device)
+        self.plan = plan
+        self.n_local = n
+        self.x = torch.zeros(D, **f)
+        self.m = torch.zeros(D, **f)
+        self.v = torch.zeros(D, **f)
+        self.grads = torch.zeros((n if grad_rows is None else grad_rows, D), **f)
+        self.worker_err = torch.zeros((n, D), **f)
+        self.worker_bits = torch.zeros((n, W), dtype=torch.int64, device=device)
+        self.worker_scales = torch.zeros((n, S), **f)
+        self.server_err = torch.zeros(D, **f)
+        self.server_bits = torch.zeros(W, dtype=torch.int64, device=device)
+        self.server_scales = torch.zeros(S, **f)
+        self.workspace = plan.workspace(device)
+
+    def warmup(self, lr, beta1, beta2, eps, step, bias_correction=0, stream=None):
+        onebit_warmup_adam_step(self.plan, self.x, self.m, self.v, self.grads, lr, beta1,
+                                beta2, eps, bias_correction, step, stream=stream)
+
+    def step(self, lr, beta1, eps, stream=None):
+        onebit_step(self.plan, self.x, self.m, self.v, self.grads, self.worker_err,
+                    self.server_err, self.worker_bits, self.worker_scales, self.server_bits,
+                    self.server_scales, lr, beta1, eps, self.workspace, stream=stream)
+
+    def worker_delta(self):
+        out = torch.zeros_like(self.worker_err)
+        onebit_error_materialize(self.plan, self.worker_err, self.worker_scales, out)
+        return out
+
+    def server_delta(self):
+        out = torch.zeros_like(self.server_err)
+        onebit_error_materialize(self.plan, self.server_err, self.server_scales, out, rows=1)
+        return out
