@@ -155,6 +155,8 @@ def onebit_decompress_update(plan, server_bits, server_scales, x, m_out, v_froze
 def onebit_step(plan, x, m, v_frozen, grads, worker_err, server_err, worker_bits,
                 worker_scales, server_bits, server_scales, lr, beta1, eps, workspace,
                 stream=None):
+    if min(_rows(grads), _rows(worker_err), _rows(worker_bits), _rows(worker_scales)) < plan.n:
+        raise ValueError("grads, worker_err, worker_bits, worker_scales need %d rows" % plan.n)
     call("onebit_step", plan.handle, _ptr(x, torch.float32, "x"), _ptr(m, torch.float32, "m"),
          _ptr(v_frozen, torch.float32, "v_frozen"), _ptr(grads, torch.float32, "grads"),
          _ld(grads), _ptr(worker_err, torch.float32, "worker_err"), _ld(worker_err),
