@@ -23,6 +23,7 @@ struct onebit_plan_s {
     int device = 0;
     int32_t K = 0, n = 0;
     int64_t d = 0, D = 0, W = 0, S = 0, T = 0;
+    int64_t max_seg_tiles = 0;                          // most tiles in one segment
     std::vector<int64_t> tensor_off, seg_begin, seg_end;
     std::vector<int64_t> seg_tile_begin, seg_tile_end;  // [S]
     std::vector<int64_t> chunk_tile_begin;              // [n+1]
@@ -204,6 +205,7 @@ int onebit_plan_create(const int64_t *tensor_numel, int32_t num_tensors, int32_t
                 tiles.push_back(t);
             }
             p->seg_tile_end[q] = (int64_t)tiles.size();
+            p->max_seg_tiles = std::max(p->max_seg_tiles, p->seg_tile_end[q] - p->seg_tile_begin[q]);
             if (en > b) {
                 p->chunk_word_lo[j] = std::min(p->chunk_word_lo[j], b / 64);
                 p->chunk_word_hi[j] = std::max(p->chunk_word_hi[j], (en - 1) / 64);
@@ -346,8 +348,8 @@ int onebit_worker_compress(onebit_plan p, const float *m, const float *grads, in
                                        worker_scales, scales_ld, worker_bits, bits_ld, part,
                                        n_local, beta1, s),
             "worker kernel launch");
-    TRY_HIP(onebit::launch_worker_finalize(p->tb, p->S, n_local, part, p->T, worker_scales,
-                                           scales_ld, s),
+    TRY_HIP(onebit::launch_finalize(p->tb, p->max_seg_tiles, (int64_t)n_local * p->S, p->S, 0,
+                                    p->n, 0, 0, part, p->T, worker_scales, scales_ld, s),
             "worker scale kernel launch");
     return ONEBIT_OK;
 }
@@ -400,8 +402,9 @@ int onebit_server_reduce_compress(onebit_plan p, int32_t server_begin, int32_t s
                                            scales_seg_base, server_err, server_scales,
                                            server_bits, part, s),
                 "server kernel launch");
-    TRY_HIP(onebit::launch_server_finalize(p->tb, p->K, p->n, server_begin, server_end, part,
-                                           server_scales, s),
+    TRY_HIP(onebit::launch_finalize(p->tb, p->max_seg_tiles,
+                                    (int64_t)p->K * (server_end - server_begin), p->S, 1, p->n,
+                                    server_begin, server_end, part, p->T, server_scales, 0, s),
             "server scale kernel launch");
     return ONEBIT_OK;
 }

@@ -42,20 +42,21 @@ hipError_t launch_worker_pass(const DeviceTables &tb, int64_t num_tiles, const f
                               int64_t bits_ld, double *partial, int n_local, float beta1,
                               hipStream_t s);
 
-// Worker scales: rows x S pairs; scale[i*scales_ld + q] from partial[i*part_ld + tiles of q].
-hipError_t launch_worker_finalize(const DeviceTables &tb, int64_t num_segments, int rows,
-                                  const double *partial, int64_t part_ld, float *scales,
-                                  int64_t scales_ld, hipStream_t s);
+// Segment scales from per-tile partial sums.  Worker form (server_form = 0):
+// num_pairs = rows * num_segments, scale[i*scales_ld + q] from
+// partial[i*part_ld + tiles of q].  Server form: num_pairs = K * (je - jb),
+// segments k*n + j for j in [jb, je), one row.  max_seg_tiles picks a wave
+// or a block per pair.
+hipError_t launch_finalize(const DeviceTables &tb, int64_t max_seg_tiles, int64_t num_pairs,
+                           int64_t num_segments, int server_form, int n, int jb, int je,
+                           const double *partial, int64_t part_ld, float *scales,
+                           int64_t scales_ld, hipStream_t s);
 
 hipError_t launch_server_pass(const DeviceTables &tb, int64_t tile_begin, int64_t tile_count,
                               int n, const uint64_t *wbits, int64_t bits_ld,
                               int64_t bits_word_base, const float *wscales, int64_t scales_ld,
                               int64_t scales_seg_base, float *serr, float *sscales,
                               uint64_t *sbits, double *partial, hipStream_t s);
-
-// Server scales for segments k*n + j, j in [jb, je), all k < K.
-hipError_t launch_server_finalize(const DeviceTables &tb, int K, int n, int jb, int je,
-                                  const double *partial, float *sscales, hipStream_t s);
 
 hipError_t launch_update(const DeviceTables &tb, int64_t num_tiles, const uint64_t *sbits,
                          const float *sscales, float *x, float *m_out, const float *v,

@@ -21,38 +21,35 @@
 namespace onebit {
 namespace {
 
-__device__ __forceinline__ float4 load4(const float *__restrict__ p, int li, int len)
+// Four consecutive floats.  The native vector type lets the non-temporal
+// builtins take it; every stream here is touched once per launch, so loads
+// and stores are non-temporal (they do not displace other data in the caches
+// on the way to HBM).
+typedef float v4f __attribute__((ext_vector_type(4)));
+
+// Loads elements li..li+3 of p; FULL means the whole tile is in range (a
+// wave-uniform fact), otherwise lanes past len read zeros.
+template <bool FULL>
+__device__ __forceinline__ v4f ld4(const float *__restrict__ p, int li, int len)
 {
-    if (li + 4 <= len) return *reinterpret_cast<const float4 *>(p + li);
-    float4 r = make_float4(0.f, 0.f, 0.f, 0.f);
+    if (FULL || li + 4 <= len) return __builtin_nontemporal_load((const v4f *)(p + li));
+    v4f r = {0.f, 0.f, 0.f, 0.f};
     if (li < len) r.x = p[li];
     if (li + 1 < len) r.y = p[li + 1];
     if (li + 2 < len) r.z = p[li + 2];
     return r;
 }
 
-__device__ __forceinline__ void store4(float *__restrict__ p, int li, int len, float4 v)
+template <bool FULL>
+__device__ __forceinline__ void st4(float *__restrict__ p, int li, int len, v4f v)
 {
-    if (li + 4 <= len) {
-        *reinterpret_cast<float4 *>(p + li) = v;
+    if (FULL || li + 4 <= len) {
+        __builtin_nontemporal_store(v, (v4f *)(p + li));
         return;
     }
     if (li < len) p[li] = v.x;
     if (li + 1 < len) p[li + 1] = v.y;
     if (li + 2 < len) p[li + 2] = v.z;
-}
-
-__device__ __forceinline__ float comp(const float4 &v, int c)
-{
-    return c == 0 ? v.x : c == 1 ? v.y : c == 2 ? v.z : v.w;
-}
-
-__device__ __forceinline__ void set_comp(float4 &v, int c, float a)
-{
-    if (c == 0) v.x = a;
-    else if (c == 1) v.y = a;
-    else if (c == 2) v.z = a;
-    else v.w = a;
 }
 
 // OR of a 32-bit value over the 16 lanes of each DPP row (every lane of the
@@ -93,6 +90,56 @@ __device__ __forceinline__ float error_of(float z, float s) { return z >= 0.f ? 
 // ---------------------------------------------------------------------------
 // Warm-up Adam (eq. (alg:v)) on the average of n_grads gradient rows.
 // ---------------------------------------------------------------------------
+template <bool FULL>
+__device__ __forceinline__ void warmup_tile(const Tile &tile, int lane, float *__restrict__ x,
+                                            float *__restrict__ m, float *__restrict__ v,
+                                            const float *__restrict__ g, int64_t g_ld,
+                                            int n_grads, float lr, float beta1, float omb1,
+                                            float beta2, float omb2, float eps, int use_bc,
+                                            float bc1, float bc2)
+{
+    const int len = tile.len;
+    const int64_t base = tile.start;
+    const double dn = (double)n_grads;
+#pragma unroll
+    for (int b = 0; b < kSubBlocks; ++b) {
+        const int li = b * (kWave * 4) + 4 * lane;
+        if (!FULL && li >= len) break;
+        double sum[4] = {0.0, 0.0, 0.0, 0.0};
+        for (int i = 0; i < n_grads; ++i) {
+            const v4f gv = ld4<FULL>(g + (int64_t)i * g_ld + base, li, len);
+#pragma unroll
+            for (int c = 0; c < 4; ++c) sum[c] += (double)gv[c];
+        }
+        v4f xv = ld4<FULL>(x + base, li, len);
+        v4f mv = ld4<FULL>(m + base, li, len);
+        v4f vv = ld4<FULL>(v + base, li, len);
+#pragma unroll
+        for (int c = 0; c < 4; ++c) {
+            const float gbar = (float)(sum[c] / dn);
+            float mn = beta1 * mv[c];
+            mn = mn + omb1 * gbar;
+            const float gsq = gbar * gbar;
+            float vn = beta2 * vv[c];
+            vn = vn + omb2 * gsq;
+            float mh = mn, vh = vn;
+            if (use_bc) {
+                mh = mn / bc1;
+                vh = vn / bc2;
+            }
+            const float denom = __builtin_sqrtf(vh) + eps;
+            const float ratio = mh / denom;
+            const float step = lr * ratio;
+            xv[c] = xv[c] - step;
+            mv[c] = mn;
+            vv[c] = vn;
+        }
+        st4<FULL>(x + base, li, len, xv);
+        st4<FULL>(m + base, li, len, mv);
+        st4<FULL>(v + base, li, len, vv);
+    }
+}
+
 __global__ __launch_bounds__(kBlock) void k_warmup(
     const Tile *__restrict__ tiles, int64_t num_tiles, float *__restrict__ x,
     float *__restrict__ m, float *__restrict__ v, const float *__restrict__ g, int64_t g_ld,
@@ -103,46 +150,12 @@ __global__ __launch_bounds__(kBlock) void k_warmup(
     const int64_t t = (int64_t)blockIdx.x * kWavesPerBlock + (threadIdx.x >> 6);
     if (t >= num_tiles) return;
     const Tile tile = tiles[t];
-    const int len = tile.len;
-    const int64_t base = tile.start;
-    const double inv_n_div = (double)n_grads;
-#pragma unroll
-    for (int b = 0; b < kSubBlocks; ++b) {
-        const int li = b * (kWave * 4) + 4 * lane;
-        if (li >= len) break;
-        double sum[4] = {0.0, 0.0, 0.0, 0.0};
-        for (int i = 0; i < n_grads; ++i) {
-            const float4 gv = load4(g + (int64_t)i * g_ld + base, li, len);
-#pragma unroll
-            for (int c = 0; c < 4; ++c) sum[c] += (double)comp(gv, c);
-        }
-        float4 xv = load4(x + base, li, len);
-        float4 mv = load4(m + base, li, len);
-        float4 vv = load4(v + base, li, len);
-#pragma unroll
-        for (int c = 0; c < 4; ++c) {
-            const float gbar = (float)(sum[c] / inv_n_div);
-            float mn = beta1 * comp(mv, c);
-            mn = mn + omb1 * gbar;
-            const float gsq = gbar * gbar;
-            float vn = beta2 * comp(vv, c);
-            vn = vn + omb2 * gsq;
-            float mh = mn, vh = vn;
-            if (use_bc) {
-                mh = mn / bc1;
-                vh = vn / bc2;
-            }
-            const float denom = __builtin_sqrtf(vh) + eps;
-            const float ratio = mh / denom;
-            const float step = lr * ratio;
-            set_comp(xv, c, comp(xv, c) - step);
-            set_comp(mv, c, mn);
-            set_comp(vv, c, vn);
-        }
-        store4(x + base, li, len, xv);
-        store4(m + base, li, len, mv);
-        store4(v + base, li, len, vv);
-    }
+    if (tile.len == kTileElems)
+        warmup_tile<true>(tile, lane, x, m, v, g, g_ld, n_grads, lr, beta1, omb1, beta2, omb2,
+                          eps, use_bc, bc1, bc2);
+    else
+        warmup_tile<false>(tile, lane, x, m, v, g, g_ld, n_grads, lr, beta1, omb1, beta2, omb2,
+                           eps, use_bc, bc1, bc2);
 }
 
 // ---------------------------------------------------------------------------
@@ -150,6 +163,62 @@ __global__ __launch_bounds__(kBlock) void k_warmup(
 // sign words of z_i, per-tile partial sum of z_i^2, and z_i written back as the
 // new compensated error state.  m is read once per tile for all workers.
 // ---------------------------------------------------------------------------
+template <bool FULL>
+__device__ __forceinline__ void worker_tile(
+    const Tile &tile, int64_t t, int lane, int64_t num_tiles, const float *__restrict__ m,
+    const float *__restrict__ g, int64_t g_ld, float *__restrict__ err, int64_t err_ld,
+    const float *__restrict__ scales, int64_t scales_ld, uint64_t *__restrict__ bits,
+    int64_t bits_ld, double *__restrict__ partial, int n_local, float beta1, float omb1)
+{
+    const int len = tile.len;
+    const int64_t base = tile.start;
+    const int nwords = (len + 63) >> 6;
+
+    v4f bm[kSubBlocks];
+#pragma unroll
+    for (int b = 0; b < kSubBlocks; ++b)
+        bm[b] = beta1 * ld4<FULL>(m + base, b * (kWave * 4) + 4 * lane, len);
+
+    for (int i = 0; i < n_local; ++i) {
+        const float sp = scales[(int64_t)i * scales_ld + tile.seg];
+        const float *gi = g + (int64_t)i * g_ld + base;
+        float *ei = err + (int64_t)i * err_ld + base;
+        uint64_t *bi = bits + (int64_t)i * bits_ld + (base >> 6);
+        v4f gv[kSubBlocks], cv[kSubBlocks];
+#pragma unroll
+        for (int b = 0; b < kSubBlocks; ++b) {
+            const int li = b * (kWave * 4) + 4 * lane;
+            gv[b] = ld4<FULL>(gi, li, len);
+            cv[b] = ld4<FULL>(ei, li, len);
+        }
+        double acc = 0.0;
+#pragma unroll
+        for (int b = 0; b < kSubBlocks; ++b) {
+            const int li = b * (kWave * 4) + 4 * lane;
+            v4f zv;
+            uint32_t nib = 0;
+#pragma unroll
+            for (int c = 0; c < 4; ++c) {
+                const float d = error_of(cv[b][c], sp);
+                float mi = omb1 * gv[b][c];
+                mi = bm[b][c] + mi;
+                const float z = mi + d;
+                zv[c] = z;
+                const bool valid = FULL || li + c < len;
+                const double zd = valid ? (double)z : 0.0;
+                acc += zd * zd;
+                nib |= (valid && z >= 0.f) ? (1u << c) : 0u;
+            }
+            st4<FULL>(ei, li, len, zv);
+            const uint64_t word = row_sign_word(nib, lane);
+            const int w = 4 * b + (lane >> 4);
+            if ((lane & 15) == 0 && (FULL || w < nwords)) bi[w] = word;
+        }
+        acc = wave_sum(acc);
+        if (lane == 0) partial[(int64_t)i * num_tiles + t] = acc;
+    }
+}
+
 __global__ __launch_bounds__(kBlock) void k_worker_pass(
     const Tile *__restrict__ tiles, int64_t num_tiles, const float *__restrict__ m,
     const float *__restrict__ g, int64_t g_ld, float *__restrict__ err, int64_t err_ld,
@@ -160,109 +229,118 @@ __global__ __launch_bounds__(kBlock) void k_worker_pass(
     const int64_t t = (int64_t)blockIdx.x * kWavesPerBlock + (threadIdx.x >> 6);
     if (t >= num_tiles) return;
     const Tile tile = tiles[t];
-    const int len = tile.len;
-    const int64_t base = tile.start;
-    const int nwords = (len + 63) >> 6;
-
-    float bm[kSubBlocks][4];
-#pragma unroll
-    for (int b = 0; b < kSubBlocks; ++b) {
-        const float4 mv = load4(m + base, b * (kWave * 4) + 4 * lane, len);
-#pragma unroll
-        for (int c = 0; c < 4; ++c) bm[b][c] = beta1 * comp(mv, c);
-    }
-
-    for (int i = 0; i < n_local; ++i) {
-        const float sp = scales[(int64_t)i * scales_ld + tile.seg];
-        const float *gi = g + (int64_t)i * g_ld + base;
-        float *ei = err + (int64_t)i * err_ld + base;
-        uint64_t *bi = bits + (int64_t)i * bits_ld + (base >> 6);
-        double acc = 0.0;
-#pragma unroll
-        for (int b = 0; b < kSubBlocks; ++b) {
-            const int li = b * (kWave * 4) + 4 * lane;
-            const float4 gv = load4(gi, li, len);
-            const float4 cv = load4(ei, li, len);
-            float4 zv;
-            uint32_t nib = 0;
-#pragma unroll
-            for (int c = 0; c < 4; ++c) {
-                const float d = error_of(comp(cv, c), sp);
-                float mi = omb1 * comp(gv, c);
-                mi = bm[b][c] + mi;
-                const float z = mi + d;
-                set_comp(zv, c, z);
-                const bool valid = li + c < len;
-                const double zd = valid ? (double)z : 0.0;
-                acc += zd * zd;
-                nib |= (valid && z >= 0.f) ? (1u << c) : 0u;
-            }
-            store4(ei, li, len, zv);
-            const uint64_t word = row_sign_word(nib, lane);
-            const int w = 4 * b + (lane >> 4);
-            if ((lane & 15) == 0 && w < nwords) bi[w] = word;
-        }
-        acc = wave_sum(acc);
-        if (lane == 0) partial[(int64_t)i * num_tiles + t] = acc;
-    }
+    if (tile.len == kTileElems)
+        worker_tile<true>(tile, t, lane, num_tiles, m, g, g_ld, err, err_ld, scales, scales_ld,
+                          bits, bits_ld, partial, n_local, beta1, omb1);
+    else
+        worker_tile<false>(tile, t, lane, num_tiles, m, g, g_ld, err, err_ld, scales,
+                           scales_ld, bits, bits_ld, partial, n_local, beta1, omb1);
 }
 
 // ---------------------------------------------------------------------------
 // Scale finalize: scale = fp32(sqrt(sum over the segment's tiles / len)),
-// summed by one wave in a fixed order; empty segments get 0.
+// summed in a fixed order (so results do not depend on scheduling); empty
+// segments get 0.  THREADS lanes cooperate on one (row, segment) pair: a
+// wave when segments have few tiles, a whole block when they have many.
 // ---------------------------------------------------------------------------
+template <int THREADS>
 __device__ __forceinline__ float finalize_one(const double *__restrict__ part, int64_t tb,
-                                              int64_t te, int64_t len, int lane)
+                                              int64_t te, int64_t len, double *red)
 {
-    double s = 0.0;
-    for (int64_t t = tb + lane; t < te; t += kWave) s += part[t];
-    s = wave_sum(s);
+    const int tid = threadIdx.x % THREADS;
+    double s0 = 0.0, s1 = 0.0, s2 = 0.0, s3 = 0.0;
+    int64_t t = tb + tid;
+    for (; t + 3 * THREADS < te; t += 4 * THREADS) {
+        s0 += part[t];
+        s1 += part[t + THREADS];
+        s2 += part[t + 2 * THREADS];
+        s3 += part[t + 3 * THREADS];
+    }
+    for (; t < te; t += THREADS) s0 += part[t];
+    double s = wave_sum((s0 + s1) + (s2 + s3));
+    if (THREADS > kWave) {
+        const int wv = tid / kWave;
+        if ((tid & (kWave - 1)) == 0) red[wv] = s;
+        __syncthreads();
+        s = red[0];
+        for (int w = 1; w < THREADS / kWave; ++w) s += red[w];
+    }
     return len > 0 ? (float)__builtin_sqrt(s / (double)len) : 0.0f;
 }
 
-__global__ __launch_bounds__(kBlock) void k_worker_finalize(
-    DeviceTables tb, int64_t num_segments, int rows, const double *__restrict__ partial,
-    int64_t part_ld, float *__restrict__ scales, int64_t scales_ld)
+// Pair p -> (row i, segment q).  Worker form: all S segments of each row.
+// Server form: segments k*n + j for j in [jb, je) and every tensor k.
+template <int THREADS>
+__global__ __launch_bounds__(kBlock) void k_finalize(
+    DeviceTables tb, int64_t num_pairs, int64_t num_segments, int server_form, int n, int jb,
+    int je, const double *__restrict__ partial, int64_t part_ld, float *__restrict__ scales,
+    int64_t scales_ld)
 {
-    const int lane = threadIdx.x & (kWave - 1);
-    const int64_t p = (int64_t)blockIdx.x * kWavesPerBlock + (threadIdx.x >> 6);
-    if (p >= (int64_t)rows * num_segments) return;
-    const int64_t i = p / num_segments, q = p % num_segments;
-    const float s = finalize_one(partial + i * part_ld, tb.seg_tile_begin[q],
-                                 tb.seg_tile_end[q], tb.seg_len[q], lane);
-    if (lane == 0) scales[i * scales_ld + q] = s;
-}
-
-__global__ __launch_bounds__(kBlock) void k_server_finalize(
-    DeviceTables tb, int K, int n, int jb, int je, const double *__restrict__ partial,
-    float *__restrict__ sscales)
-{
-    const int lane = threadIdx.x & (kWave - 1);
-    const int64_t p = (int64_t)blockIdx.x * kWavesPerBlock + (threadIdx.x >> 6);
-    const int cnt = je - jb;
-    if (p >= (int64_t)K * cnt) return;
-    const int64_t q = (p / cnt) * n + jb + (p % cnt);
-    const float s = finalize_one(partial, tb.seg_tile_begin[q], tb.seg_tile_end[q],
-                                 tb.seg_len[q], lane);
-    if (lane == 0) sscales[q] = s;
+    __shared__ double red[kBlock / kWave];
+    const int64_t p = (int64_t)blockIdx.x * (kBlock / THREADS) + threadIdx.x / THREADS;
+    if (p >= num_pairs) return;  // whole block or whole wave: uniform for THREADS
+    int64_t i, q;
+    if (server_form) {
+        const int cnt = je - jb;
+        i = 0;
+        q = (p / cnt) * n + jb + (p % cnt);
+    } else {
+        i = p / num_segments;
+        q = p % num_segments;
+    }
+    const float s = finalize_one<THREADS>(partial + i * part_ld, tb.seg_tile_begin[q],
+                                          tb.seg_tile_end[q], tb.seg_len[q], red);
+    if (threadIdx.x % THREADS == 0) scales[i * scales_ld + q] = s;
 }
 
 // ---------------------------------------------------------------------------
 // Server pass over the tiles of the owned chunks: decode and average the n
-// incoming messages (fp64, worker order), add the server error, write the
-// sign words and the new compensated server state, and the tile's sum of
-// squares.  Incoming sign words are staged in LDS 32 worker rows at a time
-// with coalesced 128-byte row reads; each lane then reads the one word that
-// covers its 4 elements of a sub-block (a broadcast read, no bank conflict).
+// incoming messages, add the server error, write the sign words and the new
+// compensated server state, and the tile's sum of squares.
+//
+// Incoming sign words are staged in LDS 32 worker rows at a time with
+// coalesced 128-byte row reads.  The average is an fp64 sum of +-scale over
+// the workers in worker order.  When every partial sum of the segment's
+// scales is exactly representable in fp64 (the scales' exponents span at most
+// 29 - ceil(log2 n) binades; true for any realistic message set) the sum is
+// exact, so it may be formed in any grouping: then each group of 4 workers
+// is one lookup in a 16-entry table of its signed scale sums, indexed by the
+// 4 workers' bits of the element (a 4x4 bit transpose of their nibbles).
+// Otherwise every worker is added one by one.  Both give the oracle's sum.
 // ---------------------------------------------------------------------------
+__device__ __forceinline__ uint32_t transpose4x4(uint32_t x)
+{
+    // x bit 4k+c (worker k, element c) -> bit 4c+k
+    uint32_t t = (x ^ (x >> 3)) & 0x0A0Au;
+    x ^= t ^ (t << 3);
+    t = (x ^ (x >> 6)) & 0x00CCu;
+    x ^= t ^ (t << 6);
+    return x;
+}
+
+__device__ __forceinline__ int wave_max(int v)
+{
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) v = max(v, __shfl_xor(v, off, kWave));
+    return v;
+}
+
+__device__ __forceinline__ int wave_min(int v)
+{
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) v = min(v, __shfl_xor(v, off, kWave));
+    return v;
+}
+
 __global__ __launch_bounds__(kBlock) void k_server_pass(
     const Tile *__restrict__ tiles, int64_t tile_begin, int64_t tile_count, int n,
-    const uint64_t *__restrict__ wbits, int64_t bits_ld, int64_t bits_word_base,
-    const float *__restrict__ wscales, int64_t scales_ld, int64_t scales_seg_base,
-    float *__restrict__ serr, const float *__restrict__ sscales,
+    int grouping_limit, const uint64_t *__restrict__ wbits, int64_t bits_ld,
+    int64_t bits_word_base, const float *__restrict__ wscales, int64_t scales_ld,
+    int64_t scales_seg_base, float *__restrict__ serr, const float *__restrict__ sscales,
     uint64_t *__restrict__ sbits, double *__restrict__ partial)
 {
-    __shared__ uint64_t s_bits[kWavesPerBlock][kServerRowBatch][kTileWords];
+    __shared__ uint32_t s_bits[kWavesPerBlock][kServerRowBatch][2 * kTileWords];
+    __shared__ double s_lut[kWavesPerBlock][kServerRowBatch / 4][16];
     __shared__ float s_scale[kWavesPerBlock][kServerRowBatch];
 
     const int lane = threadIdx.x & (kWave - 1);
@@ -276,6 +354,27 @@ __global__ __launch_bounds__(kBlock) void k_server_pass(
     const int nwords = (len + 63) >> 6;
     const int64_t w0 = (base >> 6) - bits_word_base;
     const int64_t sq = (int64_t)tile.seg - scales_seg_base;
+
+    // Exponent span of the segment's non-zero scales (biased exponents; a
+    // subnormal counts as exponent 1, whose ulp it shares).
+    int emax = 0, emin = 1 << 20;
+    if (active) {
+        for (int r = lane; r < n; r += kWave) {
+            const uint32_t u = __float_as_uint(wscales[(int64_t)r * scales_ld + sq]) & 0x7FFFFFFFu;
+            if (u == 0) continue;
+            const int e = max((int)(u >> 23), 1);
+            emax = max(emax, e);
+            emin = min(emin, e);
+        }
+    }
+    emax = wave_max(emax);
+    emin = wave_min(emin);
+    const bool grouped = active && emax < 255 && (emax == 0 || emax - emin <= grouping_limit);
+
+    // In sub-block b, lane L's 4 elements are bits 4(L%16)..+3 of word 4b+L/16,
+    // i.e. bits 4(L%8).. of 32-bit half (L/8)%2 of that word.
+    const int half = (lane >> 3) & 1;
+    const int shift = 4 * (lane & 7);
 
     double sum[kSubBlocks][4];
 #pragma unroll
@@ -291,20 +390,55 @@ __global__ __launch_bounds__(kBlock) void k_server_pass(
             for (int k = 0; k < kServerRowBatch / 4; ++k) {
                 const int r = (lane >> 4) + 4 * k;
                 if (r < rows && wi < nwords)
-                    s_bits[wv][r][wi] = wbits[(int64_t)(r0 + r) * bits_ld + w0 + wi];
+                    *(uint64_t *)&s_bits[wv][r][2 * wi] =
+                        __builtin_nontemporal_load(wbits + (int64_t)(r0 + r) * bits_ld + w0 + wi);
             }
             if (lane < rows && active)
                 s_scale[wv][lane] = wscales[(int64_t)(r0 + lane) * scales_ld + sq];
         }
         __syncthreads();
-        if (active) {
+        if (grouped) {
+            for (int e = lane; e < 16 * (kServerRowBatch / 4); e += kWave) {
+                const int q = e >> 4, idx = e & 15;
+                double v = 0.0;
+#pragma unroll
+                for (int k = 0; k < 4; ++k) {
+                    const int r = 4 * q + k;
+                    if (r < rows) {
+                        const double sc = (double)s_scale[wv][r];
+                        v += ((idx >> k) & 1) ? sc : -sc;
+                    }
+                }
+                s_lut[wv][q][idx] = v;
+            }
+        }
+        __syncthreads();
+        if (grouped) {
+            const int groups = (rows + 3) >> 2;
+            for (int q = 0; q < groups; ++q) {
+#pragma unroll
+                for (int b = 0; b < kSubBlocks; ++b) {
+                    const int hw = 2 * (4 * b + (lane >> 4)) + half;
+                    uint32_t x = 0;
+#pragma unroll
+                    for (int k = 0; k < 4; ++k) {
+                        const int r = 4 * q + k;
+                        const uint32_t nib = r < rows ? (s_bits[wv][r][hw] >> shift) & 0xFu : 0u;
+                        x |= nib << (4 * k);
+                    }
+                    const uint32_t y = transpose4x4(x);
+#pragma unroll
+                    for (int c = 0; c < 4; ++c) sum[b][c] += s_lut[wv][q][(y >> (4 * c)) & 0xFu];
+                }
+            }
+        } else if (active) {
             for (int r = 0; r < rows; ++r) {
                 const double sp = (double)s_scale[wv][r];
                 const double sn = -sp;
 #pragma unroll
                 for (int b = 0; b < kSubBlocks; ++b) {
-                    const uint64_t word = s_bits[wv][r][4 * b + (lane >> 4)];
-                    const uint32_t nib = (uint32_t)(word >> (4 * (lane & 15))) & 0xFu;
+                    const uint32_t nib =
+                        (s_bits[wv][r][2 * (4 * b + (lane >> 4)) + half] >> shift) & 0xFu;
 #pragma unroll
                     for (int c = 0; c < 4; ++c) sum[b][c] += ((nib >> c) & 1u) ? sp : sn;
                 }
@@ -320,20 +454,20 @@ __global__ __launch_bounds__(kBlock) void k_server_pass(
 #pragma unroll
     for (int b = 0; b < kSubBlocks; ++b) {
         const int li = b * (kWave * 4) + 4 * lane;
-        const float4 cv = load4(serr + base, li, len);
-        float4 zv;
+        const v4f cv = ld4<false>(serr + base, li, len);
+        v4f zv;
         uint32_t nib = 0;
 #pragma unroll
         for (int c = 0; c < 4; ++c) {
             const float avg = (float)(sum[b][c] / dn);
-            const float z = avg + error_of(comp(cv, c), sprev);
-            set_comp(zv, c, z);
+            const float z = avg + error_of(cv[c], sprev);
+            zv[c] = z;
             const bool valid = li + c < len;
             const double zd = valid ? (double)z : 0.0;
             acc += zd * zd;
             nib |= (valid && z >= 0.f) ? (1u << c) : 0u;
         }
-        store4(serr + base, li, len, zv);
+        st4<false>(serr + base, li, len, zv);
         const uint64_t word = row_sign_word(nib, lane);
         const int w = 4 * b + (lane >> 4);
         if ((lane & 15) == 0 && w < nwords) sbits[(base >> 6) + w] = word;
@@ -345,6 +479,37 @@ __global__ __launch_bounds__(kBlock) void k_server_pass(
 // ---------------------------------------------------------------------------
 // Decompress + preconditioned update: x -= lr * (+-scale) / sqrt(v + eps).
 // ---------------------------------------------------------------------------
+template <bool FULL>
+__device__ __forceinline__ void update_tile(const Tile &tile, int lane,
+                                            const uint64_t *__restrict__ sbits, float s,
+                                            float *__restrict__ x, float *__restrict__ m_out,
+                                            const float *__restrict__ v, float lr, float eps)
+{
+    const int len = tile.len;
+    const int64_t base = tile.start;
+#pragma unroll
+    for (int b = 0; b < kSubBlocks; ++b) {
+        const int li = b * (kWave * 4) + 4 * lane;
+        if (!FULL && li >= len) break;
+        const uint64_t word = sbits[(base >> 6) + 4 * b + (lane >> 4)];
+        const uint32_t nib = (uint32_t)(word >> (4 * (lane & 15))) & 0xFu;
+        v4f xv = ld4<FULL>(x + base, li, len);
+        const v4f vv = ld4<FULL>(v + base, li, len);
+        v4f mv;
+#pragma unroll
+        for (int c = 0; c < 4; ++c) {
+            const float mbar = ((nib >> c) & 1u) ? s : -s;
+            const float denom = __builtin_sqrtf(vv[c] + eps);
+            const float ratio = mbar / denom;
+            const float step = lr * ratio;
+            xv[c] = xv[c] - step;
+            mv[c] = mbar;
+        }
+        st4<FULL>(x + base, li, len, xv);
+        if (m_out) st4<FULL>(m_out + base, li, len, mv);
+    }
+}
+
 __global__ __launch_bounds__(kBlock) void k_update(
     const Tile *__restrict__ tiles, int64_t num_tiles, const uint64_t *__restrict__ sbits,
     const float *__restrict__ sscales, float *__restrict__ x, float *__restrict__ m_out,
@@ -354,30 +519,9 @@ __global__ __launch_bounds__(kBlock) void k_update(
     const int64_t t = (int64_t)blockIdx.x * kWavesPerBlock + (threadIdx.x >> 6);
     if (t >= num_tiles) return;
     const Tile tile = tiles[t];
-    const int len = tile.len;
-    const int64_t base = tile.start;
     const float s = sscales[tile.seg];
-#pragma unroll
-    for (int b = 0; b < kSubBlocks; ++b) {
-        const int li = b * (kWave * 4) + 4 * lane;
-        if (li >= len) break;
-        const uint64_t word = sbits[(base >> 6) + 4 * b + (lane >> 4)];
-        const uint32_t nib = (uint32_t)(word >> (4 * (lane & 15))) & 0xFu;
-        float4 xv = load4(x + base, li, len);
-        const float4 vv = load4(v + base, li, len);
-        float4 mv;
-#pragma unroll
-        for (int c = 0; c < 4; ++c) {
-            const float mbar = ((nib >> c) & 1u) ? s : -s;
-            const float denom = __builtin_sqrtf(comp(vv, c) + eps);
-            const float ratio = mbar / denom;
-            const float step = lr * ratio;
-            set_comp(xv, c, comp(xv, c) - step);
-            set_comp(mv, c, mbar);
-        }
-        store4(x + base, li, len, xv);
-        if (m_out) store4(m_out + base, li, len, mv);
-    }
+    if (tile.len == kTileElems) update_tile<true>(tile, lane, sbits, s, x, m_out, v, lr, eps);
+    else update_tile<false>(tile, lane, sbits, s, x, m_out, v, lr, eps);
 }
 
 // ---------------------------------------------------------------------------
@@ -400,10 +544,10 @@ __global__ __launch_bounds__(kBlock) void k_materialize(
         for (int b = 0; b < kSubBlocks; ++b) {
             const int li = b * (kWave * 4) + 4 * lane;
             if (li >= len) break;
-            float4 zv = load4(err + (int64_t)r * err_ld + base, li, len);
+            v4f zv = ld4<false>(err + (int64_t)r * err_ld + base, li, len);
 #pragma unroll
-            for (int c = 0; c < 4; ++c) set_comp(zv, c, error_of(comp(zv, c), s));
-            store4(out + (int64_t)r * out_ld + base, li, len, zv);
+            for (int c = 0; c < 4; ++c) zv[c] = error_of(zv[c], s);
+            st4<false>(out + (int64_t)r * out_ld + base, li, len, zv);
         }
     }
 }
@@ -440,13 +584,21 @@ hipError_t launch_worker_pass(const DeviceTables &tb, int64_t num_tiles, const f
     return hipGetLastError();
 }
 
-hipError_t launch_worker_finalize(const DeviceTables &tb, int64_t num_segments, int rows,
-                                  const double *partial, int64_t part_ld, float *scales,
-                                  int64_t scales_ld, hipStream_t s)
+hipError_t launch_finalize(const DeviceTables &tb, int64_t max_seg_tiles, int64_t num_pairs,
+                           int64_t num_segments, int server_form, int n, int jb, int je,
+                           const double *partial, int64_t part_ld, float *scales,
+                           int64_t scales_ld, hipStream_t s)
 {
-    hipLaunchKernelGGL(k_worker_finalize, dim3(blocks_for((int64_t)rows * num_segments)),
-                       dim3(kBlock), 0, s, tb, num_segments, rows, partial, part_ld, scales,
-                       scales_ld);
+    if (num_pairs <= 0) return hipSuccess;
+    if (max_seg_tiles > 4 * kWave) {
+        hipLaunchKernelGGL(k_finalize<kBlock>, dim3((unsigned)num_pairs), dim3(kBlock), 0, s, tb,
+                           num_pairs, num_segments, server_form, n, jb, je, partial, part_ld,
+                           scales, scales_ld);
+    } else {
+        hipLaunchKernelGGL(k_finalize<kWave>, dim3(blocks_for(num_pairs)), dim3(kBlock), 0, s,
+                           tb, num_pairs, num_segments, server_form, n, jb, je, partial, part_ld,
+                           scales, scales_ld);
+    }
     return hipGetLastError();
 }
 
@@ -456,17 +608,13 @@ hipError_t launch_server_pass(const DeviceTables &tb, int64_t tile_begin, int64_
                               int64_t scales_seg_base, float *serr, float *sscales,
                               uint64_t *sbits, double *partial, hipStream_t s)
 {
+    int log2n = 0;
+    while ((1 << log2n) < n) ++log2n;
+    const int grouping_limit = 29 - log2n;
     hipLaunchKernelGGL(k_server_pass, dim3(blocks_for(tile_count)), dim3(kBlock), 0, s,
-                       tb.tiles, tile_begin, tile_count, n, wbits, bits_ld, bits_word_base,
-                       wscales, scales_ld, scales_seg_base, serr, sscales, sbits, partial);
-    return hipGetLastError();
-}
-
-hipError_t launch_server_finalize(const DeviceTables &tb, int K, int n, int jb, int je,
-                                  const double *partial, float *sscales, hipStream_t s)
-{
-    hipLaunchKernelGGL(k_server_finalize, dim3(blocks_for((int64_t)K * (je - jb))),
-                       dim3(kBlock), 0, s, tb, K, n, jb, je, partial, sscales);
+                       tb.tiles, tile_begin, tile_count, n, grouping_limit, wbits, bits_ld,
+                       bits_word_base, wscales, scales_ld, scales_seg_base, serr, sscales, sbits,
+                       partial);
     return hipGetLastError();
 }
 

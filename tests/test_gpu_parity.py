@@ -107,8 +107,16 @@ def test_worker_compress_parity(ob, dev, numel, n):
     plan.close()
 
 
-@pytest.mark.parametrize("numel,n", CASES)
-def test_server_parity(ob, dev, numel, n):
+SERVER_CASES = [c + ("lognormal",) for c in CASES] + [
+    ([1 << 20], 4, "wide"), ([5000, 300, 64], 5, "wide"), ([70_000], 37, "lognormal"),
+    ([70_000], 37, "zeros"), ([100_000], 256, "lognormal"), ([100_000], 256, "wide")]
+
+
+@pytest.mark.parametrize("numel,n,scales", SERVER_CASES)
+def test_server_parity(ob, dev, numel, n, scales):
+    """Incoming scales 'lognormal' have a narrow exponent span (the grouped
+    summation path); 'wide' spans ~80 binades (one-by-one path); 'zeros'
+    mixes zero scales in."""
     L = oracle.Layout(numel, n)
     plan = ob.Plan(numel, n)
     *_, dbar = _random_state(L, 20 + n, n)
@@ -116,6 +124,10 @@ def test_server_parity(ob, dev, numel, n):
     wbits = rng.integers(0, np.iinfo(np.uint64).max, size=(n, L.W), dtype=np.uint64,
                          endpoint=True)
     wscales = np.exp(rng.normal(-7, 0.5, size=(n, L.S))).astype(np.float32)
+    if scales == "wide":
+        wscales *= np.float32(2.0) ** rng.integers(-40, 40, size=(n, L.S)).astype(np.float32)
+    elif scales == "zeros":
+        wscales[rng.random((n, L.S)) < 0.3] = 0
     serr = _put(dbar, dev)
     sbits = torch.zeros(L.W, dtype=torch.int64, device=dev)
     sscales = torch.zeros(L.S, dtype=torch.float32, device=dev)
