@@ -133,6 +133,12 @@ def warmup_step(layout, x, m, v, g, n_grads, lr, beta1, beta2, eps,
                                int(bias_correction), int(t))
 
 
+def warmup_range(b, e, x, m, v, g, g_ld, n_grads, lr, beta1, beta2, eps, bias_correction, t):
+    """Warm-up step on elements [b, e) of flat arrays; g: n_grads rows of g_ld."""
+    lib().orc_warmup_range(int(b), int(e), _f(x), _f(m), _f(v), _f(g), int(g_ld), int(n_grads),
+                           lr, beta1, beta2, eps, int(bias_correction), int(t))
+
+
 def worker_segment(b, e, beta1, m, g_i, delta_i, bits_i, z_scratch):
     return np.float32(lib().orc_worker_segment(b, e, beta1, _f(m), _f(g_i), _f(delta_i),
                                                _u(bits_i), _f(z_scratch)))
