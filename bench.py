@@ -38,6 +38,27 @@ def algorithmic_bytes_per_param(n):
     return worker, server, update
 
 
+def measured_traffic(workload, kernel):
+    """HBM bytes per launch of `kernel` from the committed rocprofv3 counter
+    summary (FETCH_SIZE + WRITE_SIZE, each calibrated on a plain device copy),
+    or None when there is none for this workload or the kernel source has
+    changed since the counters were taken."""
+    import hashlib
+    import re
+    path = os.path.join(ROOT, "profiles", "pmc_traffic_%s.md" % workload)
+    if not os.path.exists(path):
+        return None
+    m = re.search(r"```json\n(.*?)\n```", open(path).read(), re.S)
+    if not m:
+        return None
+    info = json.loads(m.group(1))
+    src = os.path.join(ROOT, "paper_2102_02888_amd", "csrc", "onebit_kernels.hip")
+    if hashlib.sha256(open(src, "rb").read()).hexdigest() != info.get("kernels_source_sha256"):
+        return None
+    k = info["kernels"].get(kernel)
+    return None if k is None else k["traffic_bytes"]
+
+
 def cpu_baseline(st, plan, wl, target_s=12.0, max_segments=3):
     """Times the oracle (single thread) on whole segments of the workload:
     every worker's pass over the segment, the owner's average and
@@ -207,7 +228,9 @@ def main():
         "warmup_adam_step_ms": sum(warm_ms[1:]) / max(1, len(warm_ms) - 1) if warm_ms else None,
         "roofline": {"bound": "hbm", "kernel": "worker_compress (k_worker_pass)",
                      "achieved": achieved, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
-                     "frac": achieved / HBM_PEAK_GBPS, "traffic": None},
+                     "frac": achieved / HBM_PEAK_GBPS,
+                     "traffic": measured_traffic(wl.name, "k_worker_pass"),
+                     "algorithmic_bytes_per_launch": worker_bytes},
     }
     if not args.no_probe:
         del events

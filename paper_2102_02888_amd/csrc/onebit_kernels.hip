@@ -298,8 +298,10 @@ __global__ __launch_bounds__(kBlock) void k_finalize(
 // incoming messages, add the server error, write the sign words and the new
 // compensated server state, and the tile's sum of squares.
 //
-// Incoming sign words are staged in LDS 32 worker rows at a time with
-// coalesced 128-byte row reads.  The average is an fp64 sum of +-scale over
+// Each wave owns one tile and its own LDS region, so it synchronises only
+// with itself (no workgroup barrier); the tile's error-state loads are issued
+// first so that they overlap the sign-word traffic.  Incoming sign words are
+// staged in LDS 32 worker rows at a time with coalesced 128-byte row reads.  The average is an fp64 sum of +-scale over
 // the workers in worker order.  When every partial sum of the segment's
 // scales is exactly representable in fp64 (the scales' exponents span at most
 // 29 - ceil(log2 n) binades; true for any realistic message set) the sum is
@@ -342,40 +344,39 @@ __global__ __launch_bounds__(kBlock) void k_server_pass(
     __shared__ uint32_t s_bits[kWavesPerBlock][kServerRowBatch][2 * kTileWords];
     __shared__ double s_lut[kWavesPerBlock][kServerRowBatch / 4][16];
     __shared__ float s_scale[kWavesPerBlock][kServerRowBatch];
-
     const int lane = threadIdx.x & (kWave - 1);
     const int wv = threadIdx.x >> 6;
     const int64_t rel = (int64_t)blockIdx.x * kWavesPerBlock + wv;
-    const bool active = rel < tile_count;  // no early exit: the block syncs below
-    const int64_t t = tile_begin + (active ? rel : 0);
+    if (rel >= tile_count) return;
+    const int64_t t = tile_begin + rel;
     const Tile tile = tiles[t];
-    const int len = active ? tile.len : 0;
+    const int len = tile.len;
     const int64_t base = tile.start;
     const int nwords = (len + 63) >> 6;
     const int64_t w0 = (base >> 6) - bits_word_base;
     const int64_t sq = (int64_t)tile.seg - scales_seg_base;
+    const bool full = len == kTileElems;
 
-    // Exponent span of the segment's non-zero scales (biased exponents; a
-    // subnormal counts as exponent 1, whose ulp it shares).
+    // issue the error-state loads first; they are consumed at the end
+    v4f cv[kSubBlocks];
+#pragma unroll
+    for (int b = 0; b < kSubBlocks; ++b) {
+        const int li = b * (kWave * 4) + 4 * lane;
+        cv[b] = full ? ld4<true>(serr + base, li, len) : ld4<false>(serr + base, li, len);
+    }
     int emax = 0, emin = 1 << 20;
-    if (active) {
-        for (int r = lane; r < n; r += kWave) {
-            const uint32_t u = __float_as_uint(wscales[(int64_t)r * scales_ld + sq]) & 0x7FFFFFFFu;
-            if (u == 0) continue;
-            const int e = max((int)(u >> 23), 1);
-            emax = max(emax, e);
-            emin = min(emin, e);
-        }
+    for (int r = lane; r < n; r += kWave) {
+        const uint32_t u = __float_as_uint(wscales[(int64_t)r * scales_ld + sq]) & 0x7FFFFFFFu;
+        if (u == 0) continue;
+        const int e = max((int)(u >> 23), 1);
+        emax = max(emax, e);
+        emin = min(emin, e);
     }
     emax = wave_max(emax);
     emin = wave_min(emin);
-    const bool grouped = active && emax < 255 && (emax == 0 || emax - emin <= grouping_limit);
-
-    // In sub-block b, lane L's 4 elements are bits 4(L%16)..+3 of word 4b+L/16,
-    // i.e. bits 4(L%8).. of 32-bit half (L/8)%2 of that word.
+    const bool grouped = emax < 255 && (emax == 0 || emax - emin <= grouping_limit);
     const int half = (lane >> 3) & 1;
     const int shift = 4 * (lane & 7);
-
     double sum[kSubBlocks][4];
 #pragma unroll
     for (int b = 0; b < kSubBlocks; ++b)
@@ -384,19 +385,18 @@ __global__ __launch_bounds__(kBlock) void k_server_pass(
 
     for (int r0 = 0; r0 < n; r0 += kServerRowBatch) {
         const int rows = min(kServerRowBatch, n - r0);
-        {
-            const int wi = lane & (kTileWords - 1);
+        const int wi = lane & (kTileWords - 1);
 #pragma unroll
-            for (int k = 0; k < kServerRowBatch / 4; ++k) {
-                const int r = (lane >> 4) + 4 * k;
-                if (r < rows && wi < nwords)
-                    *(uint64_t *)&s_bits[wv][r][2 * wi] =
-                        __builtin_nontemporal_load(wbits + (int64_t)(r0 + r) * bits_ld + w0 + wi);
-            }
-            if (lane < rows && active)
-                s_scale[wv][lane] = wscales[(int64_t)(r0 + lane) * scales_ld + sq];
+        for (int k = 0; k < kServerRowBatch / 4; ++k) {
+            const int r = (lane >> 4) + 4 * k;
+            if (r < rows && wi < nwords)
+                *(uint64_t *)&s_bits[wv][r][2 * wi] =
+                    __builtin_nontemporal_load(wbits + (int64_t)(r0 + r) * bits_ld + w0 + wi);
         }
-        __syncthreads();
+        if (lane < rows) s_scale[wv][lane] = wscales[(int64_t)(r0 + lane) * scales_ld + sq];
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+        __builtin_amdgcn_wave_barrier();
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
         if (grouped) {
             for (int e = lane; e < 16 * (kServerRowBatch / 4); e += kWave) {
                 const int q = e >> 4, idx = e & 15;
@@ -411,9 +411,9 @@ __global__ __launch_bounds__(kBlock) void k_server_pass(
                 }
                 s_lut[wv][q][idx] = v;
             }
-        }
-        __syncthreads();
-        if (grouped) {
+            __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+            __builtin_amdgcn_wave_barrier();
+            __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
             const int groups = (rows + 3) >> 2;
             for (int q = 0; q < groups; ++q) {
 #pragma unroll
@@ -431,43 +431,41 @@ __global__ __launch_bounds__(kBlock) void k_server_pass(
                     for (int c = 0; c < 4; ++c) sum[b][c] += s_lut[wv][q][(y >> (4 * c)) & 0xFu];
                 }
             }
-        } else if (active) {
+        } else {
             for (int r = 0; r < rows; ++r) {
                 const double sp = (double)s_scale[wv][r];
                 const double sn = -sp;
 #pragma unroll
                 for (int b = 0; b < kSubBlocks; ++b) {
-                    const uint32_t nib =
-                        (s_bits[wv][r][2 * (4 * b + (lane >> 4)) + half] >> shift) & 0xFu;
+                    const uint32_t nib = (s_bits[wv][r][2 * (4 * b + (lane >> 4)) + half] >> shift) & 0xFu;
 #pragma unroll
                     for (int c = 0; c < 4; ++c) sum[b][c] += ((nib >> c) & 1u) ? sp : sn;
                 }
             }
         }
-        __syncthreads();
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+        __builtin_amdgcn_wave_barrier();
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
     }
-    if (!active) return;
-
     const float sprev = sscales[tile.seg];
     const double dn = (double)n;
     double acc = 0.0;
 #pragma unroll
     for (int b = 0; b < kSubBlocks; ++b) {
         const int li = b * (kWave * 4) + 4 * lane;
-        const v4f cv = ld4<false>(serr + base, li, len);
         v4f zv;
         uint32_t nib = 0;
 #pragma unroll
         for (int c = 0; c < 4; ++c) {
             const float avg = (float)(sum[b][c] / dn);
-            const float z = avg + error_of(cv[c], sprev);
+            const float z = avg + error_of(cv[b][c], sprev);
             zv[c] = z;
             const bool valid = li + c < len;
             const double zd = valid ? (double)z : 0.0;
             acc += zd * zd;
             nib |= (valid && z >= 0.f) ? (1u << c) : 0u;
         }
-        st4<false>(serr + base, li, len, zv);
+        if (full) st4<true>(serr + base, li, len, zv); else st4<false>(serr + base, li, len, zv);
         const uint64_t word = row_sign_word(nib, lane);
         const int w = 4 * b + (lane >> 4);
         if ((lane & 15) == 0 && w < nwords) sbits[(base >> 6) + w] = word;
@@ -475,6 +473,7 @@ __global__ __launch_bounds__(kBlock) void k_server_pass(
     acc = wave_sum(acc);
     if (lane == 0) partial[t] = acc;
 }
+
 
 // ---------------------------------------------------------------------------
 // Decompress + preconditioned update: x -= lr * (+-scale) / sqrt(v + eps).
