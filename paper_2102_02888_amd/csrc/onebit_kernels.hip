@@ -358,12 +358,31 @@ __global__ __launch_bounds__(kBlock) void k_server_pass(
     const bool full = len == kTileElems;
 
     // issue the error-state loads first; they are consumed at the end
+    const float sprev = sscales[tile.seg];
     v4f cv[kSubBlocks];
 #pragma unroll
     for (int b = 0; b < kSubBlocks; ++b) {
         const int li = b * (kWave * 4) + 4 * lane;
         cv[b] = full ? ld4<true>(serr + base, li, len) : ld4<false>(serr + base, li, len);
     }
+    // the first batch of sign words and scales is loaded before the exponent
+    // check below, so that both memory round trips overlap
+    const int wi = lane & (kTileWords - 1);
+    uint64_t stg[kServerRowBatch / 4];
+    float scl = 0.f;
+    auto load_batch = [&](int r0) {
+        const int rows = min(kServerRowBatch, n - r0);
+#pragma unroll
+        for (int k = 0; k < kServerRowBatch / 4; ++k) {
+            const int r = (lane >> 4) + 4 * k;
+            stg[k] = (r < rows && wi < nwords)
+                         ? __builtin_nontemporal_load(wbits + (int64_t)(r0 + r) * bits_ld + w0 + wi)
+                         : 0ull;
+        }
+        scl = lane < rows ? wscales[(int64_t)(r0 + lane) * scales_ld + sq] : 0.f;
+    };
+    load_batch(0);
+
     int emax = 0, emin = 1 << 20;
     for (int r = lane; r < n; r += kWave) {
         const uint32_t u = __float_as_uint(wscales[(int64_t)r * scales_ld + sq]) & 0x7FFFFFFFu;
@@ -384,16 +403,15 @@ __global__ __launch_bounds__(kBlock) void k_server_pass(
         for (int c = 0; c < 4; ++c) sum[b][c] = 0.0;
 
     for (int r0 = 0; r0 < n; r0 += kServerRowBatch) {
+        if (r0 > 0) load_batch(r0);
         const int rows = min(kServerRowBatch, n - r0);
-        const int wi = lane & (kTileWords - 1);
+        const int rows4 = (rows + 3) & ~3;  // rows past the last worker hold zero words
 #pragma unroll
         for (int k = 0; k < kServerRowBatch / 4; ++k) {
             const int r = (lane >> 4) + 4 * k;
-            if (r < rows && wi < nwords)
-                *(uint64_t *)&s_bits[wv][r][2 * wi] =
-                    __builtin_nontemporal_load(wbits + (int64_t)(r0 + r) * bits_ld + w0 + wi);
+            if (r < rows4 && wi < nwords) *(uint64_t *)&s_bits[wv][r][2 * wi] = stg[k];
         }
-        if (lane < rows) s_scale[wv][lane] = wscales[(int64_t)(r0 + lane) * scales_ld + sq];
+        if (lane < rows) s_scale[wv][lane] = scl;
         __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
         __builtin_amdgcn_wave_barrier();
         __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
@@ -421,11 +439,8 @@ __global__ __launch_bounds__(kBlock) void k_server_pass(
                     const int hw = 2 * (4 * b + (lane >> 4)) + half;
                     uint32_t x = 0;
 #pragma unroll
-                    for (int k = 0; k < 4; ++k) {
-                        const int r = 4 * q + k;
-                        const uint32_t nib = r < rows ? (s_bits[wv][r][hw] >> shift) & 0xFu : 0u;
-                        x |= nib << (4 * k);
-                    }
+                    for (int k = 0; k < 4; ++k)
+                        x |= ((s_bits[wv][4 * q + k][hw] >> shift) & 0xFu) << (4 * k);
                     const uint32_t y = transpose4x4(x);
 #pragma unroll
                     for (int c = 0; c < 4; ++c) sum[b][c] += s_lut[wv][q][(y >> (4 * c)) & 0xFu];
@@ -447,7 +462,6 @@ __global__ __launch_bounds__(kBlock) void k_server_pass(
         __builtin_amdgcn_wave_barrier();
         __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
     }
-    const float sprev = sscales[tile.seg];
     const double dn = (double)n;
     double acc = 0.0;
 #pragma unroll
