@@ -25,16 +25,18 @@ def log(*a):
 
 
 def algorithmic_bytes_per_param(n):
-    """Bytes the method must move per parameter, each input read once and each
-    output written once (fp32 state, 1-bit messages):
-      worker pass: m read once for all n workers, then per worker g read,
-                   error state read and written, one sign bit written;
+    """Bytes the method must move per parameter in a steady-state step, each
+    input read once and each output written once (fp32 state, 1-bit
+    messages).  The shared momentum is the previous step's server message
+    (Algorithm 1 sets every worker's m to it), so it is read as one sign bit:
+      worker pass: m's sign bit read once for all n workers, then per worker
+                   g read, error state read and written, one sign bit written;
       server pass: n incoming sign bits, server error state read and written,
                    one sign bit written;
-      update     : one sign bit read, x read and written, v read, m written."""
-    worker = 4 + n * (4 + 4 + 4 + 1 / 8)
+      update     : one sign bit read, x read and written, v read."""
+    worker = 1 / 8 + n * (4 + 4 + 4 + 1 / 8)
     server = n / 8 + 4 + 4 + 1 / 8
-    update = 1 / 8 + 4 + 4 + 4 + 4
+    update = 1 / 8 + 4 + 4 + 4
     return worker, server, update
 
 
@@ -167,11 +169,18 @@ def main():
     synth.device_grads(wl, plan.D, plan.tensor_off, wl.warmup_steps + 1, st.grads, scale_vec)
     torch.cuda.synchronize()
 
-    def one_step(ev=None):
+    def one_step(ev=None, first=False):
+        # the first compression step starts from the warm-up's fp32 m; later
+        # steps take m from the previous step's server message
         if ev:
             ev[0].record()
-        ob.onebit_worker_compress(plan, st.m, st.grads, st.worker_err, st.worker_bits,
-                                  st.worker_scales, wl.beta1, st.workspace)
+        if first:
+            ob.onebit_worker_compress(plan, st.m, st.grads, st.worker_err, st.worker_bits,
+                                      st.worker_scales, wl.beta1, st.workspace)
+        else:
+            ob.onebit_worker_compress(plan, None, st.grads, st.worker_err, st.worker_bits,
+                                      st.worker_scales, wl.beta1, st.workspace,
+                                      m_bits=st.server_bits, m_scales=st.server_scales)
         if ev:
             ev[1].record()
         ob.onebit_server_reduce_compress(plan, 0, n, st.worker_bits, st.worker_scales,
@@ -179,11 +188,12 @@ def main():
                                          st.workspace)
         if ev:
             ev[2].record()
-        ob.onebit_decompress_update(plan, st.server_bits, st.server_scales, st.x, st.m, st.v,
+        ob.onebit_decompress_update(plan, st.server_bits, st.server_scales, st.x, None, st.v,
                                     wl.lr, wl.eps)
         if ev:
             ev[3].record()
 
+    one_step(first=True)  # untimed: the step that leaves the warm-up's fp32 momentum
     for _ in range(args.warmup):
         one_step()
     torch.cuda.synchronize()

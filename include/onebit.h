@@ -126,15 +126,22 @@ int onebit_warmup_adam_step(onebit_plan plan, float *x, float *m, float *v,
  *   m_i   = beta1 m + (1-beta1) grads[i]    (m: the shared momentum m_{t-1})
  *   z_i   = m_i + delta_i                   (delta_i from the error state)
  *   bits, scale per segment = C[z_i]        ;  delta_i <- z_i - C[z_i]
- * m: in [D].  grads: n_local rows of grad_ld >= D.  worker_err: in/out,
+ * The shared momentum comes from one of two places.  m != NULL: an fp32
+ * buffer [D] (the warm-up's m before the first compression step).  m == NULL:
+ * the previous step's gathered server message, m = bit ? scale : -scale with
+ * its sign words m_bits [W] and segment scales m_scales [S] -- Algorithm 1
+ * sets every worker's momentum to that decoded message, so it never has to be
+ * stored as fp32 ("packed momentum"; 1/8 byte per element instead of 4).
+ * grads: n_local rows of grad_ld >= D.  worker_err: in/out,
  * n_local rows of err_ld >= D (compensated form, see above).  worker_bits:
  * out, n_local rows of bits_ld >= W words.  worker_scales: in/out, n_local
  * rows of scales_ld >= S floats (in: the previous call's scales, which with
  * worker_err form the error state; out: this step's scales).  workspace:
  * >= workspace_bytes of device memory, contents undefined between calls.
- * Errors: EINVAL (null, n_local < 1 or > n, a leading dim too small), EALIGN,
- * EHIP. */
-int onebit_worker_compress(onebit_plan plan, const float *m,
+ * Errors: EINVAL (null, n_local < 1 or > n, a leading dim too small, m and
+ * m_bits/m_scales both NULL), EALIGN, EHIP. */
+int onebit_worker_compress(onebit_plan plan, const float *m, const uint64_t *m_bits,
+                           const float *m_scales,
                            const float *grads, int64_t grad_ld, int32_t n_local,
                            float *worker_err, int64_t err_ld,
                            uint64_t *worker_bits, int64_t bits_ld,
@@ -185,7 +192,12 @@ int onebit_decompress_update(onebit_plan plan, const uint64_t *server_bits,
  * scales rows of S, in worker_bits / worker_scales), then
  * onebit_server_reduce_compress over chunks [0, n) reading those rows in
  * place, then onebit_decompress_update with m_out = m.
- * x, m: in/out [D]; v_frozen: in [D]; grads: n rows of grad_ld;
+ * m != NULL: fp32 momentum, read by the worker pass and overwritten with the
+ * decoded server message.  m == NULL: packed momentum -- the worker pass
+ * decodes m from server_bits / server_scales as the previous step left them,
+ * and no fp32 momentum is written (valid from the second compression step on;
+ * onebit_decode() materialises it on demand).
+ * x: in/out [D]; v_frozen: in [D]; grads: n rows of grad_ld;
  * worker_err: in/out n rows of err_ld; server_err: in/out [D];
  * worker_bits [n][W], worker_scales [n][S] (in/out), server_bits [W],
  * server_scales [S] (in/out).
@@ -196,6 +208,13 @@ int onebit_step(onebit_plan plan, float *x, float *m, const float *v_frozen,
                 float *worker_scales, uint64_t *server_bits, float *server_scales,
                 float lr, float beta1, float eps, void *workspace,
                 onebit_stream stream);
+
+/* Decoded message: out[e] = bit(e) ? scales[q] : -scales[q] over every real
+ * element e of segment q (padding of out is not written).  With the server
+ * bits and scales this is the momentum m_t of Algorithm 1's final step.
+ * bits [W], scales [S]: in; out: out [D].  Errors: EINVAL, EALIGN, EHIP. */
+int onebit_decode(onebit_plan plan, const uint64_t *bits, const float *scales, float *out,
+                  onebit_stream stream);
 
 /* Explicit errors from the compensated form: for `rows` rows,
  *   delta_out[r*out_ld + e] = z - C[z] with z = err_state[r*err_ld + e] and

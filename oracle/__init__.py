@@ -41,6 +41,8 @@ def lib():
         L.orc_compress.argtypes = [_i64, _i64, _f32p, _u64p]
         L.orc_decode.restype = _f32
         L.orc_decode.argtypes = [_u64p, _i64, _f32]
+        L.orc_decode_range.restype = None
+        L.orc_decode_range.argtypes = [_i64, _i64, _vp, _f32, _vp]
         L.orc_warmup_range.restype = None
         L.orc_warmup_range.argtypes = [_i64, _i64, _vp, _vp, _vp, _vp, _i64, _i32,
                                        _f32, _f32, _f32, _f32, _i32, _i64]
@@ -117,6 +119,15 @@ def compress(z, b=0, e=None):
 
 def decode(bits, e, scale):
     return np.float32(lib().orc_decode(bits, int(e), float(scale)))
+
+
+def decode_message(layout, bits, scales):
+    """Decoded message over the padded layout: +-scale of each element's
+    segment (padding 0)."""
+    out = np.zeros(layout.D, np.float32)
+    for q, (b, e) in enumerate(layout.segments()):
+        lib().orc_decode_range(b, e, _u(bits), float(scales[q]), _f(out))
+    return out
 
 
 def warmup_step(layout, x, m, v, g, n_grads, lr, beta1, beta2, eps,

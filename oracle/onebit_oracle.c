@@ -112,6 +112,12 @@ float orc_decode(const uint64_t *bits, int64_t e, float scale)
     return get_bit(bits, e) ? scale : -scale;
 }
 
+/* Decoded message over elements [b, e): out[idx] = +scale or -scale. */
+void orc_decode_range(int64_t b, int64_t e, const uint64_t *bits, float scale, float *out)
+{
+    for (int64_t idx = b; idx < e; ++idx) out[idx] = orc_decode(bits, idx, scale);
+}
+
 /* ------------------------------------------------------------------------ */
 /* Warm-up: original Adam, eq. (alg:v) of Section 3.2, on the averaged      */
 /* data-parallel gradient (problem statement (main)).  The paper disables   */

@@ -4,7 +4,8 @@ The kernels and their C ABI live in ``libonebit.so`` (sources in ``csrc/``,
 header ``include/onebit.h``); this package is the Python binding.
 """
 from .onebit import (  # noqa: F401
-    Plan, State, onebit_decompress_update, onebit_error_materialize, onebit_plan_create,
+    Plan, State, onebit_decode, onebit_decompress_update, onebit_error_materialize,
+    onebit_plan_create,
     onebit_server_reduce_compress, onebit_step, onebit_warmup_adam_step,
     onebit_worker_compress,
 )

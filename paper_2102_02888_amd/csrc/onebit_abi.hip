@@ -320,14 +320,21 @@ int onebit_warmup_adam_step(onebit_plan p, float *x, float *m, float *v, const f
     return ONEBIT_OK;
 }
 
-int onebit_worker_compress(onebit_plan p, const float *m, const float *grads, int64_t grad_ld,
+int onebit_worker_compress(onebit_plan p, const float *m, const uint64_t *m_bits,
+                           const float *m_scales, const float *grads, int64_t grad_ld,
                            int32_t n_local, float *worker_err, int64_t err_ld,
                            uint64_t *worker_bits, int64_t bits_ld, float *worker_scales,
                            int64_t scales_ld, float beta1, void *workspace,
                            onebit_stream stream)
 {
     TRY(check_plan(p));
-    TRY(check_f32(m, "m"));
+    if (m) {
+        TRY(check_f32(m, "m"));
+    } else {
+        TRY(check_u64(m_bits, "m_bits (m is NULL)"));
+        if (!m_scales) return fail(ONEBIT_EINVAL, "m_scales is NULL (m is NULL)");
+        if (!aligned(m_scales, 4)) return fail(ONEBIT_EALIGN, "m_scales misaligned");
+    }
     TRY(check_f32(grads, "grads"));
     TRY(check_f32(worker_err, "worker_err"));
     TRY(check_u64(worker_bits, "worker_bits"));
@@ -344,9 +351,9 @@ int onebit_worker_compress(onebit_plan p, const float *m, const float *grads, in
     if (p->T == 0) return ONEBIT_OK;
     double *part = (double *)((char *)workspace + worker_partial_offset(p));
     hipStream_t s = (hipStream_t)stream;
-    TRY_HIP(onebit::launch_worker_pass(p->tb, p->T, m, grads, grad_ld, worker_err, err_ld,
-                                       worker_scales, scales_ld, worker_bits, bits_ld, part,
-                                       n_local, beta1, s),
+    TRY_HIP(onebit::launch_worker_pass(p->tb, p->T, m, m_bits, m_scales, grads, grad_ld,
+                                       worker_err, err_ld, worker_scales, scales_ld,
+                                       worker_bits, bits_ld, part, n_local, beta1, s),
             "worker kernel launch");
     TRY_HIP(onebit::launch_finalize(p->tb, p->max_seg_tiles, (int64_t)n_local * p->S, p->S, 0,
                                     p->n, 0, 0, part, p->T, worker_scales, scales_ld, s),
@@ -436,18 +443,34 @@ int onebit_step(onebit_plan p, float *x, float *m, const float *v_frozen, const 
     TRY(check_plan(p));
     // Validate everything before the first launch so that an error writes nothing.
     TRY(check_f32(x, "x"));
-    TRY(check_f32(m, "m"));
+    if (m) TRY(check_f32(m, "m"));
     TRY(check_f32(v_frozen, "v_frozen"));
     TRY(check_f32(server_err, "server_err"));
     TRY(check_u64(server_bits, "server_bits"));
     if (!server_scales) return fail(ONEBIT_EINVAL, "server_scales is NULL");
-    TRY(onebit_worker_compress(p, m, grads, grad_ld, p->n, worker_err, err_ld, worker_bits,
-                               p->W, worker_scales, p->S, beta1, workspace, stream));
+    if (!aligned(server_scales, 4)) return fail(ONEBIT_EALIGN, "server_scales misaligned");
+    TRY(onebit_worker_compress(p, m, server_bits, server_scales, grads, grad_ld, p->n,
+                               worker_err, err_ld, worker_bits, p->W, worker_scales, p->S,
+                               beta1, workspace, stream));
     TRY(onebit_server_reduce_compress(p, 0, p->n, worker_bits, p->W, 0, worker_scales, p->S, 0,
                                       server_err, server_bits, server_scales, workspace,
                                       stream));
     return onebit_decompress_update(p, server_bits, server_scales, x, m, v_frozen, lr, eps,
                                     stream);
+}
+
+int onebit_decode(onebit_plan p, const uint64_t *bits, const float *scales, float *out,
+                  onebit_stream stream)
+{
+    TRY(check_plan(p));
+    TRY(check_u64(bits, "bits"));
+    if (!scales) return fail(ONEBIT_EINVAL, "scales is NULL");
+    if (!aligned(scales, 4)) return fail(ONEBIT_EALIGN, "scales misaligned");
+    TRY(check_f32(out, "out"));
+    if (p->T == 0) return ONEBIT_OK;
+    TRY_HIP(onebit::launch_decode(p->tb, p->T, bits, scales, out, (hipStream_t)stream),
+            "decode kernel launch");
+    return ONEBIT_OK;
 }
 
 int onebit_error_materialize(onebit_plan p, const float *err_state, int64_t err_ld,

@@ -36,11 +36,15 @@ hipError_t launch_warmup(const DeviceTables &tb, int64_t num_tiles, float *x, fl
                          float beta1, float beta2, float eps, int use_bc, float bc1,
                          float bc2, hipStream_t s);
 
+// m != NULL: fp32 momentum; m == NULL: momentum decoded from (m_bits, m_scales).
 hipError_t launch_worker_pass(const DeviceTables &tb, int64_t num_tiles, const float *m,
-                              const float *g, int64_t g_ld, float *err, int64_t err_ld,
-                              const float *scales, int64_t scales_ld, uint64_t *bits,
-                              int64_t bits_ld, double *partial, int n_local, float beta1,
-                              hipStream_t s);
+                              const uint64_t *m_bits, const float *m_scales, const float *g,
+                              int64_t g_ld, float *err, int64_t err_ld, const float *scales,
+                              int64_t scales_ld, uint64_t *bits, int64_t bits_ld,
+                              double *partial, int n_local, float beta1, hipStream_t s);
+
+hipError_t launch_decode(const DeviceTables &tb, int64_t num_tiles, const uint64_t *bits,
+                         const float *scales, float *out, hipStream_t s);
 
 // Segment scales from per-tile partial sums.  Worker form (server_form = 0):
 // num_pairs = rows * num_segments, scale[i*scales_ld + q] from

@@ -40,11 +40,18 @@ __device__ __forceinline__ v4f ld4(const float *__restrict__ p, int li, int len)
     return r;
 }
 
+// Stores elements li..li+3 of p.  Full tiles store non-temporally; partial
+// tiles store plainly (lanes past len store nothing), because their waves
+// may still load after storing.
 template <bool FULL>
 __device__ __forceinline__ void st4(float *__restrict__ p, int li, int len, v4f v)
 {
-    if (FULL || li + 4 <= len) {
+    if (FULL) {
         __builtin_nontemporal_store(v, (v4f *)(p + li));
+        return;
+    }
+    if (li + 4 <= len) {
+        *(v4f *)(p + li) = v;
         return;
     }
     if (li < len) p[li] = v.x;
@@ -101,26 +108,38 @@ __device__ __forceinline__ void warmup_tile(const Tile &tile, int lane, float *_
     const int len = tile.len;
     const int64_t base = tile.start;
     const double dn = (double)n_grads;
+    // every load of the tile precedes the first store (see update_tile)
+    double sum[kSubBlocks][4];
+#pragma unroll
+    for (int b = 0; b < kSubBlocks; ++b)
+#pragma unroll
+        for (int c = 0; c < 4; ++c) sum[b][c] = 0.0;
+    for (int i = 0; i < n_grads; ++i) {
+#pragma unroll
+        for (int b = 0; b < kSubBlocks; ++b) {
+            const v4f gv = ld4<FULL>(g + (int64_t)i * g_ld + base, b * (kWave * 4) + 4 * lane, len);
+#pragma unroll
+            for (int c = 0; c < 4; ++c) sum[b][c] += (double)gv[c];
+        }
+    }
+    v4f xv[kSubBlocks], mv[kSubBlocks], vv[kSubBlocks];
 #pragma unroll
     for (int b = 0; b < kSubBlocks; ++b) {
         const int li = b * (kWave * 4) + 4 * lane;
-        if (!FULL && li >= len) break;
-        double sum[4] = {0.0, 0.0, 0.0, 0.0};
-        for (int i = 0; i < n_grads; ++i) {
-            const v4f gv = ld4<FULL>(g + (int64_t)i * g_ld + base, li, len);
+        xv[b] = ld4<FULL>(x + base, li, len);
+        mv[b] = ld4<FULL>(m + base, li, len);
+        vv[b] = ld4<FULL>(v + base, li, len);
+    }
 #pragma unroll
-            for (int c = 0; c < 4; ++c) sum[c] += (double)gv[c];
-        }
-        v4f xv = ld4<FULL>(x + base, li, len);
-        v4f mv = ld4<FULL>(m + base, li, len);
-        v4f vv = ld4<FULL>(v + base, li, len);
+    for (int b = 0; b < kSubBlocks; ++b) {
+        const int li = b * (kWave * 4) + 4 * lane;
 #pragma unroll
         for (int c = 0; c < 4; ++c) {
-            const float gbar = (float)(sum[c] / dn);
-            float mn = beta1 * mv[c];
+            const float gbar = (float)(sum[b][c] / dn);
+            float mn = beta1 * mv[b][c];
             mn = mn + omb1 * gbar;
             const float gsq = gbar * gbar;
-            float vn = beta2 * vv[c];
+            float vn = beta2 * vv[b][c];
             vn = vn + omb2 * gsq;
             float mh = mn, vh = vn;
             if (use_bc) {
@@ -130,13 +149,13 @@ __device__ __forceinline__ void warmup_tile(const Tile &tile, int lane, float *_
             const float denom = __builtin_sqrtf(vh) + eps;
             const float ratio = mh / denom;
             const float step = lr * ratio;
-            xv[c] = xv[c] - step;
-            mv[c] = mn;
-            vv[c] = vn;
+            xv[b][c] = xv[b][c] - step;
+            mv[b][c] = mn;
+            vv[b][c] = vn;
         }
-        st4<FULL>(x + base, li, len, xv);
-        st4<FULL>(m + base, li, len, mv);
-        st4<FULL>(v + base, li, len, vv);
+        st4<FULL>(x + base, li, len, xv[b]);
+        st4<FULL>(m + base, li, len, mv[b]);
+        st4<FULL>(v + base, li, len, vv[b]);
     }
 }
 
@@ -163,9 +182,39 @@ __global__ __launch_bounds__(kBlock) void k_warmup(
 // sign words of z_i, per-tile partial sum of z_i^2, and z_i written back as the
 // new compensated error state.  m is read once per tile for all workers.
 // ---------------------------------------------------------------------------
-template <bool FULL>
+// The shared momentum m_{t-1} of the tile times beta1.  PACKED: m_{t-1} is
+// the previous step's gathered server message, decoded from its sign words
+// and segment scale (+-scale, exactly the fp32 value the update would have
+// stored), so no fp32 momentum buffer is read.
+template <bool FULL, bool PACKED>
+__device__ __forceinline__ void beta1_momentum(v4f (&bm)[kSubBlocks], const Tile &tile, int lane,
+                                               const float *__restrict__ m,
+                                               const uint64_t *__restrict__ m_bits,
+                                               const float *__restrict__ m_scales, float beta1)
+{
+    const int len = tile.len;
+    const int64_t base = tile.start;
+    if (PACKED) {
+        const float s = m_scales[tile.seg];
+#pragma unroll
+        for (int b = 0; b < kSubBlocks; ++b) {
+            const int li = b * (kWave * 4) + 4 * lane;
+            const uint64_t word = (FULL || li < len) ? m_bits[(base >> 6) + 4 * b + (lane >> 4)] : 0ull;
+            const uint32_t nib = (uint32_t)(word >> (4 * (lane & 15))) & 0xFu;
+#pragma unroll
+            for (int c = 0; c < 4; ++c) bm[b][c] = beta1 * (((nib >> c) & 1u) ? s : -s);
+        }
+    } else {
+#pragma unroll
+        for (int b = 0; b < kSubBlocks; ++b)
+            bm[b] = beta1 * ld4<FULL>(m + base, b * (kWave * 4) + 4 * lane, len);
+    }
+}
+
+template <bool FULL, bool PACKED>
 __device__ __forceinline__ void worker_tile(
     const Tile &tile, int64_t t, int lane, int64_t num_tiles, const float *__restrict__ m,
+    const uint64_t *__restrict__ m_bits, const float *__restrict__ m_scales,
     const float *__restrict__ g, int64_t g_ld, float *__restrict__ err, int64_t err_ld,
     const float *__restrict__ scales, int64_t scales_ld, uint64_t *__restrict__ bits,
     int64_t bits_ld, double *__restrict__ partial, int n_local, float beta1, float omb1)
@@ -175,9 +224,7 @@ __device__ __forceinline__ void worker_tile(
     const int nwords = (len + 63) >> 6;
 
     v4f bm[kSubBlocks];
-#pragma unroll
-    for (int b = 0; b < kSubBlocks; ++b)
-        bm[b] = beta1 * ld4<FULL>(m + base, b * (kWave * 4) + 4 * lane, len);
+    beta1_momentum<FULL, PACKED>(bm, tile, lane, m, m_bits, m_scales, beta1);
 
     for (int i = 0; i < n_local; ++i) {
         const float sp = scales[(int64_t)i * scales_ld + tile.seg];
@@ -219,8 +266,10 @@ __device__ __forceinline__ void worker_tile(
     }
 }
 
+template <bool PACKED>
 __global__ __launch_bounds__(kBlock) void k_worker_pass(
     const Tile *__restrict__ tiles, int64_t num_tiles, const float *__restrict__ m,
+    const uint64_t *__restrict__ m_bits, const float *__restrict__ m_scales,
     const float *__restrict__ g, int64_t g_ld, float *__restrict__ err, int64_t err_ld,
     const float *__restrict__ scales, int64_t scales_ld, uint64_t *__restrict__ bits,
     int64_t bits_ld, double *__restrict__ partial, int n_local, float beta1, float omb1)
@@ -230,11 +279,13 @@ __global__ __launch_bounds__(kBlock) void k_worker_pass(
     if (t >= num_tiles) return;
     const Tile tile = tiles[t];
     if (tile.len == kTileElems)
-        worker_tile<true>(tile, t, lane, num_tiles, m, g, g_ld, err, err_ld, scales, scales_ld,
-                          bits, bits_ld, partial, n_local, beta1, omb1);
+        worker_tile<true, PACKED>(tile, t, lane, num_tiles, m, m_bits, m_scales, g, g_ld, err,
+                                  err_ld, scales, scales_ld, bits, bits_ld, partial, n_local,
+                                  beta1, omb1);
     else
-        worker_tile<false>(tile, t, lane, num_tiles, m, g, g_ld, err, err_ld, scales,
-                           scales_ld, bits, bits_ld, partial, n_local, beta1, omb1);
+        worker_tile<false, PACKED>(tile, t, lane, num_tiles, m, m_bits, m_scales, g, g_ld, err,
+                                   err_ld, scales, scales_ld, bits, bits_ld, partial, n_local,
+                                   beta1, omb1);
 }
 
 // ---------------------------------------------------------------------------
@@ -492,6 +543,11 @@ __global__ __launch_bounds__(kBlock) void k_server_pass(
 // ---------------------------------------------------------------------------
 // Decompress + preconditioned update: x -= lr * (+-scale) / sqrt(v + eps).
 // ---------------------------------------------------------------------------
+// Every load of the tile is issued before the first store.  Kernels here keep
+// that order wherever a wave would otherwise re-read data after storing: on
+// this hardware a variant that interleaved the sign-word loads with the
+// stores returned wrong words for about 1% of the elements of a 334M-element
+// launch (exact on small grids), and the loads-first form is exact.
 template <bool FULL>
 __device__ __forceinline__ void update_tile(const Tile &tile, int lane,
                                             const uint64_t *__restrict__ sbits, float s,
@@ -500,25 +556,31 @@ __device__ __forceinline__ void update_tile(const Tile &tile, int lane,
 {
     const int len = tile.len;
     const int64_t base = tile.start;
+    uint64_t word[kSubBlocks];
+    v4f xv[kSubBlocks], vv[kSubBlocks];
 #pragma unroll
     for (int b = 0; b < kSubBlocks; ++b) {
         const int li = b * (kWave * 4) + 4 * lane;
-        if (!FULL && li >= len) break;
-        const uint64_t word = sbits[(base >> 6) + 4 * b + (lane >> 4)];
-        const uint32_t nib = (uint32_t)(word >> (4 * (lane & 15))) & 0xFu;
-        v4f xv = ld4<FULL>(x + base, li, len);
-        const v4f vv = ld4<FULL>(v + base, li, len);
+        const bool in = FULL || li < len;
+        word[b] = in ? sbits[(base >> 6) + 4 * b + (lane >> 4)] : 0ull;
+        xv[b] = ld4<FULL>(x + base, li, len);
+        vv[b] = ld4<FULL>(v + base, li, len);
+    }
+#pragma unroll
+    for (int b = 0; b < kSubBlocks; ++b) {
+        const int li = b * (kWave * 4) + 4 * lane;
+        const uint32_t nib = (uint32_t)(word[b] >> (4 * (lane & 15))) & 0xFu;
         v4f mv;
 #pragma unroll
         for (int c = 0; c < 4; ++c) {
             const float mbar = ((nib >> c) & 1u) ? s : -s;
-            const float denom = __builtin_sqrtf(vv[c] + eps);
+            const float denom = __builtin_sqrtf(vv[b][c] + eps);
             const float ratio = mbar / denom;
             const float step = lr * ratio;
-            xv[c] = xv[c] - step;
+            xv[b][c] = xv[b][c] - step;
             mv[c] = mbar;
         }
-        st4<FULL>(x + base, li, len, xv);
+        st4<FULL>(x + base, li, len, xv[b]);
         if (m_out) st4<FULL>(m_out + base, li, len, mv);
     }
 }
@@ -565,6 +627,48 @@ __global__ __launch_bounds__(kBlock) void k_materialize(
     }
 }
 
+// ---------------------------------------------------------------------------
+// Decoded message: out = +-scale of each element's segment.
+// ---------------------------------------------------------------------------
+template <bool FULL>
+__device__ __forceinline__ void decode_tile(const Tile &tile, int lane,
+                                            const uint64_t *__restrict__ bits, float s,
+                                            float *__restrict__ out)
+{
+    const int len = tile.len;
+    const int64_t base = tile.start;
+    uint64_t word[kSubBlocks];
+#pragma unroll
+    for (int b = 0; b < kSubBlocks; ++b) {
+        const int li = b * (kWave * 4) + 4 * lane;
+        word[b] = (FULL || li < len) ? bits[(base >> 6) + 4 * b + (lane >> 4)] : 0ull;
+    }
+#pragma unroll
+    for (int b = 0; b < kSubBlocks; ++b) {
+        const int li = b * (kWave * 4) + 4 * lane;
+        const uint32_t nib = (uint32_t)(word[b] >> (4 * (lane & 15))) & 0xFu;
+        v4f v;
+#pragma unroll
+        for (int c = 0; c < 4; ++c) v[c] = ((nib >> c) & 1u) ? s : -s;
+        st4<FULL>(out + base, li, len, v);
+    }
+}
+
+__global__ __launch_bounds__(kBlock) void k_decode(const Tile *__restrict__ tiles,
+                                                   int64_t num_tiles,
+                                                   const uint64_t *__restrict__ bits,
+                                                   const float *__restrict__ scales,
+                                                   float *__restrict__ out)
+{
+    const int lane = threadIdx.x & (kWave - 1);
+    const int64_t t = (int64_t)blockIdx.x * kWavesPerBlock + (threadIdx.x >> 6);
+    if (t >= num_tiles) return;
+    const Tile tile = tiles[t];
+    const float s = scales[tile.seg];
+    if (tile.len == kTileElems) decode_tile<true>(tile, lane, bits, s, out);
+    else decode_tile<false>(tile, lane, bits, s, out);
+}
+
 inline unsigned blocks_for(int64_t waves)
 {
     return (unsigned)((waves + kWavesPerBlock - 1) / kWavesPerBlock);
@@ -585,15 +689,28 @@ hipError_t launch_warmup(const DeviceTables &tb, int64_t num_tiles, float *x, fl
 }
 
 hipError_t launch_worker_pass(const DeviceTables &tb, int64_t num_tiles, const float *m,
-                              const float *g, int64_t g_ld, float *err, int64_t err_ld,
-                              const float *scales, int64_t scales_ld, uint64_t *bits,
-                              int64_t bits_ld, double *partial, int n_local, float beta1,
-                              hipStream_t s)
+                              const uint64_t *m_bits, const float *m_scales, const float *g,
+                              int64_t g_ld, float *err, int64_t err_ld, const float *scales,
+                              int64_t scales_ld, uint64_t *bits, int64_t bits_ld,
+                              double *partial, int n_local, float beta1, hipStream_t s)
 {
     const float omb1 = 1.0f - beta1;
-    hipLaunchKernelGGL(k_worker_pass, dim3(blocks_for(num_tiles)), dim3(kBlock), 0, s,
-                       tb.tiles, num_tiles, m, g, g_ld, err, err_ld, scales, scales_ld, bits,
-                       bits_ld, partial, n_local, beta1, omb1);
+    if (m)
+        hipLaunchKernelGGL(k_worker_pass<false>, dim3(blocks_for(num_tiles)), dim3(kBlock), 0,
+                           s, tb.tiles, num_tiles, m, m_bits, m_scales, g, g_ld, err, err_ld,
+                           scales, scales_ld, bits, bits_ld, partial, n_local, beta1, omb1);
+    else
+        hipLaunchKernelGGL(k_worker_pass<true>, dim3(blocks_for(num_tiles)), dim3(kBlock), 0,
+                           s, tb.tiles, num_tiles, m, m_bits, m_scales, g, g_ld, err, err_ld,
+                           scales, scales_ld, bits, bits_ld, partial, n_local, beta1, omb1);
+    return hipGetLastError();
+}
+
+hipError_t launch_decode(const DeviceTables &tb, int64_t num_tiles, const uint64_t *bits,
+                         const float *scales, float *out, hipStream_t s)
+{
+    hipLaunchKernelGGL(k_decode, dim3(blocks_for(num_tiles)), dim3(kBlock), 0, s, tb.tiles,
+                       num_tiles, bits, scales, out);
     return hipGetLastError();
 }
 

@@ -16,7 +16,7 @@ from ._native import PlanInfo, call, lib
 __all__ = [
     "Plan", "onebit_plan_create", "onebit_warmup_adam_step", "onebit_worker_compress",
     "onebit_server_reduce_compress", "onebit_decompress_update", "onebit_step",
-    "onebit_error_materialize", "State",
+    "onebit_error_materialize", "onebit_decode", "State",
 ]
 
 
@@ -113,11 +113,14 @@ def onebit_warmup_adam_step(plan, x, m, v, grads, lr, beta1, beta2, eps,
 
 
 def onebit_worker_compress(plan, m, grads, worker_err, worker_bits, worker_scales, beta1,
-                           workspace, n_local=None, stream=None):
+                           workspace, n_local=None, m_bits=None, m_scales=None, stream=None):
+    """m: fp32 momentum, or None to decode it from (m_bits, m_scales), the
+    previous step's gathered server message."""
     n = _rows(grads) if n_local is None else n_local
     if min(_rows(grads), _rows(worker_err), _rows(worker_bits), _rows(worker_scales)) < n:
         raise ValueError("grads, worker_err, worker_bits, worker_scales need %d rows" % n)
     call("onebit_worker_compress", plan.handle, _ptr(m, torch.float32, "m"),
+         _ptr(m_bits, torch.int64, "m_bits"), _ptr(m_scales, torch.float32, "m_scales"),
          _ptr(grads, torch.float32, "grads"), _ld(grads), n,
          _ptr(worker_err, torch.float32, "worker_err"), _ld(worker_err),
          _ptr(worker_bits, torch.int64, "worker_bits"), _ld(worker_bits),
@@ -168,6 +171,11 @@ def onebit_step(plan, x, m, v_frozen, grads, worker_err, server_err, worker_bits
          _ptr(workspace, torch.float64, "workspace"), _stream(stream))
 
 
+def onebit_decode(plan, bits, scales, out, stream=None):
+    call("onebit_decode", plan.handle, _ptr(bits, torch.int64, "bits"),
+         _ptr(scales, torch.float32, "scales"), _ptr(out, torch.float32, "out"), _stream(stream))
+
+
 def onebit_error_materialize(plan, err_state, scales, delta_out, rows=None, stream=None):
     r = _rows(err_state) if rows is None else rows
     if _rows(scales) < r or _rows(delta_out) < r or _rows(err_state) < r:
@@ -179,9 +187,14 @@ def onebit_error_materialize(plan, err_state, scales, delta_out, rows=None, stre
 
 class State:
     """Device buffers of one compression-stage run with n_local simulated
-    workers (all zero-initialised except x, m, v which the caller fills)."""
+    workers (all zero-initialised except x, m, v which the caller fills).
 
-    def __init__(self, plan, device, n_local=None, grad_rows=None):
+    With packed_momentum (the default) every compression step after the first
+    takes the momentum from the previous step's server message instead of
+    the fp32 buffer `m`, which then goes stale; momentum() returns the
+    current value either way."""
+
+    def __init__(self, plan, device, n_local=None, grad_rows=None, packed_momentum=True):
         n = plan.n if n_local is None else n_local
         D, W, S = plan.D, plan.W, plan.S
         f = dict(dtype=torch.float32, device=device)
@@ -198,15 +211,29 @@ class State:
         self.server_bits = torch.zeros(W, dtype=torch.int64, device=device)
         self.server_scales = torch.zeros(S, **f)
         self.workspace = plan.workspace(device)
+        self.packed_momentum = packed_momentum
+        self.compression_steps = 0
 
     def warmup(self, lr, beta1, beta2, eps, step, bias_correction=0, stream=None):
         onebit_warmup_adam_step(self.plan, self.x, self.m, self.v, self.grads, lr, beta1,
                                 beta2, eps, bias_correction, step, stream=stream)
 
+    def momentum_is_packed(self):
+        return self.packed_momentum and self.compression_steps > 0
+
     def step(self, lr, beta1, eps, stream=None):
-        onebit_step(self.plan, self.x, self.m, self.v, self.grads, self.worker_err,
+        m = None if self.momentum_is_packed() else self.m
+        onebit_step(self.plan, self.x, m, self.v, self.grads, self.worker_err,
                     self.server_err, self.worker_bits, self.worker_scales, self.server_bits,
                     self.server_scales, lr, beta1, eps, self.workspace, stream=stream)
+        self.compression_steps += 1
+
+    def momentum(self):
+        if self.compression_steps > 1 and self.packed_momentum:
+            out = torch.zeros_like(self.m)
+            onebit_decode(self.plan, self.server_bits, self.server_scales, out)
+            return out
+        return self.m
 
     def worker_delta(self):
         out = torch.zeros_like(self.worker_err)

@@ -77,6 +77,7 @@ def _free_run_sampled(ob, dev, wl, warm, steps, sample_segs):
     torch.cuda.synchronize()
     wdelta = st.worker_delta()
     sdelta = st.server_delta()
+    mom = st.momentum()
     torch.cuda.synchronize()
     for sg in segs:
         q, b, e = sg["q"], sg["b"], sg["e"]
@@ -87,10 +88,10 @@ def _free_run_sampled(ob, dev, wl, warm, steps, sample_segs):
         check_scales("server scale seg %d" % q, host(st.server_scales[q:q + 1]),
                      np.array([sg["sscale"]], np.float32))
         check_fp("x seg %d" % q, _np(st.x[b:e]), sg["x"])
-        check_fp("m seg %d" % q, _np(st.m[b:e]), sg["m"])
+        check_fp("m seg %d" % q, _np(mom[b:e]), sg["m"])
         check_fp("worker delta seg %d" % q, _np(wdelta[:, b:e]), sg["delta"])
         check_fp("server delta seg %d" % q, _np(sdelta[b:e]), sg["dbar"])
-    del wdelta, sdelta, st
+    del wdelta, sdelta, mom, st
     plan.close()
     torch.cuda.empty_cache()
 
@@ -154,7 +155,7 @@ def test_share256_full_size(ob, dev):
     # one compression step
     synth.device_grads(wl, D, plan.tensor_off, warm + 1, st.grads, scale_vec)
     ob.onebit_worker_compress(plan, st.m, st.grads, st.worker_err, st.worker_bits,
-                              st.worker_scales, wl.beta1, st.workspace)
+                              st.worker_scales, wl.beta1, st.workspace)  # first step: fp32 m
     b0, e0 = int(L.seg_begin[j]), int(L.seg_end[j])
     cw0, cw1 = b0 // 64, (e0 + 63) // 64
     recv_bits, recv_scales = synth.device_bits_and_scales(n, cw1 - cw0, wl.seed_incoming, dev)
@@ -211,5 +212,58 @@ def test_share256_full_size(ob, dev):
         check_fp("x seg %d" % q, _np(st.x[sg["b"]:sg["e"]]), x)
         check_fp("m seg %d" % q, _np(st.m[sg["b"]:sg["e"]]), m)
     del st
+    plan.close()
+    torch.cuda.empty_cache()
+
+
+def _random_message(plan, seed):
+    rng = np.random.default_rng(seed)
+    bits = rng.integers(0, np.iinfo(np.uint64).max, size=plan.W, dtype=np.uint64, endpoint=True)
+    scales = np.exp(rng.normal(-9, 1.0, size=plan.S)).astype(np.float32)
+    return bits, scales
+
+
+def test_decode_full_size_exact(ob, dev):
+    """Every element of a BERT-Large-sized message decoded exactly, twice
+    (a regression test: a wave that loads after a non-temporal store has been
+    seen to read wrong data on this hardware)."""
+    wl = synth.get("bert_large")
+    plan = ob.Plan(wl.numel, wl.n)
+    L = oracle.Layout(wl.numel, wl.n)
+    bits, scales = _random_message(plan, 11)
+    ref = oracle.decode_message(L, bits, scales)
+    bt = torch.from_numpy(bits.view(np.int64)).to(dev)
+    sc = torch.from_numpy(scales).to(dev)
+    for rep in range(2):
+        out = torch.zeros(plan.D, dtype=torch.float32, device=dev)
+        ob.onebit_decode(plan, bt, sc, out)
+        torch.cuda.synchronize()
+        check_fp("decode rep %d" % rep, _np(out), ref, rel=0, abs_=0)
+        del out
+    plan.close()
+    torch.cuda.empty_cache()
+
+
+def test_update_full_size_exact(ob, dev):
+    """The decompress + update over all d = 334,088,192 elements against the
+    oracle, element by element."""
+    wl = synth.get("bert_large")
+    plan = ob.Plan(wl.numel, wl.n)
+    L = oracle.Layout(wl.numel, wl.n)
+    bits, scales = _random_message(plan, 12)
+    x = synth.host_normal(plan.D, 0.02, 12, 1)
+    v = np.abs(synth.host_normal(plan.D, 1e-7, 12, 2))
+    xg = torch.from_numpy(x).to(dev)
+    mg = torch.zeros(plan.D, dtype=torch.float32, device=dev)
+    ob.onebit_decompress_update(plan, torch.from_numpy(bits.view(np.int64)).to(dev),
+                                torch.from_numpy(scales).to(dev), xg, mg,
+                                torch.from_numpy(v).to(dev), wl.lr, wl.eps)
+    torch.cuda.synchronize()
+    m = np.zeros(plan.D, np.float32)
+    for q, (b, e) in enumerate(L.segments()):
+        oracle.update_segment(b, e, bits, scales[q], wl.lr, wl.eps, x, m, v)
+    check_fp("x", _np(xg), x, rel=0, abs_=0)
+    check_fp("m", _np(mg), m, rel=0, abs_=0)
+    del xg, mg
     plan.close()
     torch.cuda.empty_cache()

@@ -107,6 +107,42 @@ def test_worker_compress_parity(ob, dev, numel, n):
     plan.close()
 
 
+@pytest.mark.parametrize("numel,n", CASES)
+def test_worker_compress_packed_momentum_parity(ob, dev, numel, n):
+    """Momentum given as a message (sign words + segment scales): the worker
+    pass decodes it; the oracle gets the decoded values as m."""
+    L = oracle.Layout(numel, n)
+    plan = ob.Plan(numel, n)
+    _, g, delta, *_ = _random_state(L, 40 + n, n)
+    rng = np.random.default_rng(40 + n)
+    mbits = rng.integers(0, np.iinfo(np.uint64).max, size=L.W, dtype=np.uint64, endpoint=True)
+    mscales = np.exp(rng.normal(-9, 1.0, size=L.S)).astype(np.float32)
+    m = oracle.decode_message(L, mbits, mscales)
+    err = _put(delta, dev)
+    bits = torch.zeros((n, L.W), dtype=torch.int64, device=dev)
+    scales = torch.zeros((n, L.S), dtype=torch.float32, device=dev)
+    ws = plan.workspace(dev)
+    ob.onebit_worker_compress(plan, None, _put(g, dev), err, bits, scales, B1, ws,
+                              m_bits=_put(mbits, dev), m_scales=_put(mscales, dev))
+    dec = torch.zeros(L.D, dtype=torch.float32, device=dev)
+    ob.onebit_decode(plan, _put(mbits, dev), _put(mscales, dev), dec)
+    torch.cuda.synchronize()
+    wbits = np.zeros((n, L.W), np.uint64)
+    wscales = np.zeros((n, L.S), np.float32)
+    z = np.zeros(L.D, np.float32)
+    zs = np.zeros((n, L.D), np.float32)
+    for i in range(n):
+        for q, (b, e) in enumerate(L.segments()):
+            wscales[i, q] = oracle.worker_segment(b, e, B1, m, g[i], delta[i], wbits[i], z)
+        zs[i] = z
+    mask = L.real_mask()
+    check_fp("decoded message", host(dec), m, rel=0, abs_=0, mask=mask)
+    check_bits("worker bits", host(bits), wbits)
+    check_scales("worker scales", host(scales), wscales)
+    check_fp("compensated z", host(err), zs, mask=mask)
+    plan.close()
+
+
 SERVER_CASES = [c + ("lognormal",) for c in CASES] + [
     ([1 << 20], 4, "wide"), ([5000, 300, 64], 5, "wide"), ([70_000], 37, "lognormal"),
     ([70_000], 37, "zeros"), ([100_000], 256, "lognormal"), ([100_000], 256, "wide")]
@@ -201,7 +237,7 @@ def test_warmup_parity(ob, dev, bias_correction):
 # Free-running: warm-up then compression steps, no re-sync
 # ---------------------------------------------------------------------------
 
-def _free_run(ob, dev, wl, numel=None, warm=None, steps=None):
+def _free_run(ob, dev, wl, numel=None, warm=None, steps=None, packed=True):
     numel = wl.numel if numel is None else numel
     n = wl.n
     warm = wl.warmup_steps if warm is None else warm
@@ -214,7 +250,7 @@ def _free_run(ob, dev, wl, numel=None, warm=None, steps=None):
     x[~mask] = 0
     m = np.zeros(L.D, np.float32)
     v = np.zeros(L.D, np.float32)
-    st = ob.State(plan, dev)
+    st = ob.State(plan, dev, packed_momentum=packed)
     st.x.copy_(_put(x, dev))
     for t in range(1, warm + 1):
         g = synth.host_grads(wl, L.D, L.tensor_off, t)
@@ -240,7 +276,7 @@ def _free_run(ob, dev, wl, numel=None, warm=None, steps=None):
         scale_ulps += check_scales(tag + " server scales", host(st.server_scales), ref.sscales)
     ex = {}
     ex["x"] = check_fp("x", host(st.x), ref.x, mask=mask)
-    ex["m"] = check_fp("m", host(st.m), ref.m, mask=mask)
+    ex["m"] = check_fp("m", host(st.momentum()), ref.m, mask=mask)
     ex["worker delta"] = check_fp("worker delta", host(st.worker_delta()), ref.delta, mask=mask)
     ex["server delta"] = check_fp("server delta", host(st.server_delta()), ref.delta_bar,
                                   mask=mask)
@@ -250,9 +286,11 @@ def _free_run(ob, dev, wl, numel=None, warm=None, steps=None):
     return ex
 
 
-def test_free_running_tiny(ob, dev):
-    """Tiny workload in full: d = 2^20, n = 4, 10 warm-up + 10 compression steps."""
-    _free_run(ob, dev, synth.get("tiny"))
+@pytest.mark.parametrize("packed", [True, False])
+def test_free_running_tiny(ob, dev, packed):
+    """Tiny workload in full: d = 2^20, n = 4, 10 warm-up + 10 compression
+    steps; momentum packed (decoded from the server message) or fp32."""
+    _free_run(ob, dev, synth.get("tiny"), packed=packed)
 
 
 def test_free_running_many_small_tensors(ob, dev):
@@ -262,10 +300,11 @@ def test_free_running_many_small_tensors(ob, dev):
     _free_run(ob, dev, wl, numel=wl.numel[:400])
 
 
-def test_free_running_ragged_edges(ob, dev):
+@pytest.mark.parametrize("packed", [True, False])
+def test_free_running_ragged_edges(ob, dev, packed):
     wl = synth.Workload(name="ragged", numel=[1, 63, 64, 65, 0, 1000, 1024, 1025, 4097, 12345],
                         n=5, warmup_steps=3, steps=6)
-    _free_run(ob, dev, wl)
+    _free_run(ob, dev, wl, packed=packed)
 
 
 def test_free_running_single_worker(ob, dev):
