@@ -124,13 +124,97 @@ def hbm_copy_probe(dev, nbytes=4 << 30, reps=10):
     return 2 * nbytes / (ms * 1e-3) / 1e9
 
 
+def bench_share(args, wl):
+    """One GPU's share of an n-worker step: the local worker's pass over all
+    d, the owner of one chunk reducing n incoming packed chunks (synthetic,
+    seeded), and the update over all d with the gathered message."""
+    import torch
+
+    import paper_2102_02888_amd as ob
+    import synth
+    dev = torch.device("cuda:0")
+    n, j = wl.n, wl.server_chunk
+    plan = ob.Plan(wl.numel, n)
+    st = ob.State(plan, dev, n_local=wl.n_local)
+    scale_vec = torch.from_numpy(synth.grad_scale_per_element(wl, plan.D, plan.tensor_off)).to(dev)
+    st.x.copy_(synth.device_params(wl, plan.D, dev))
+    for t in range(1, wl.warmup_steps + 1):
+        synth.device_grads(wl, plan.D, plan.tensor_off, t, st.grads, scale_vec)
+        st.warmup(wl.lr, wl.beta1, wl.beta2, wl.eps, t)
+    synth.device_grads(wl, plan.D, plan.tensor_off, wl.warmup_steps + 1, st.grads, scale_vec)
+    b0, e0 = int(plan.seg_begin[j]), int(plan.seg_end[j])
+    cw0, cw1 = b0 // 64, (e0 + 63) // 64
+    recv_bits, recv_scales = synth.device_bits_and_scales(n, cw1 - cw0, wl.seed_incoming, dev)
+    gath_bits, gath_scales = synth.device_bits_and_scales(1, plan.W, wl.seed_incoming + 1, dev)
+    st.server_bits.copy_(gath_bits[0])
+    st.server_scales.fill_(float(gath_scales[0]))
+    st.server_scales[j] = 0.0
+    torch.cuda.synchronize()
+
+    def one_step(ev=None, first=False):
+        if ev:
+            ev[0].record()
+        if first:
+            ob.onebit_worker_compress(plan, st.m, st.grads, st.worker_err, st.worker_bits,
+                                      st.worker_scales, wl.beta1, st.workspace)
+        else:
+            ob.onebit_worker_compress(plan, None, st.grads, st.worker_err, st.worker_bits,
+                                      st.worker_scales, wl.beta1, st.workspace,
+                                      m_bits=st.server_bits, m_scales=st.server_scales)
+        if ev:
+            ev[1].record()
+        ob.onebit_server_reduce_compress(plan, j, j + 1, recv_bits, recv_scales, st.server_err,
+                                         st.server_bits, st.server_scales, st.workspace,
+                                         bits_word_base=cw0, scales_seg_base=j, scales_ld=1)
+        if ev:
+            ev[2].record()
+        ob.onebit_decompress_update(plan, st.server_bits, st.server_scales, st.x, None, st.v,
+                                    wl.lr, wl.eps)
+        if ev:
+            ev[3].record()
+
+    one_step(first=True)
+    for _ in range(args.warmup):
+        one_step()
+    events = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for k in range(args.steps):
+        one_step(events[k])
+    torch.cuda.synchronize()
+    ms_step = (time.perf_counter() - t0) * 1e3 / args.steps
+    part_ms = [sum(ev[i].elapsed_time(ev[i + 1]) for ev in events) / args.steps for i in range(3)]
+    d = plan.d
+    chunk = e0 - b0
+    worker_b = d * (1 / 8 + 12.125)
+    server_b = chunk * (n / 8 + 8.125)
+    update_b = d * 12.125
+    step_b = worker_b + server_b + update_b
+    result = {
+        "metric": "compression-phase step params/sec (one GPU's share of a %d-worker step)" % n,
+        "value": d / (ms_step * 1e-3), "unit": "params/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": ms_step, "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "f32", "data": "synthetic",
+        "config": {"workload": wl.name, "d": d, "n_workers": n, "n_local": wl.n_local,
+                   "server_chunk": j, "chunk_len": chunk, "description": wl.description},
+        "step_hbm_gbps_algorithmic": step_b / (ms_step * 1e-3) / 1e9,
+        "step_frac_of_peak": step_b / (ms_step * 1e-3) / 1e9 / HBM_PEAK_GBPS,
+        "kernel_ms": {"worker_compress": part_ms[0], "server_reduce_compress": part_ms[1],
+                      "decompress_update": part_ms[2], "sum": sum(part_ms)},
+        "kernel_gbps_algorithmic": {"worker_compress": worker_b / (part_ms[0] * 1e-3) / 1e9,
+                                    "server_reduce_compress": server_b / (part_ms[1] * 1e-3) / 1e9,
+                                    "decompress_update": update_b / (part_ms[2] * 1e-3) / 1e9},
+    }
+    print(json.dumps(result), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__)
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="bert_large",
-                    choices=["tiny", "bert_base", "bert_large", "stress"])
+                    choices=["tiny", "bert_base", "bert_large", "stress", "share256"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-probe", action="store_true")
     args = ap.parse_args()
@@ -148,6 +232,8 @@ def main():
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     wl = synth.get(args.workload)
+    if wl.n_local is not None:
+        return bench_share(args, wl)
     n = wl.n
     plan = ob.Plan(wl.numel, n)
     log("workload %s: d=%d D=%d n=%d segments=%d tiles=%d" % (wl.name, plan.d, plan.D, n,
@@ -215,7 +301,9 @@ def main():
     worker_bytes = d * bw
     achieved = worker_bytes / (part_ms[0] * 1e-3) / 1e9
     result = {
-        "metric": "compression-phase step params/sec (1-bit Adam, BERT-Large-shaped)",
+        "metric": ("compression-phase step params/sec and achieved HBM GB/s vs peak, BERT-Large"
+                   if wl.name == "bert_large" else
+                   "compression-phase step params/sec and achieved HBM GB/s vs peak, %s" % wl.name),
         "value": d / (ms_step * 1e-3),
         "unit": "params/s",
         "n_gpus": 1,
