@@ -24,7 +24,7 @@ def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
-def algorithmic_bytes_per_param(n):
+def algorithmic_bytes_per_param(n, grad_bytes=4):
     """Bytes the method must move per parameter in a steady-state step, each
     input read once and each output written once (fp32 state, 1-bit
     messages).  The shared momentum is the previous step's server message
@@ -34,7 +34,7 @@ def algorithmic_bytes_per_param(n):
       server pass: n incoming sign bits, server error state read and written,
                    one sign bit written;
       update     : one sign bit read, x read and written, v read."""
-    worker = 1 / 8 + n * (4 + 4 + 4 + 1 / 8)
+    worker = 1 / 8 + n * (grad_bytes + 4 + 4 + 1 / 8)
     server = n / 8 + 4 + 4 + 1 / 8
     update = 1 / 8 + 4 + 4 + 4
     return worker, server, update
@@ -215,6 +215,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="bert_large",
                     choices=["tiny", "bert_base", "bert_large", "stress", "share256"])
+    ap.add_argument("--grad-dtype", default="f32", choices=["f32", "bf16", "f16"],
+                    help="gradient element type (16-bit gradients are widened exactly)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-probe", action="store_true")
     args = ap.parse_args()
@@ -238,7 +240,9 @@ def main():
     plan = ob.Plan(wl.numel, n)
     log("workload %s: d=%d D=%d n=%d segments=%d tiles=%d" % (wl.name, plan.d, plan.D, n,
                                                               plan.S, plan.T))
-    st = ob.State(plan, dev)
+    gdt = {"f32": torch.float32, "bf16": torch.bfloat16, "f16": torch.float16}[args.grad_dtype]
+    gbytes = {"f32": 4, "bf16": 2, "f16": 2}[args.grad_dtype]
+    st = ob.State(plan, dev, grad_dtype=gdt)
     scale_vec = torch.from_numpy(synth.grad_scale_per_element(wl, plan.D, plan.tensor_off)).to(dev)
     st.x.copy_(synth.device_params(wl, plan.D, dev))
 
@@ -295,7 +299,7 @@ def main():
                for j in range(3)]
     gpu_step_ms = sum(part_ms)
 
-    bw, bs, bu = algorithmic_bytes_per_param(n)
+    bw, bs, bu = algorithmic_bytes_per_param(n, gbytes)
     d = plan.d
     step_bytes = d * (bw + bs + bu)
     worker_bytes = d * bw
@@ -316,6 +320,7 @@ def main():
         "dtype": "f32",
         "data": "synthetic",
         "config": {"workload": wl.name, "d": d, "n_workers": n, "segments": plan.S,
+                   "grad_dtype": args.grad_dtype,
                    "tensors_shaped": len(wl.grad_scale_ranges or wl.numel),
                    "adam_warmup_steps": wl.warmup_steps, "description": wl.description},
         "step_hbm_gbps_algorithmic": step_bytes / (ms_step * 1e-3) / 1e9,

@@ -68,6 +68,12 @@ extern "C" {
 #define ONEBIT_EHIP (-3)   /* HIP runtime or launch error                    */
 #define ONEBIT_ENOMEM (-4) /* device allocation failed (plan creation only)  */
 
+/* Gradient element types.  16-bit gradients are widened to fp32 exactly on
+ * load, so every later operation is the fp32 arithmetic described above. */
+#define ONEBIT_GRAD_F32 0
+#define ONEBIT_GRAD_BF16 1
+#define ONEBIT_GRAD_F16 2
+
 typedef struct onebit_plan_s *onebit_plan;
 typedef struct ihipStream_t *onebit_stream; /* a hipStream_t */
 
@@ -111,12 +117,16 @@ int onebit_plan_get_layout(onebit_plan plan, int64_t *tensor_offset,
  * with m_hat = m, v_hat = v when bias_correction == 0 (the paper's choice)
  * and m_hat = m/(1-beta1^step), v_hat = v/(1-beta2^step) otherwise (step is
  * 1-based; the factors are computed in fp64 on the host and rounded to fp32).
- * x, m, v: in/out [D].  grads: n_grads rows of grad_ld >= D floats (n_grads =
- * 1 when the caller already holds the averaged gradient).  The v left after
+ * x, m, v: in/out [D].  grads: n_grads rows of grad_ld >= D elements of type
+ * grad_dtype (ONEBIT_GRAD_F32, _BF16 or _F16; 16-byte aligned for fp32, 8-byte
+ * for 16-bit types; n_grads = 1 when the caller already holds the averaged
+ * gradient).  The v left after
  * the last warm-up step is the frozen variance of the compression stage.
- * Errors: EINVAL (null, n_grads < 1, grad_ld < D, step < 1), EALIGN, EHIP. */
+ * Errors: EINVAL (null, n_grads < 1, grad_ld < D, step < 1, unknown
+ * grad_dtype), EALIGN, EHIP. */
 int onebit_warmup_adam_step(onebit_plan plan, float *x, float *m, float *v,
-                            const float *grads, int64_t grad_ld, int32_t n_grads,
+                            const void *grads, int32_t grad_dtype, int64_t grad_ld,
+                            int32_t n_grads,
                             float lr, float beta1, float beta2, float eps,
                             int32_t bias_correction, int64_t step,
                             onebit_stream stream);
@@ -132,7 +142,7 @@ int onebit_warmup_adam_step(onebit_plan plan, float *x, float *m, float *v,
  * its sign words m_bits [W] and segment scales m_scales [S] -- Algorithm 1
  * sets every worker's momentum to that decoded message, so it never has to be
  * stored as fp32 ("packed momentum"; 1/8 byte per element instead of 4).
- * grads: n_local rows of grad_ld >= D.  worker_err: in/out,
+ * grads: n_local rows of grad_ld >= D elements of type grad_dtype.  worker_err: in/out,
  * n_local rows of err_ld >= D (compensated form, see above).  worker_bits:
  * out, n_local rows of bits_ld >= W words.  worker_scales: in/out, n_local
  * rows of scales_ld >= S floats (in: the previous call's scales, which with
@@ -141,8 +151,8 @@ int onebit_warmup_adam_step(onebit_plan plan, float *x, float *m, float *v,
  * Errors: EINVAL (null, n_local < 1 or > n, a leading dim too small, m and
  * m_bits/m_scales both NULL), EALIGN, EHIP. */
 int onebit_worker_compress(onebit_plan plan, const float *m, const uint64_t *m_bits,
-                           const float *m_scales,
-                           const float *grads, int64_t grad_ld, int32_t n_local,
+                           const float *m_scales, const void *grads, int32_t grad_dtype,
+                           int64_t grad_ld, int32_t n_local,
                            float *worker_err, int64_t err_ld,
                            uint64_t *worker_bits, int64_t bits_ld,
                            float *worker_scales, int64_t scales_ld,
@@ -203,7 +213,7 @@ int onebit_decompress_update(onebit_plan plan, const uint64_t *server_bits,
  * server_scales [S] (in/out).
  * Errors: those of the three calls. */
 int onebit_step(onebit_plan plan, float *x, float *m, const float *v_frozen,
-                const float *grads, int64_t grad_ld, float *worker_err,
+                const void *grads, int32_t grad_dtype, int64_t grad_ld, float *worker_err,
                 int64_t err_ld, float *server_err, uint64_t *worker_bits,
                 float *worker_scales, uint64_t *server_bits, float *server_scales,
                 float lr, float beta1, float eps, void *workspace,

@@ -88,6 +88,16 @@ int check_u64(const void *ptr, const char *name)
     return ONEBIT_OK;
 }
 
+int check_grads(const void *g, int32_t dtype)
+{
+    if (!g) return fail(ONEBIT_EINVAL, "grads is NULL");
+    if (dtype != ONEBIT_GRAD_F32 && dtype != ONEBIT_GRAD_BF16 && dtype != ONEBIT_GRAD_F16)
+        return fail(ONEBIT_EINVAL, "grad_dtype %d is not one of ONEBIT_GRAD_*", dtype);
+    const size_t need = dtype == ONEBIT_GRAD_F32 ? 16 : 8;
+    if (!aligned(g, need)) return fail(ONEBIT_EALIGN, "grads is not %zu-byte aligned", need);
+    return ONEBIT_OK;
+}
+
 int check_ld(int64_t ld, int64_t need, bool mult4, const char *name)
 {
     if (ld < need) return fail(ONEBIT_EINVAL, "%s = %lld is below %lld", name, (long long)ld,
@@ -294,8 +304,9 @@ int onebit_plan_get_layout(onebit_plan p, int64_t *tensor_offset, int64_t *seg_b
     return ONEBIT_OK;
 }
 
-int onebit_warmup_adam_step(onebit_plan p, float *x, float *m, float *v, const float *grads,
-                            int64_t grad_ld, int32_t n_grads, float lr, float beta1,
+int onebit_warmup_adam_step(onebit_plan p, float *x, float *m, float *v, const void *grads,
+                            int32_t grad_dtype, int64_t grad_ld, int32_t n_grads, float lr,
+                            float beta1,
                             float beta2, float eps, int32_t bias_correction, int64_t step,
                             onebit_stream stream)
 {
@@ -303,7 +314,7 @@ int onebit_warmup_adam_step(onebit_plan p, float *x, float *m, float *v, const f
     TRY(check_f32(x, "x"));
     TRY(check_f32(m, "m"));
     TRY(check_f32(v, "v"));
-    TRY(check_f32(grads, "grads"));
+    TRY(check_grads(grads, grad_dtype));
     if (n_grads < 1) return fail(ONEBIT_EINVAL, "n_grads < 1");
     if (step < 1) return fail(ONEBIT_EINVAL, "step < 1 (steps are 1-based)");
     TRY(check_ld(grad_ld, p->D, n_grads > 1, "grad_ld"));
@@ -313,7 +324,8 @@ int onebit_warmup_adam_step(onebit_plan p, float *x, float *m, float *v, const f
         bc1 = (float)(1.0 - std::pow((double)beta1, (double)step));
         bc2 = (float)(1.0 - std::pow((double)beta2, (double)step));
     }
-    TRY_HIP(onebit::launch_warmup(p->tb, p->T, x, m, v, grads, grad_ld, n_grads, lr, beta1,
+    TRY_HIP(onebit::launch_warmup(p->tb, p->T, x, m, v, grads, grad_dtype, grad_ld, n_grads, lr,
+                                  beta1,
                                   beta2, eps, bias_correction ? 1 : 0, bc1, bc2,
                                   (hipStream_t)stream),
             "warm-up kernel launch");
@@ -321,8 +333,8 @@ int onebit_warmup_adam_step(onebit_plan p, float *x, float *m, float *v, const f
 }
 
 int onebit_worker_compress(onebit_plan p, const float *m, const uint64_t *m_bits,
-                           const float *m_scales, const float *grads, int64_t grad_ld,
-                           int32_t n_local, float *worker_err, int64_t err_ld,
+                           const float *m_scales, const void *grads, int32_t grad_dtype,
+                           int64_t grad_ld, int32_t n_local, float *worker_err, int64_t err_ld,
                            uint64_t *worker_bits, int64_t bits_ld, float *worker_scales,
                            int64_t scales_ld, float beta1, void *workspace,
                            onebit_stream stream)
@@ -335,7 +347,7 @@ int onebit_worker_compress(onebit_plan p, const float *m, const uint64_t *m_bits
         if (!m_scales) return fail(ONEBIT_EINVAL, "m_scales is NULL (m is NULL)");
         if (!aligned(m_scales, 4)) return fail(ONEBIT_EALIGN, "m_scales misaligned");
     }
-    TRY(check_f32(grads, "grads"));
+    TRY(check_grads(grads, grad_dtype));
     TRY(check_f32(worker_err, "worker_err"));
     TRY(check_u64(worker_bits, "worker_bits"));
     if (!worker_scales) return fail(ONEBIT_EINVAL, "worker_scales is NULL");
@@ -351,8 +363,8 @@ int onebit_worker_compress(onebit_plan p, const float *m, const uint64_t *m_bits
     if (p->T == 0) return ONEBIT_OK;
     double *part = (double *)((char *)workspace + worker_partial_offset(p));
     hipStream_t s = (hipStream_t)stream;
-    TRY_HIP(onebit::launch_worker_pass(p->tb, p->T, m, m_bits, m_scales, grads, grad_ld,
-                                       worker_err, err_ld, worker_scales, scales_ld,
+    TRY_HIP(onebit::launch_worker_pass(p->tb, p->T, m, m_bits, m_scales, grads, grad_dtype,
+                                       grad_ld, worker_err, err_ld, worker_scales, scales_ld,
                                        worker_bits, bits_ld, part, n_local, beta1, s),
             "worker kernel launch");
     TRY_HIP(onebit::launch_finalize(p->tb, p->max_seg_tiles, (int64_t)n_local * p->S, p->S, 0,
@@ -434,8 +446,8 @@ int onebit_decompress_update(onebit_plan p, const uint64_t *server_bits,
     return ONEBIT_OK;
 }
 
-int onebit_step(onebit_plan p, float *x, float *m, const float *v_frozen, const float *grads,
-                int64_t grad_ld, float *worker_err, int64_t err_ld, float *server_err,
+int onebit_step(onebit_plan p, float *x, float *m, const float *v_frozen, const void *grads,
+                int32_t grad_dtype, int64_t grad_ld, float *worker_err, int64_t err_ld, float *server_err,
                 uint64_t *worker_bits, float *worker_scales, uint64_t *server_bits,
                 float *server_scales, float lr, float beta1, float eps, void *workspace,
                 onebit_stream stream)
@@ -449,7 +461,7 @@ int onebit_step(onebit_plan p, float *x, float *m, const float *v_frozen, const 
     TRY(check_u64(server_bits, "server_bits"));
     if (!server_scales) return fail(ONEBIT_EINVAL, "server_scales is NULL");
     if (!aligned(server_scales, 4)) return fail(ONEBIT_EALIGN, "server_scales misaligned");
-    TRY(onebit_worker_compress(p, m, server_bits, server_scales, grads, grad_ld, p->n,
+    TRY(onebit_worker_compress(p, m, server_bits, server_scales, grads, grad_dtype, grad_ld, p->n,
                                worker_err, err_ld, worker_bits, p->W, worker_scales, p->S,
                                beta1, workspace, stream));
     TRY(onebit_server_reduce_compress(p, 0, p->n, worker_bits, p->W, 0, worker_scales, p->S, 0,

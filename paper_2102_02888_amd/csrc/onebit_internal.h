@@ -31,17 +31,23 @@ struct DeviceTables {
     const int64_t *seg_len;        // [S]
 };
 
+// Gradient element types (the values of the ONEBIT_GRAD_* constants).
+constexpr int kGradF32 = 0;
+constexpr int kGradBF16 = 1;
+constexpr int kGradF16 = 2;
+
 hipError_t launch_warmup(const DeviceTables &tb, int64_t num_tiles, float *x, float *m,
-                         float *v, const float *g, int64_t g_ld, int n_grads, float lr,
-                         float beta1, float beta2, float eps, int use_bc, float bc1,
+                         float *v, const void *g, int grad_dtype, int64_t g_ld, int n_grads,
+                         float lr, float beta1, float beta2, float eps, int use_bc, float bc1,
                          float bc2, hipStream_t s);
 
 // m != NULL: fp32 momentum; m == NULL: momentum decoded from (m_bits, m_scales).
 hipError_t launch_worker_pass(const DeviceTables &tb, int64_t num_tiles, const float *m,
-                              const uint64_t *m_bits, const float *m_scales, const float *g,
-                              int64_t g_ld, float *err, int64_t err_ld, const float *scales,
-                              int64_t scales_ld, uint64_t *bits, int64_t bits_ld,
-                              double *partial, int n_local, float beta1, hipStream_t s);
+                              const uint64_t *m_bits, const float *m_scales, const void *g,
+                              int grad_dtype, int64_t g_ld, float *err, int64_t err_ld,
+                              const float *scales, int64_t scales_ld, uint64_t *bits,
+                              int64_t bits_ld, double *partial, int n_local, float beta1,
+                              hipStream_t s);
 
 hipError_t launch_decode(const DeviceTables &tb, int64_t num_tiles, const uint64_t *bits,
                          const float *scales, float *out, hipStream_t s);

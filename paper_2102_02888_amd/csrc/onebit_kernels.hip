@@ -59,6 +59,52 @@ __device__ __forceinline__ void st4(float *__restrict__ p, int li, int len, v4f 
     if (li + 2 < len) p[li + 2] = v.z;
 }
 
+// Gradient element types.  16-bit gradients are widened to fp32 exactly
+// (bf16 by a 16-bit shift, fp16 by the hardware conversion), so the method's
+// arithmetic is the same as for fp32 gradients of those values.
+struct GradF32 {
+    using T = float;
+};
+struct GradBF16 {
+    using T = uint16_t;
+};
+struct GradF16 {
+    using T = _Float16;
+};
+
+__device__ __forceinline__ float widen(uint16_t a) { return __uint_as_float((uint32_t)a << 16); }
+__device__ __forceinline__ float widen(_Float16 a) { return (float)a; }
+
+typedef uint16_t v4u16 __attribute__((ext_vector_type(4)));
+typedef _Float16 v4f16 __attribute__((ext_vector_type(4)));
+
+// Gradient elements li..li+3 as fp32 (zeros past len when !FULL).
+template <bool FULL, class G>
+__device__ __forceinline__ v4f ldg4(const typename G::T *__restrict__ p, int li, int len)
+{
+    if constexpr (sizeof(typename G::T) == 4) {
+        return ld4<FULL>((const float *)p, li, len);
+    } else {
+        v4f r = {0.f, 0.f, 0.f, 0.f};
+        if (FULL || li + 4 <= len) {
+            if constexpr (sizeof(typename G::T) == 2 && __is_same(typename G::T, uint16_t)) {
+                const v4u16 h = __builtin_nontemporal_load((const v4u16 *)(p + li));
+#pragma unroll
+                for (int c = 0; c < 4; ++c) r[c] = widen((uint16_t)h[c]);
+            } else {
+                const v4f16 h = __builtin_nontemporal_load((const v4f16 *)(p + li));
+#pragma unroll
+                for (int c = 0; c < 4; ++c) r[c] = widen((_Float16)h[c]);
+            }
+            return r;
+        }
+        if (li < len) r.x = widen(p[li]);
+        if (li + 1 < len) r.y = widen(p[li + 1]);
+        if (li + 2 < len) r.z = widen(p[li + 2]);
+        return r;
+    }
+}
+
 // OR of a 32-bit value over the 16 lanes of each DPP row (every lane of the
 // row receives the result).  xor-1 and xor-2 quad permutes OR each quad; the
 // row rotations by 4 and by 8 then OR the four quads, whichever way the
@@ -97,10 +143,10 @@ __device__ __forceinline__ float error_of(float z, float s) { return z >= 0.f ? 
 // ---------------------------------------------------------------------------
 // Warm-up Adam (eq. (alg:v)) on the average of n_grads gradient rows.
 // ---------------------------------------------------------------------------
-template <bool FULL>
+template <bool FULL, class G>
 __device__ __forceinline__ void warmup_tile(const Tile &tile, int lane, float *__restrict__ x,
                                             float *__restrict__ m, float *__restrict__ v,
-                                            const float *__restrict__ g, int64_t g_ld,
+                                            const typename G::T *__restrict__ g, int64_t g_ld,
                                             int n_grads, float lr, float beta1, float omb1,
                                             float beta2, float omb2, float eps, int use_bc,
                                             float bc1, float bc2)
@@ -117,7 +163,7 @@ __device__ __forceinline__ void warmup_tile(const Tile &tile, int lane, float *_
     for (int i = 0; i < n_grads; ++i) {
 #pragma unroll
         for (int b = 0; b < kSubBlocks; ++b) {
-            const v4f gv = ld4<FULL>(g + (int64_t)i * g_ld + base, b * (kWave * 4) + 4 * lane, len);
+            const v4f gv = ldg4<FULL, G>(g + (int64_t)i * g_ld + base, b * (kWave * 4) + 4 * lane, len);
 #pragma unroll
             for (int c = 0; c < 4; ++c) sum[b][c] += (double)gv[c];
         }
@@ -159,9 +205,10 @@ __device__ __forceinline__ void warmup_tile(const Tile &tile, int lane, float *_
     }
 }
 
+template <class G>
 __global__ __launch_bounds__(kBlock) void k_warmup(
     const Tile *__restrict__ tiles, int64_t num_tiles, float *__restrict__ x,
-    float *__restrict__ m, float *__restrict__ v, const float *__restrict__ g, int64_t g_ld,
+    float *__restrict__ m, float *__restrict__ v, const typename G::T *__restrict__ g, int64_t g_ld,
     int n_grads, float lr, float beta1, float omb1, float beta2, float omb2, float eps,
     int use_bc, float bc1, float bc2)
 {
@@ -170,10 +217,10 @@ __global__ __launch_bounds__(kBlock) void k_warmup(
     if (t >= num_tiles) return;
     const Tile tile = tiles[t];
     if (tile.len == kTileElems)
-        warmup_tile<true>(tile, lane, x, m, v, g, g_ld, n_grads, lr, beta1, omb1, beta2, omb2,
+        warmup_tile<true, G>(tile, lane, x, m, v, g, g_ld, n_grads, lr, beta1, omb1, beta2, omb2,
                           eps, use_bc, bc1, bc2);
     else
-        warmup_tile<false>(tile, lane, x, m, v, g, g_ld, n_grads, lr, beta1, omb1, beta2, omb2,
+        warmup_tile<false, G>(tile, lane, x, m, v, g, g_ld, n_grads, lr, beta1, omb1, beta2, omb2,
                            eps, use_bc, bc1, bc2);
 }
 
@@ -211,11 +258,11 @@ __device__ __forceinline__ void beta1_momentum(v4f (&bm)[kSubBlocks], const Tile
     }
 }
 
-template <bool FULL, bool PACKED>
+template <bool FULL, bool PACKED, class G>
 __device__ __forceinline__ void worker_tile(
     const Tile &tile, int64_t t, int lane, int64_t num_tiles, const float *__restrict__ m,
     const uint64_t *__restrict__ m_bits, const float *__restrict__ m_scales,
-    const float *__restrict__ g, int64_t g_ld, float *__restrict__ err, int64_t err_ld,
+    const typename G::T *__restrict__ g, int64_t g_ld, float *__restrict__ err, int64_t err_ld,
     const float *__restrict__ scales, int64_t scales_ld, uint64_t *__restrict__ bits,
     int64_t bits_ld, double *__restrict__ partial, int n_local, float beta1, float omb1)
 {
@@ -228,14 +275,14 @@ __device__ __forceinline__ void worker_tile(
 
     for (int i = 0; i < n_local; ++i) {
         const float sp = scales[(int64_t)i * scales_ld + tile.seg];
-        const float *gi = g + (int64_t)i * g_ld + base;
+        const typename G::T *gi = g + (int64_t)i * g_ld + base;
         float *ei = err + (int64_t)i * err_ld + base;
         uint64_t *bi = bits + (int64_t)i * bits_ld + (base >> 6);
         v4f gv[kSubBlocks], cv[kSubBlocks];
 #pragma unroll
         for (int b = 0; b < kSubBlocks; ++b) {
             const int li = b * (kWave * 4) + 4 * lane;
-            gv[b] = ld4<FULL>(gi, li, len);
+            gv[b] = ldg4<FULL, G>(gi, li, len);
             cv[b] = ld4<FULL>(ei, li, len);
         }
         double acc = 0.0;
@@ -266,11 +313,11 @@ __device__ __forceinline__ void worker_tile(
     }
 }
 
-template <bool PACKED>
+template <bool PACKED, class G>
 __global__ __launch_bounds__(kBlock) void k_worker_pass(
     const Tile *__restrict__ tiles, int64_t num_tiles, const float *__restrict__ m,
     const uint64_t *__restrict__ m_bits, const float *__restrict__ m_scales,
-    const float *__restrict__ g, int64_t g_ld, float *__restrict__ err, int64_t err_ld,
+    const typename G::T *__restrict__ g, int64_t g_ld, float *__restrict__ err, int64_t err_ld,
     const float *__restrict__ scales, int64_t scales_ld, uint64_t *__restrict__ bits,
     int64_t bits_ld, double *__restrict__ partial, int n_local, float beta1, float omb1)
 {
@@ -279,11 +326,11 @@ __global__ __launch_bounds__(kBlock) void k_worker_pass(
     if (t >= num_tiles) return;
     const Tile tile = tiles[t];
     if (tile.len == kTileElems)
-        worker_tile<true, PACKED>(tile, t, lane, num_tiles, m, m_bits, m_scales, g, g_ld, err,
+        worker_tile<true, PACKED, G>(tile, t, lane, num_tiles, m, m_bits, m_scales, g, g_ld, err,
                                   err_ld, scales, scales_ld, bits, bits_ld, partial, n_local,
                                   beta1, omb1);
     else
-        worker_tile<false, PACKED>(tile, t, lane, num_tiles, m, m_bits, m_scales, g, g_ld, err,
+        worker_tile<false, PACKED, G>(tile, t, lane, num_tiles, m, m_bits, m_scales, g, g_ld, err,
                                    err_ld, scales, scales_ld, bits, bits_ld, partial, n_local,
                                    beta1, omb1);
 }
@@ -676,33 +723,86 @@ inline unsigned blocks_for(int64_t waves)
 
 }  // namespace
 
-hipError_t launch_warmup(const DeviceTables &tb, int64_t num_tiles, float *x, float *m,
-                         float *v, const float *g, int64_t g_ld, int n_grads, float lr,
-                         float beta1, float beta2, float eps, int use_bc, float bc1,
-                         float bc2, hipStream_t s)
+template <class G>
+static hipError_t launch_warmup_t(const DeviceTables &tb, int64_t num_tiles, float *x, float *m,
+                                  float *v, const void *g, int64_t g_ld, int n_grads, float lr,
+                                  float beta1, float beta2, float eps, int use_bc, float bc1,
+                                  float bc2, hipStream_t s)
 {
     const float omb1 = 1.0f - beta1, omb2 = 1.0f - beta2;
-    hipLaunchKernelGGL(k_warmup, dim3(blocks_for(num_tiles)), dim3(kBlock), 0, s, tb.tiles,
-                       num_tiles, x, m, v, g, g_ld, n_grads, lr, beta1, omb1, beta2, omb2,
-                       eps, use_bc, bc1, bc2);
+    hipLaunchKernelGGL(k_warmup<G>, dim3(blocks_for(num_tiles)), dim3(kBlock), 0, s, tb.tiles,
+                       num_tiles, x, m, v, (const typename G::T *)g, g_ld, n_grads, lr, beta1,
+                       omb1, beta2, omb2, eps, use_bc, bc1, bc2);
     return hipGetLastError();
 }
 
-hipError_t launch_worker_pass(const DeviceTables &tb, int64_t num_tiles, const float *m,
-                              const uint64_t *m_bits, const float *m_scales, const float *g,
-                              int64_t g_ld, float *err, int64_t err_ld, const float *scales,
-                              int64_t scales_ld, uint64_t *bits, int64_t bits_ld,
-                              double *partial, int n_local, float beta1, hipStream_t s)
+hipError_t launch_warmup(const DeviceTables &tb, int64_t num_tiles, float *x, float *m,
+                         float *v, const void *g, int grad_dtype, int64_t g_ld, int n_grads,
+                         float lr, float beta1, float beta2, float eps, int use_bc, float bc1,
+                         float bc2, hipStream_t s)
+{
+    switch (grad_dtype) {
+    case kGradBF16:
+        return launch_warmup_t<GradBF16>(tb, num_tiles, x, m, v, g, g_ld, n_grads, lr, beta1,
+                                         beta2, eps, use_bc, bc1, bc2, s);
+    case kGradF16:
+        return launch_warmup_t<GradF16>(tb, num_tiles, x, m, v, g, g_ld, n_grads, lr, beta1,
+                                        beta2, eps, use_bc, bc1, bc2, s);
+    default:
+        return launch_warmup_t<GradF32>(tb, num_tiles, x, m, v, g, g_ld, n_grads, lr, beta1,
+                                        beta2, eps, use_bc, bc1, bc2, s);
+    }
+}
+
+template <bool PACKED, class G>
+static void launch_worker_t(const DeviceTables &tb, int64_t num_tiles, const float *m,
+                            const uint64_t *m_bits, const float *m_scales, const void *g,
+                            int64_t g_ld, float *err, int64_t err_ld, const float *scales,
+                            int64_t scales_ld, uint64_t *bits, int64_t bits_ld, double *partial,
+                            int n_local, float beta1, hipStream_t s)
 {
     const float omb1 = 1.0f - beta1;
+    hipLaunchKernelGGL((k_worker_pass<PACKED, G>), dim3(blocks_for(num_tiles)), dim3(kBlock), 0,
+                       s, tb.tiles, num_tiles, m, m_bits, m_scales, (const typename G::T *)g,
+                       g_ld, err, err_ld, scales, scales_ld, bits, bits_ld, partial, n_local,
+                       beta1, omb1);
+}
+
+template <class G>
+static void launch_worker_g(const DeviceTables &tb, int64_t num_tiles, const float *m,
+                            const uint64_t *m_bits, const float *m_scales, const void *g,
+                            int64_t g_ld, float *err, int64_t err_ld, const float *scales,
+                            int64_t scales_ld, uint64_t *bits, int64_t bits_ld, double *partial,
+                            int n_local, float beta1, hipStream_t s)
+{
     if (m)
-        hipLaunchKernelGGL(k_worker_pass<false>, dim3(blocks_for(num_tiles)), dim3(kBlock), 0,
-                           s, tb.tiles, num_tiles, m, m_bits, m_scales, g, g_ld, err, err_ld,
-                           scales, scales_ld, bits, bits_ld, partial, n_local, beta1, omb1);
+        launch_worker_t<false, G>(tb, num_tiles, m, m_bits, m_scales, g, g_ld, err, err_ld,
+                                  scales, scales_ld, bits, bits_ld, partial, n_local, beta1, s);
     else
-        hipLaunchKernelGGL(k_worker_pass<true>, dim3(blocks_for(num_tiles)), dim3(kBlock), 0,
-                           s, tb.tiles, num_tiles, m, m_bits, m_scales, g, g_ld, err, err_ld,
-                           scales, scales_ld, bits, bits_ld, partial, n_local, beta1, omb1);
+        launch_worker_t<true, G>(tb, num_tiles, m, m_bits, m_scales, g, g_ld, err, err_ld,
+                                 scales, scales_ld, bits, bits_ld, partial, n_local, beta1, s);
+}
+
+hipError_t launch_worker_pass(const DeviceTables &tb, int64_t num_tiles, const float *m,
+                              const uint64_t *m_bits, const float *m_scales, const void *g,
+                              int grad_dtype, int64_t g_ld, float *err, int64_t err_ld,
+                              const float *scales, int64_t scales_ld, uint64_t *bits,
+                              int64_t bits_ld, double *partial, int n_local, float beta1,
+                              hipStream_t s)
+{
+    switch (grad_dtype) {
+    case kGradBF16:
+        launch_worker_g<GradBF16>(tb, num_tiles, m, m_bits, m_scales, g, g_ld, err, err_ld,
+                                  scales, scales_ld, bits, bits_ld, partial, n_local, beta1, s);
+        break;
+    case kGradF16:
+        launch_worker_g<GradF16>(tb, num_tiles, m, m_bits, m_scales, g, g_ld, err, err_ld,
+                                 scales, scales_ld, bits, bits_ld, partial, n_local, beta1, s);
+        break;
+    default:
+        launch_worker_g<GradF32>(tb, num_tiles, m, m_bits, m_scales, g, g_ld, err, err_ld,
+                                 scales, scales_ld, bits, bits_ld, partial, n_local, beta1, s);
+    }
     return hipGetLastError();
 }
 

@@ -39,6 +39,16 @@ def _ptr(t, dtype, name):
     return ctypes.c_void_p(t.data_ptr())
 
 
+_GRAD_DTYPES = {torch.float32: 0, torch.bfloat16: 1, torch.float16: 2}
+
+
+def _grads(t):
+    """(pointer, ONEBIT_GRAD_* code) of a gradient tensor."""
+    if not isinstance(t, torch.Tensor) or t.dtype not in _GRAD_DTYPES:
+        raise TypeError("grads must be a float32, bfloat16 or float16 tensor")
+    return _ptr(t, t.dtype, "grads"), _GRAD_DTYPES[t.dtype]
+
+
 def _ld(t):
     return t.stride(0) if t.dim() == 2 else t.numel()
 
@@ -108,7 +118,7 @@ def onebit_warmup_adam_step(plan, x, m, v, grads, lr, beta1, beta2, eps,
         raise ValueError("grads has fewer than %d rows" % n)
     call("onebit_warmup_adam_step", plan.handle, _ptr(x, torch.float32, "x"),
          _ptr(m, torch.float32, "m"), _ptr(v, torch.float32, "v"),
-         _ptr(grads, torch.float32, "grads"), _ld(grads), n, lr, beta1, beta2, eps,
+         *_grads(grads), _ld(grads), n, lr, beta1, beta2, eps,
          int(bias_correction), int(step), _stream(stream))
 
 
@@ -121,7 +131,7 @@ def onebit_worker_compress(plan, m, grads, worker_err, worker_bits, worker_scale
         raise ValueError("grads, worker_err, worker_bits, worker_scales need %d rows" % n)
     call("onebit_worker_compress", plan.handle, _ptr(m, torch.float32, "m"),
          _ptr(m_bits, torch.int64, "m_bits"), _ptr(m_scales, torch.float32, "m_scales"),
-         _ptr(grads, torch.float32, "grads"), _ld(grads), n,
+         *_grads(grads), _ld(grads), n,
          _ptr(worker_err, torch.float32, "worker_err"), _ld(worker_err),
          _ptr(worker_bits, torch.int64, "worker_bits"), _ld(worker_bits),
          _ptr(worker_scales, torch.float32, "worker_scales"), _ld(worker_scales),
@@ -161,7 +171,7 @@ def onebit_step(plan, x, m, v_frozen, grads, worker_err, server_err, worker_bits
     if min(_rows(grads), _rows(worker_err), _rows(worker_bits), _rows(worker_scales)) < plan.n:
         raise ValueError("grads, worker_err, worker_bits, worker_scales need %d rows" % plan.n)
     call("onebit_step", plan.handle, _ptr(x, torch.float32, "x"), _ptr(m, torch.float32, "m"),
-         _ptr(v_frozen, torch.float32, "v_frozen"), _ptr(grads, torch.float32, "grads"),
+         _ptr(v_frozen, torch.float32, "v_frozen"), *_grads(grads),
          _ld(grads), _ptr(worker_err, torch.float32, "worker_err"), _ld(worker_err),
          _ptr(server_err, torch.float32, "server_err"),
          _ptr(worker_bits, torch.int64, "worker_bits"),
@@ -194,7 +204,8 @@ class State:
     the fp32 buffer `m`, which then goes stale; momentum() returns the
     current value either way."""
 
-    def __init__(self, plan, device, n_local=None, grad_rows=None, packed_momentum=True):
+    def __init__(self, plan, device, n_local=None, grad_rows=None, packed_momentum=True,
+                 grad_dtype=torch.float32):
         n = plan.n if n_local is None else n_local
         D, W, S = plan.D, plan.W, plan.S
         f = dict(dtype=torch.float32, device=device)
@@ -203,7 +214,8 @@ class State:
         self.x = torch.zeros(D, **f)
         self.m = torch.zeros(D, **f)
         self.v = torch.zeros(D, **f)
-        self.grads = torch.zeros((n if grad_rows is None else grad_rows, D), **f)
+        self.grads = torch.zeros((n if grad_rows is None else grad_rows, D), dtype=grad_dtype,
+                                 device=device)
         self.worker_err = torch.zeros((n, D), **f)
         self.worker_bits = torch.zeros((n, W), dtype=torch.int64, device=device)
         self.worker_scales = torch.zeros((n, S), **f)

@@ -74,8 +74,10 @@ def test_argument_errors_before_device(native):
         assert getattr(lib, fn)(None) == -1
     assert lib.onebit_plan_get_info(None, None) == -1
     assert lib.onebit_decompress_update(None, None, None, None, None, None, 0.0, 0.0, None) == -1
-    assert lib.onebit_step(None, *([None] * 4), 0, None, 0, *([None] * 5), 0.0, 0.0, 0.0,
+    assert lib.onebit_step(None, *([None] * 4), 0, 0, None, 0, *([None] * 5), 0.0, 0.0, 0.0,
                            None, None) == -1
+    assert lib.onebit_worker_compress(None, None, None, None, None, 0, 0, 1, None, 0, None, 0,
+                                      None, 0, 0.9, None, None) == -1
 
 
 def test_binding_fails_loudly_without_library(tmp_path, monkeypatch):

@@ -25,17 +25,19 @@ def ob():
 
 
 def _np(t):
+    if t.dtype in (torch.bfloat16, torch.float16):
+        t = t.float()
     return np.ascontiguousarray(t.detach().cpu().numpy())
 
 
-def _free_run_sampled(ob, dev, wl, warm, steps, sample_segs):
+def _free_run_sampled(ob, dev, wl, warm, steps, sample_segs, grad_dtype=torch.float32):
     n = wl.n
     plan = ob.Plan(wl.numel, n)
     L = oracle.Layout(wl.numel, n)
     assert (plan.D, plan.W, plan.S) == (L.D, L.W, L.S)
     np.testing.assert_array_equal(plan.seg_begin, L.seg_begin)
     np.testing.assert_array_equal(plan.seg_end, L.seg_end)
-    st = ob.State(plan, dev)
+    st = ob.State(plan, dev, grad_dtype=grad_dtype)
     scale_vec = torch.from_numpy(synth.grad_scale_per_element(wl, plan.D, plan.tensor_off)).to(dev)
     st.x.copy_(synth.device_params(wl, plan.D, dev))
     segs = []
@@ -99,6 +101,12 @@ def _free_run_sampled(ob, dev, wl, warm, steps, sample_segs):
 def test_bert_large_full_size(ob, dev):
     """d = 334,088,192, n = 32: first and last of the 32 chunks."""
     _free_run_sampled(ob, dev, synth.get("bert_large"), warm=2, steps=2, sample_segs=[0, 31])
+
+
+def test_bert_large_full_size_bf16_grads(ob, dev):
+    """BERT-Large with bfloat16 gradients (the paper trains in 16-bit): chunk 7."""
+    _free_run_sampled(ob, dev, synth.get("bert_large"), warm=1, steps=2, sample_segs=[7],
+                      grad_dtype=torch.bfloat16)
 
 
 def test_bert_base_full_size(ob, dev):

@@ -237,7 +237,15 @@ def test_warmup_parity(ob, dev, bias_correction):
 # Free-running: warm-up then compression steps, no re-sync
 # ---------------------------------------------------------------------------
 
-def _free_run(ob, dev, wl, numel=None, warm=None, steps=None, packed=True):
+def _lowp(g, dtype):
+    """Gradients rounded to a 16-bit type: (device tensor of that type, the
+    same values as exact fp32 numpy for the oracle)."""
+    t = torch.from_numpy(np.ascontiguousarray(g)).to(dtype)
+    return t, t.float().numpy()
+
+
+def _free_run(ob, dev, wl, numel=None, warm=None, steps=None, packed=True,
+              grad_dtype=torch.float32):
     numel = wl.numel if numel is None else numel
     n = wl.n
     warm = wl.warmup_steps if warm is None else warm
@@ -250,12 +258,13 @@ def _free_run(ob, dev, wl, numel=None, warm=None, steps=None, packed=True):
     x[~mask] = 0
     m = np.zeros(L.D, np.float32)
     v = np.zeros(L.D, np.float32)
-    st = ob.State(plan, dev, packed_momentum=packed)
+    st = ob.State(plan, dev, packed_momentum=packed, grad_dtype=grad_dtype)
     st.x.copy_(_put(x, dev))
     for t in range(1, warm + 1):
         g = synth.host_grads(wl, L.D, L.tensor_off, t)
+        gt, g = _lowp(g, grad_dtype)
         oracle.warmup_step(L, x, m, v, g, n, wl.lr, wl.beta1, wl.beta2, wl.eps, 0, t)
-        st.grads.copy_(_put(g, dev))
+        st.grads.copy_(gt.to(dev))
         st.warmup(wl.lr, wl.beta1, wl.beta2, wl.eps, t)
     torch.cuda.synchronize()
     check_fp("warm-up x", host(st.x), x)
@@ -265,8 +274,9 @@ def _free_run(ob, dev, wl, numel=None, warm=None, steps=None, packed=True):
     scale_ulps = 0
     for t in range(warm + 1, warm + steps + 1):
         g = synth.host_grads(wl, L.D, L.tensor_off, t)
+        gt, g = _lowp(g, grad_dtype)
         ref.step(g, wl.lr, wl.beta1, wl.eps)
-        st.grads.copy_(_put(g, dev))
+        st.grads.copy_(gt.to(dev))
         st.step(wl.lr, wl.beta1, wl.eps)
         torch.cuda.synchronize()
         tag = "step %d" % (t - warm)
@@ -291,6 +301,19 @@ def test_free_running_tiny(ob, dev, packed):
     """Tiny workload in full: d = 2^20, n = 4, 10 warm-up + 10 compression
     steps; momentum packed (decoded from the server message) or fp32."""
     _free_run(ob, dev, synth.get("tiny"), packed=packed)
+
+
+@pytest.mark.parametrize("grad_dtype", [torch.bfloat16, torch.float16])
+def test_free_running_tiny_16bit_grads(ob, dev, grad_dtype):
+    """Tiny workload with 16-bit gradients (widened exactly to fp32)."""
+    _free_run(ob, dev, synth.get("tiny"), grad_dtype=grad_dtype)
+
+
+@pytest.mark.parametrize("grad_dtype", [torch.bfloat16, torch.float16])
+def test_free_running_ragged_16bit_grads(ob, dev, grad_dtype):
+    wl = synth.Workload(name="ragged16", numel=[1, 63, 64, 65, 0, 1000, 1025, 4097, 12345],
+                        n=3, warmup_steps=2, steps=4)
+    _free_run(ob, dev, wl, grad_dtype=grad_dtype)
 
 
 def test_free_running_many_small_tensors(ob, dev):
