@@ -124,6 +124,38 @@ def hbm_copy_probe(dev, nbytes=4 << 30, reps=10):
     return 2 * nbytes / (ms * 1e-3) / 1e9
 
 
+def bench_variant(args, wl, plan, st, gbytes):
+    """Times one of the paper's comparison variants on the same workload."""
+    import torch
+    n, d = wl.n, plan.d
+    if args.variant == "uncompressed":
+        step = lambda k: st.step_uncompressed(wl.lr, wl.beta1, wl.eps)
+        bytes_pp = n * gbytes + 4 + 4 + 4 + 4 + 4
+        name = "1-bit Adam (32-bits) step: momenta averaged uncompressed, variance frozen"
+    else:
+        t0 = wl.warmup_steps
+        step = lambda k: st.step_naive(wl.lr, wl.beta1, wl.beta2, wl.eps, t0 + k + 1)
+        bytes_pp = (4 + n * (gbytes + 8 + 1 / 8)) + (n / 8 + 8 + 1 / 8) + (1 / 8 + 24)
+        name = "Adam(1-bit Naive) step: gradient compressed, Adam on the decoded average"
+    for k in range(args.warmup):
+        step(k)
+    torch.cuda.synchronize()
+    t0w = time.perf_counter()
+    for k in range(args.steps):
+        step(args.warmup + k)
+    torch.cuda.synchronize()
+    ms = (time.perf_counter() - t0w) * 1e3 / args.steps
+    print(json.dumps({
+        "metric": "%s params/sec, %s" % (args.variant, wl.name), "value": d / (ms * 1e-3),
+        "unit": "params/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": ms, "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "f32", "data": "synthetic",
+        "config": {"workload": wl.name, "d": d, "n_workers": n, "variant": args.variant,
+                   "grad_dtype": args.grad_dtype, "description": name},
+        "bytes_per_param": bytes_pp,
+        "step_hbm_gbps_algorithmic": bytes_pp * d / (ms * 1e-3) / 1e9}), flush=True)
+
+
 def bench_share(args, wl):
     """One GPU's share of an n-worker step: the local worker's pass over all
     d, the owner of one chunk reducing n incoming packed chunks (synthetic,
@@ -217,6 +249,9 @@ def main():
                     choices=["tiny", "bert_base", "bert_large", "stress", "share256"])
     ap.add_argument("--grad-dtype", default="f32", choices=["f32", "bf16", "f16"],
                     help="gradient element type (16-bit gradients are widened exactly)")
+    ap.add_argument("--variant", default="onebit", choices=["onebit", "uncompressed", "naive"],
+                    help="1-bit Adam (default), or one of the paper's comparison variants: "
+                         "'1-bit Adam (32-bits)' (uncompressed) or 'Adam(1-bit Naive)'")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-probe", action="store_true")
     args = ap.parse_args()
@@ -282,6 +317,9 @@ def main():
                                     wl.lr, wl.eps)
         if ev:
             ev[3].record()
+
+    if args.variant != "onebit":
+        return bench_variant(args, wl, plan, st, gbytes)
 
     one_step(first=True)  # untimed: the step that leaves the warm-up's fp32 momentum
     for _ in range(args.warmup):

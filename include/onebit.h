@@ -219,6 +219,31 @@ int onebit_step(onebit_plan plan, float *x, float *m, const float *v_frozen,
                 float lr, float beta1, float eps, void *workspace,
                 onebit_stream stream);
 
+/* Comparison variants of Section 7.2 (not part of 1-bit Adam itself). */
+
+/* "1-bit Adam (32-bits)": the compression stage with the identity compressor
+ * -- variance frozen, momenta averaged uncompressed:
+ *   m_i = beta1 m + (1-beta1) grads[i];  m = (1/n) sum_i m_i (fp64, one rounding)
+ *   x = x - lr * m / sqrt(v_frozen + eps)
+ * x, m: in/out [D]; v_frozen: in [D]; grads: n_grads rows of grad_ld >= D
+ * elements of grad_dtype.  Errors: EINVAL, EALIGN, EHIP. */
+int onebit_uncompressed_step(onebit_plan plan, float *x, float *m, const float *v_frozen,
+                             const void *grads, int32_t grad_dtype, int64_t grad_ld,
+                             int32_t n_grads, float lr, float beta1, float eps,
+                             onebit_stream stream);
+
+/* Adam step (eq. (alg:v)) whose gradient is a decoded message,
+ * g = bit ? scale : -scale: the update of "Adam(1-bit Naive)", which
+ * error-compensates and compresses the gradient (onebit_worker_compress with
+ * beta1 = 0 and a zero momentum, then onebit_server_reduce_compress) and
+ * updates both m and v from the result, without freezing v.  Bias correction
+ * as in onebit_warmup_adam_step.  x, m, v: in/out [D]; bits [W], scales [S]:
+ * in.  Errors: EINVAL, EALIGN, EHIP. */
+int onebit_adam_message_step(onebit_plan plan, float *x, float *m, float *v,
+                             const uint64_t *bits, const float *scales, float lr, float beta1,
+                             float beta2, float eps, int32_t bias_correction, int64_t step,
+                             onebit_stream stream);
+
 /* Decoded message: out[e] = bit(e) ? scales[q] : -scales[q] over every real
  * element e of segment q (padding of out is not written).  With the server
  * bits and scales this is the momentum m_t of Algorithm 1's final step.

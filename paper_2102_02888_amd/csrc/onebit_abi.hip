@@ -471,6 +471,49 @@ int onebit_step(onebit_plan p, float *x, float *m, const float *v_frozen, const 
                                     stream);
 }
 
+int onebit_adam_message_step(onebit_plan p, float *x, float *m, float *v, const uint64_t *bits,
+                             const float *scales, float lr, float beta1, float beta2, float eps,
+                             int32_t bias_correction, int64_t step, onebit_stream stream)
+{
+    TRY(check_plan(p));
+    TRY(check_f32(x, "x"));
+    TRY(check_f32(m, "m"));
+    TRY(check_f32(v, "v"));
+    TRY(check_u64(bits, "bits"));
+    if (!scales) return fail(ONEBIT_EINVAL, "scales is NULL");
+    if (!aligned(scales, 4)) return fail(ONEBIT_EALIGN, "scales misaligned");
+    if (step < 1) return fail(ONEBIT_EINVAL, "step < 1 (steps are 1-based)");
+    if (p->T == 0) return ONEBIT_OK;
+    float bc1 = 1.0f, bc2 = 1.0f;
+    if (bias_correction) {
+        bc1 = (float)(1.0 - std::pow((double)beta1, (double)step));
+        bc2 = (float)(1.0 - std::pow((double)beta2, (double)step));
+    }
+    TRY_HIP(onebit::launch_adam_message(p->tb, p->T, bits, scales, x, m, v, lr, beta1, beta2, eps,
+                                        bias_correction ? 1 : 0, bc1, bc2, (hipStream_t)stream),
+            "message Adam kernel launch");
+    return ONEBIT_OK;
+}
+
+int onebit_uncompressed_step(onebit_plan p, float *x, float *m, const float *v_frozen,
+                             const void *grads, int32_t grad_dtype, int64_t grad_ld,
+                             int32_t n_grads, float lr, float beta1, float eps,
+                             onebit_stream stream)
+{
+    TRY(check_plan(p));
+    TRY(check_f32(x, "x"));
+    TRY(check_f32(m, "m"));
+    TRY(check_f32(v_frozen, "v_frozen"));
+    TRY(check_grads(grads, grad_dtype));
+    if (n_grads < 1) return fail(ONEBIT_EINVAL, "n_grads < 1");
+    TRY(check_ld(grad_ld, p->D, n_grads > 1, "grad_ld"));
+    if (p->T == 0) return ONEBIT_OK;
+    TRY_HIP(onebit::launch_uncompressed(p->tb, p->T, x, m, v_frozen, grads, grad_dtype, grad_ld,
+                                        n_grads, lr, beta1, eps, (hipStream_t)stream),
+            "uncompressed step kernel launch");
+    return ONEBIT_OK;
+}
+
 int onebit_decode(onebit_plan p, const uint64_t *bits, const float *scales, float *out,
                   onebit_stream stream)
 {

@@ -49,6 +49,15 @@ hipError_t launch_worker_pass(const DeviceTables &tb, int64_t num_tiles, const f
                               int64_t bits_ld, double *partial, int n_local, float beta1,
                               hipStream_t s);
 
+hipError_t launch_adam_message(const DeviceTables &tb, int64_t num_tiles, const uint64_t *bits,
+                               const float *scales, float *x, float *m, float *v, float lr,
+                               float beta1, float beta2, float eps, int use_bc, float bc1,
+                               float bc2, hipStream_t s);
+
+hipError_t launch_uncompressed(const DeviceTables &tb, int64_t num_tiles, float *x, float *m,
+                               const float *v, const void *g, int grad_dtype, int64_t g_ld,
+                               int n, float lr, float beta1, float eps, hipStream_t s);
+
 hipError_t launch_decode(const DeviceTables &tb, int64_t num_tiles, const uint64_t *bits,
                          const float *scales, float *out, hipStream_t s);
 

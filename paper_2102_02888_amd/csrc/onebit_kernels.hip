@@ -205,6 +205,156 @@ __device__ __forceinline__ void warmup_tile(const Tile &tile, int lane, float *_
     }
 }
 
+// ---------------------------------------------------------------------------
+// Adam step whose gradient is a decoded message (g = bit ? scale : -scale);
+// the "Adam(1-bit Naive)" comparison variant of Section 7.2 updates m and v
+// from the compressed gradient this way.  Loads first, then stores.
+// ---------------------------------------------------------------------------
+template <bool FULL>
+__device__ __forceinline__ void adam_message_tile(const Tile &tile, int lane,
+                                                  const uint64_t *__restrict__ bits, float s,
+                                                  float *__restrict__ x, float *__restrict__ m,
+                                                  float *__restrict__ v, float lr, float beta1,
+                                                  float omb1, float beta2, float omb2,
+                                                  float eps, int use_bc, float bc1, float bc2)
+{
+    const int len = tile.len;
+    const int64_t base = tile.start;
+    uint64_t word[kSubBlocks];
+    v4f xv[kSubBlocks], mv[kSubBlocks], vv[kSubBlocks];
+#pragma unroll
+    for (int b = 0; b < kSubBlocks; ++b) {
+        const int li = b * (kWave * 4) + 4 * lane;
+        word[b] = (FULL || li < len) ? bits[(base >> 6) + 4 * b + (lane >> 4)] : 0ull;
+        xv[b] = ld4<FULL>(x + base, li, len);
+        mv[b] = ld4<FULL>(m + base, li, len);
+        vv[b] = ld4<FULL>(v + base, li, len);
+    }
+#pragma unroll
+    for (int b = 0; b < kSubBlocks; ++b) {
+        const int li = b * (kWave * 4) + 4 * lane;
+        const uint32_t nib = (uint32_t)(word[b] >> (4 * (lane & 15))) & 0xFu;
+#pragma unroll
+        for (int c = 0; c < 4; ++c) {
+            const float gbar = ((nib >> c) & 1u) ? s : -s;
+            float mn = beta1 * mv[b][c];
+            mn = mn + omb1 * gbar;
+            const float gsq = gbar * gbar;
+            float vn = beta2 * vv[b][c];
+            vn = vn + omb2 * gsq;
+            float mh = mn, vh = vn;
+            if (use_bc) {
+                mh = mn / bc1;
+                vh = vn / bc2;
+            }
+            const float denom = __builtin_sqrtf(vh) + eps;
+            const float ratio = mh / denom;
+            const float step = lr * ratio;
+            xv[b][c] = xv[b][c] - step;
+            mv[b][c] = mn;
+            vv[b][c] = vn;
+        }
+        st4<FULL>(x + base, li, len, xv[b]);
+        st4<FULL>(m + base, li, len, mv[b]);
+        st4<FULL>(v + base, li, len, vv[b]);
+    }
+}
+
+__global__ __launch_bounds__(kBlock) void k_adam_message(
+    const Tile *__restrict__ tiles, int64_t num_tiles, const uint64_t *__restrict__ bits,
+    const float *__restrict__ scales, float *__restrict__ x, float *__restrict__ m,
+    float *__restrict__ v, float lr, float beta1, float omb1, float beta2, float omb2, float eps,
+    int use_bc, float bc1, float bc2)
+{
+    const int lane = threadIdx.x & (kWave - 1);
+    const int64_t t = (int64_t)blockIdx.x * kWavesPerBlock + (threadIdx.x >> 6);
+    if (t >= num_tiles) return;
+    const Tile tile = tiles[t];
+    const float s = scales[tile.seg];
+    if (tile.len == kTileElems)
+        adam_message_tile<true>(tile, lane, bits, s, x, m, v, lr, beta1, omb1, beta2, omb2, eps,
+                                use_bc, bc1, bc2);
+    else
+        adam_message_tile<false>(tile, lane, bits, s, x, m, v, lr, beta1, omb1, beta2, omb2, eps,
+                                 use_bc, bc1, bc2);
+}
+
+// ---------------------------------------------------------------------------
+// "1-bit Adam (32-bits)" comparison variant (Section 7.2): the compression
+// stage with the identity compressor -- variance frozen, momenta averaged
+// uncompressed.  m_i = beta1 m + (1-beta1) g_i per worker, m = mean_i m_i
+// (fp64 sum in worker order, one rounding), x -= lr m / sqrt(v + eps).
+// ---------------------------------------------------------------------------
+template <bool FULL, class G>
+__device__ __forceinline__ void uncompressed_tile(const Tile &tile, int lane,
+                                                  float *__restrict__ x, float *__restrict__ m,
+                                                  const float *__restrict__ v,
+                                                  const typename G::T *__restrict__ g,
+                                                  int64_t g_ld, int n, float lr, float beta1,
+                                                  float omb1, float eps)
+{
+    const int len = tile.len;
+    const int64_t base = tile.start;
+    v4f bm[kSubBlocks], xv[kSubBlocks], vv[kSubBlocks];
+#pragma unroll
+    for (int b = 0; b < kSubBlocks; ++b) {
+        const int li = b * (kWave * 4) + 4 * lane;
+        bm[b] = beta1 * ld4<FULL>(m + base, li, len);
+        xv[b] = ld4<FULL>(x + base, li, len);
+        vv[b] = ld4<FULL>(v + base, li, len);
+    }
+    double sum[kSubBlocks][4];
+#pragma unroll
+    for (int b = 0; b < kSubBlocks; ++b)
+#pragma unroll
+        for (int c = 0; c < 4; ++c) sum[b][c] = 0.0;
+    for (int i = 0; i < n; ++i) {
+#pragma unroll
+        for (int b = 0; b < kSubBlocks; ++b) {
+            const v4f gv = ldg4<FULL, G>(g + (int64_t)i * g_ld + base, b * (kWave * 4) + 4 * lane, len);
+#pragma unroll
+            for (int c = 0; c < 4; ++c) {
+                float mi = omb1 * gv[c];
+                mi = bm[b][c] + mi;
+                sum[b][c] += (double)mi;
+            }
+        }
+    }
+    const double dn = (double)n;
+#pragma unroll
+    for (int b = 0; b < kSubBlocks; ++b) {
+        const int li = b * (kWave * 4) + 4 * lane;
+        v4f mv;
+#pragma unroll
+        for (int c = 0; c < 4; ++c) {
+            const float mbar = (float)(sum[b][c] / dn);
+            const float denom = __builtin_sqrtf(vv[b][c] + eps);
+            const float ratio = mbar / denom;
+            const float step = lr * ratio;
+            xv[b][c] = xv[b][c] - step;
+            mv[c] = mbar;
+        }
+        st4<FULL>(x + base, li, len, xv[b]);
+        st4<FULL>(m + base, li, len, mv);
+    }
+}
+
+template <class G>
+__global__ __launch_bounds__(kBlock) void k_uncompressed(
+    const Tile *__restrict__ tiles, int64_t num_tiles, float *__restrict__ x,
+    float *__restrict__ m, const float *__restrict__ v, const typename G::T *__restrict__ g,
+    int64_t g_ld, int n, float lr, float beta1, float omb1, float eps)
+{
+    const int lane = threadIdx.x & (kWave - 1);
+    const int64_t t = (int64_t)blockIdx.x * kWavesPerBlock + (threadIdx.x >> 6);
+    if (t >= num_tiles) return;
+    const Tile tile = tiles[t];
+    if (tile.len == kTileElems)
+        uncompressed_tile<true, G>(tile, lane, x, m, v, g, g_ld, n, lr, beta1, omb1, eps);
+    else
+        uncompressed_tile<false, G>(tile, lane, x, m, v, g, g_ld, n, lr, beta1, omb1, eps);
+}
+
 template <class G>
 __global__ __launch_bounds__(kBlock) void k_warmup(
     const Tile *__restrict__ tiles, int64_t num_tiles, float *__restrict__ x,
@@ -802,6 +952,46 @@ hipError_t launch_worker_pass(const DeviceTables &tb, int64_t num_tiles, const f
     default:
         launch_worker_g<GradF32>(tb, num_tiles, m, m_bits, m_scales, g, g_ld, err, err_ld,
                                  scales, scales_ld, bits, bits_ld, partial, n_local, beta1, s);
+    }
+    return hipGetLastError();
+}
+
+hipError_t launch_adam_message(const DeviceTables &tb, int64_t num_tiles, const uint64_t *bits,
+                               const float *scales, float *x, float *m, float *v, float lr,
+                               float beta1, float beta2, float eps, int use_bc, float bc1,
+                               float bc2, hipStream_t s)
+{
+    const float omb1 = 1.0f - beta1, omb2 = 1.0f - beta2;
+    hipLaunchKernelGGL(k_adam_message, dim3(blocks_for(num_tiles)), dim3(kBlock), 0, s,
+                       tb.tiles, num_tiles, bits, scales, x, m, v, lr, beta1, omb1, beta2, omb2,
+                       eps, use_bc, bc1, bc2);
+    return hipGetLastError();
+}
+
+template <class G>
+static void launch_uncompressed_t(const DeviceTables &tb, int64_t num_tiles, float *x, float *m,
+                                  const float *v, const void *g, int64_t g_ld, int n, float lr,
+                                  float beta1, float eps, hipStream_t s)
+{
+    const float omb1 = 1.0f - beta1;
+    hipLaunchKernelGGL(k_uncompressed<G>, dim3(blocks_for(num_tiles)), dim3(kBlock), 0, s,
+                       tb.tiles, num_tiles, x, m, v, (const typename G::T *)g, g_ld, n, lr, beta1,
+                       omb1, eps);
+}
+
+hipError_t launch_uncompressed(const DeviceTables &tb, int64_t num_tiles, float *x, float *m,
+                               const float *v, const void *g, int grad_dtype, int64_t g_ld,
+                               int n, float lr, float beta1, float eps, hipStream_t s)
+{
+    switch (grad_dtype) {
+    case kGradBF16:
+        launch_uncompressed_t<GradBF16>(tb, num_tiles, x, m, v, g, g_ld, n, lr, beta1, eps, s);
+        break;
+    case kGradF16:
+        launch_uncompressed_t<GradF16>(tb, num_tiles, x, m, v, g, g_ld, n, lr, beta1, eps, s);
+        break;
+    default:
+        launch_uncompressed_t<GradF32>(tb, num_tiles, x, m, v, g, g_ld, n, lr, beta1, eps, s);
     }
     return hipGetLastError();
 }

@@ -16,7 +16,8 @@ from ._native import PlanInfo, call, lib
 __all__ = [
     "Plan", "onebit_plan_create", "onebit_warmup_adam_step", "onebit_worker_compress",
     "onebit_server_reduce_compress", "onebit_decompress_update", "onebit_step",
-    "onebit_error_materialize", "onebit_decode", "State",
+    "onebit_error_materialize", "onebit_decode", "onebit_uncompressed_step",
+    "onebit_adam_message_step", "State",
 ]
 
 
@@ -186,6 +187,24 @@ def onebit_decode(plan, bits, scales, out, stream=None):
          _ptr(scales, torch.float32, "scales"), _ptr(out, torch.float32, "out"), _stream(stream))
 
 
+def onebit_uncompressed_step(plan, x, m, v_frozen, grads, lr, beta1, eps, n_grads=None,
+                             stream=None):
+    n = _rows(grads) if n_grads is None else n_grads
+    if _rows(grads) < n:
+        raise ValueError("grads has fewer than %d rows" % n)
+    call("onebit_uncompressed_step", plan.handle, _ptr(x, torch.float32, "x"),
+         _ptr(m, torch.float32, "m"), _ptr(v_frozen, torch.float32, "v_frozen"), *_grads(grads),
+         _ld(grads), n, lr, beta1, eps, _stream(stream))
+
+
+def onebit_adam_message_step(plan, x, m, v, bits, scales, lr, beta1, beta2, eps, bias_correction,
+                             step, stream=None):
+    call("onebit_adam_message_step", plan.handle, _ptr(x, torch.float32, "x"),
+         _ptr(m, torch.float32, "m"), _ptr(v, torch.float32, "v"),
+         _ptr(bits, torch.int64, "bits"), _ptr(scales, torch.float32, "scales"), lr, beta1, beta2,
+         eps, int(bias_correction), int(step), _stream(stream))
+
+
 def onebit_error_materialize(plan, err_state, scales, delta_out, rows=None, stream=None):
     r = _rows(err_state) if rows is None else rows
     if _rows(scales) < r or _rows(delta_out) < r or _rows(err_state) < r:
@@ -239,6 +258,27 @@ class State:
                     self.server_err, self.worker_bits, self.worker_scales, self.server_bits,
                     self.server_scales, lr, beta1, eps, self.workspace, stream=stream)
         self.compression_steps += 1
+
+    def step_uncompressed(self, lr, beta1, eps, stream=None):
+        """One step of the "1-bit Adam (32-bits)" comparison variant (fp32 m)."""
+        onebit_uncompressed_step(self.plan, self.x, self.m, self.v, self.grads, lr, beta1, eps,
+                                 stream=stream)
+
+    def step_naive(self, lr, beta1, beta2, eps, t, stream=None):
+        """One step of the "Adam(1-bit Naive)" comparison variant: the gradient
+        is error-compensated and compressed by every worker (the worker pass
+        with beta1 = 0 over a zero momentum), averaged and recompressed by the
+        chunk owners, and Adam updates m and v from the decoded result."""
+        if not hasattr(self, "_zero"):
+            self._zero = torch.zeros_like(self.m)
+        onebit_worker_compress(self.plan, self._zero, self.grads, self.worker_err,
+                               self.worker_bits, self.worker_scales, 0.0, self.workspace,
+                               n_local=self.n_local, stream=stream)
+        onebit_server_reduce_compress(self.plan, 0, self.plan.n, self.worker_bits,
+                                      self.worker_scales, self.server_err, self.server_bits,
+                                      self.server_scales, self.workspace, stream=stream)
+        onebit_adam_message_step(self.plan, self.x, self.m, self.v, self.server_bits,
+                                 self.server_scales, lr, beta1, beta2, eps, 0, t, stream=stream)
 
     def momentum(self):
         if self.compression_steps > 1 and self.packed_momentum:
