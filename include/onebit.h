@@ -244,6 +244,18 @@ int onebit_adam_message_step(onebit_plan plan, float *x, float *m, float *v,
                              float beta2, float eps, int32_t bias_correction, int64_t step,
                              onebit_stream stream);
 
+/* Variance-stability indicator (Section 7.1, warm-up auto-tuning): the l1
+ * norm ||v||_1 = sum_e |v[e]| over every real element, summed in fp64 in a
+ * fixed order (per-tile partials, then one ordered pass), written to *out.
+ * The warm-up can be stopped at the first step t (not before the learning-rate
+ * warm-up ends) with ||v_t||_1 / ||v_{t-Delta}||_1 >= 0.96, Delta = 1/(1-beta2);
+ * keeping the history of norms and taking that decision is host logic.
+ * v: in [D]; workspace: as for the step calls (its server partial area is
+ * used); out: device pointer to one double (8-byte aligned).
+ * Errors: EINVAL, EALIGN, EHIP. */
+int onebit_l1_norm(onebit_plan plan, const float *v, void *workspace, double *out,
+                   onebit_stream stream);
+
 /* Decoded message: out[e] = bit(e) ? scales[q] : -scales[q] over every real
  * element e of segment q (padding of out is not written).  With the server
  * bits and scales this is the momentum m_t of Algorithm 1's final step.

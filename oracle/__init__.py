@@ -41,6 +41,8 @@ def lib():
         L.orc_compress.argtypes = [_i64, _i64, _f32p, _u64p]
         L.orc_decode.restype = _f32
         L.orc_decode.argtypes = [_u64p, _i64, _f32]
+        L.orc_l1_norm_range.restype = ctypes.c_double
+        L.orc_l1_norm_range.argtypes = [_i64, _i64, _vp]
         L.orc_decode_range.restype = None
         L.orc_decode_range.argtypes = [_i64, _i64, _vp, _f32, _vp]
         L.orc_warmup_range.restype = None
@@ -119,6 +121,14 @@ def compress(z, b=0, e=None):
 
 def decode(bits, e, scale):
     return np.float32(lib().orc_decode(bits, int(e), float(scale)))
+
+
+def l1_norm(layout, v):
+    """||v||_1 over the real elements of the layout (binary64, tensor order)."""
+    total = 0.0
+    for off, d in zip(layout.tensor_off.tolist(), layout.numel.tolist()):
+        total += lib().orc_l1_norm_range(off, off + d, _f(v))
+    return total
 
 
 def decode_message(layout, bits, scales):

@@ -161,6 +161,15 @@ void orc_warmup_range(int64_t b, int64_t e, float *x, float *m, float *v,
     }
 }
 
+/* The l1 norm of v over [b, e) in binary64, index order (the warm-up's
+ * variance-stability indicator ||v||_1 of Section 7.1). */
+double orc_l1_norm_range(int64_t b, int64_t e, const float *v)
+{
+    double s = 0.0;
+    for (int64_t idx = b; idx < e; ++idx) s += fabs((double)v[idx]);
+    return s;
+}
+
 /* ------------------------------------------------------------------------ */
 /* Compression stage, Algorithm 1, one segment [b, e) at a time (each       */
 /* segment is an independent parameter-server problem).                      */

@@ -514,6 +514,21 @@ int onebit_uncompressed_step(onebit_plan p, float *x, float *m, const float *v_f
     return ONEBIT_OK;
 }
 
+int onebit_l1_norm(onebit_plan p, const float *v, void *workspace, double *out,
+                   onebit_stream stream)
+{
+    TRY(check_plan(p));
+    TRY(check_f32(v, "v"));
+    if (!workspace) return fail(ONEBIT_EINVAL, "workspace is NULL");
+    if (!aligned(workspace, 256)) return fail(ONEBIT_EALIGN, "workspace is not 256-byte aligned");
+    if (!out) return fail(ONEBIT_EINVAL, "out is NULL");
+    if (!aligned(out, 8)) return fail(ONEBIT_EALIGN, "out is not 8-byte aligned");
+    double *part = (double *)((char *)workspace + server_partial_offset(p));
+    TRY_HIP(onebit::launch_l1_norm(p->tb, p->T, v, part, out, (hipStream_t)stream),
+            "l1 norm kernel launch");
+    return ONEBIT_OK;
+}
+
 int onebit_decode(onebit_plan p, const uint64_t *bits, const float *scales, float *out,
                   onebit_stream stream)
 {

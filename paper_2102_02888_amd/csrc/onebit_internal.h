@@ -58,6 +58,10 @@ hipError_t launch_uncompressed(const DeviceTables &tb, int64_t num_tiles, float 
                                const float *v, const void *g, int grad_dtype, int64_t g_ld,
                                int n, float lr, float beta1, float eps, hipStream_t s);
 
+// out[0] = sum of |v| over the real elements (fp64, fixed order); partial: [T].
+hipError_t launch_l1_norm(const DeviceTables &tb, int64_t num_tiles, const float *v,
+                          double *partial, double *out, hipStream_t s);
+
 hipError_t launch_decode(const DeviceTables &tb, int64_t num_tiles, const uint64_t *bits,
                          const float *scales, float *out, hipStream_t s);
 

@@ -866,6 +866,53 @@ __global__ __launch_bounds__(kBlock) void k_decode(const Tile *__restrict__ tile
     else decode_tile<false>(tile, lane, bits, s, out);
 }
 
+// ---------------------------------------------------------------------------
+// l1 norm of a buffer over the real elements (the variance-stability
+// indicator of Section 7.1): per-tile fp64 partial sums of |v| (fixed lane
+// order), then one workgroup sums the partials in a fixed order.
+// ---------------------------------------------------------------------------
+template <bool FULL>
+__device__ __forceinline__ double l1_tile(const Tile &tile, int lane, const float *__restrict__ v)
+{
+    const int len = tile.len;
+    const int64_t base = tile.start;
+    v4f vv[kSubBlocks];
+#pragma unroll
+    for (int b = 0; b < kSubBlocks; ++b) vv[b] = ld4<FULL>(v + base, b * (kWave * 4) + 4 * lane, len);
+    double acc = 0.0;
+#pragma unroll
+    for (int b = 0; b < kSubBlocks; ++b)
+#pragma unroll
+        for (int c = 0; c < 4; ++c) acc += (double)__builtin_fabsf(vv[b][c]);
+    return acc;
+}
+
+__global__ __launch_bounds__(kBlock) void k_l1_partial(const Tile *__restrict__ tiles,
+                                                       int64_t num_tiles,
+                                                       const float *__restrict__ v,
+                                                       double *__restrict__ partial)
+{
+    const int lane = threadIdx.x & (kWave - 1);
+    const int64_t t = (int64_t)blockIdx.x * kWavesPerBlock + (threadIdx.x >> 6);
+    if (t >= num_tiles) return;
+    const Tile tile = tiles[t];
+    double acc = tile.len == kTileElems ? l1_tile<true>(tile, lane, v) : l1_tile<false>(tile, lane, v);
+    acc = wave_sum(acc);
+    if (lane == 0) partial[t] = acc;
+}
+
+__global__ __launch_bounds__(kBlock) void k_l1_final(const double *__restrict__ partial,
+                                                     int64_t num_tiles, double *__restrict__ out)
+{
+    __shared__ double red[kWavesPerBlock];
+    double s = 0.0;
+    for (int64_t t = threadIdx.x; t < num_tiles; t += kBlock) s += partial[t];
+    s = wave_sum(s);
+    if ((threadIdx.x & (kWave - 1)) == 0) red[threadIdx.x >> 6] = s;
+    __syncthreads();
+    if (threadIdx.x == 0) out[0] = ((red[0] + red[1]) + red[2]) + red[3];
+}
+
 inline unsigned blocks_for(int64_t waves)
 {
     return (unsigned)((waves + kWavesPerBlock - 1) / kWavesPerBlock);
@@ -993,6 +1040,16 @@ hipError_t launch_uncompressed(const DeviceTables &tb, int64_t num_tiles, float 
     default:
         launch_uncompressed_t<GradF32>(tb, num_tiles, x, m, v, g, g_ld, n, lr, beta1, eps, s);
     }
+    return hipGetLastError();
+}
+
+hipError_t launch_l1_norm(const DeviceTables &tb, int64_t num_tiles, const float *v,
+                          double *partial, double *out, hipStream_t s)
+{
+    if (num_tiles > 0)
+        hipLaunchKernelGGL(k_l1_partial, dim3(blocks_for(num_tiles)), dim3(kBlock), 0, s,
+                           tb.tiles, num_tiles, v, partial);
+    hipLaunchKernelGGL(k_l1_final, dim3(1), dim3(kBlock), 0, s, partial, num_tiles, out);
     return hipGetLastError();
 }
 

@@ -17,7 +17,7 @@ __all__ = [
     "Plan", "onebit_plan_create", "onebit_warmup_adam_step", "onebit_worker_compress",
     "onebit_server_reduce_compress", "onebit_decompress_update", "onebit_step",
     "onebit_error_materialize", "onebit_decode", "onebit_uncompressed_step",
-    "onebit_adam_message_step", "State",
+    "onebit_adam_message_step", "onebit_l1_norm", "State",
 ]
 
 
@@ -205,6 +205,13 @@ def onebit_adam_message_step(plan, x, m, v, bits, scales, lr, beta1, beta2, eps,
          eps, int(bias_correction), int(step), _stream(stream))
 
 
+def onebit_l1_norm(plan, v, workspace, out, stream=None):
+    """||v||_1 over the real elements into out (a one-element float64 GPU tensor)."""
+    call("onebit_l1_norm", plan.handle, _ptr(v, torch.float32, "v"),
+         _ptr(workspace, torch.float64, "workspace"), _ptr(out, torch.float64, "out"),
+         _stream(stream))
+
+
 def onebit_error_materialize(plan, err_state, scales, delta_out, rows=None, stream=None):
     r = _rows(err_state) if rows is None else rows
     if _rows(scales) < r or _rows(delta_out) < r or _rows(err_state) < r:
@@ -279,6 +286,13 @@ class State:
                                       self.server_scales, self.workspace, stream=stream)
         onebit_adam_message_step(self.plan, self.x, self.m, self.v, self.server_bits,
                                  self.server_scales, lr, beta1, beta2, eps, 0, t, stream=stream)
+
+    def variance_l1_norm(self, stream=None):
+        """||v||_1 (fp64) computed on the GPU; synchronises to return it."""
+        if not hasattr(self, "_norm"):
+            self._norm = torch.zeros(1, dtype=torch.float64, device=self.v.device)
+        onebit_l1_norm(self.plan, self.v, self.workspace, self._norm, stream=stream)
+        return float(self._norm.item())
 
     def momentum(self):
         if self.compression_steps > 1 and self.packed_momentum:
