@@ -367,10 +367,11 @@ def main():
         "kernel_ms": {"worker_compress": part_ms[0], "server_reduce_compress": part_ms[1],
                       "decompress_update": part_ms[2], "sum": gpu_step_ms},
         "warmup_adam_step_ms": sum(warm_ms[1:]) / max(1, len(warm_ms) - 1) if warm_ms else None,
-        "roofline": {"bound": "hbm", "kernel": "worker_compress (k_worker_pass<true>, packed momentum)",
+        "roofline": {"bound": "hbm", "kernel": "worker_compress (k_worker_pass<true, GradF32>: packed momentum, fp32 gradients)",
                      "achieved": achieved, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
                      "frac": achieved / HBM_PEAK_GBPS,
-                     "traffic": measured_traffic(wl.name, "k_worker_pass<true>"),
+                     "traffic": (measured_traffic(wl.name, "k_worker_pass<true, GradF32>")
+                                 if args.grad_dtype == "f32" else None),
                      "algorithmic_bytes_per_launch": worker_bytes},
     }
     if not args.no_probe:
