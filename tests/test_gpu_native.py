@@ -1,0 +1,129 @@
+"""The C ABI driven without Python tensors, and the hot path under HIP graph
+capture."""
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+import pytest
+import torch
+
+import synth
+from parity_util import host
+
+pytestmark = pytest.mark.gpu
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+
+
+def test_plain_c_program_matches_oracle(dev):
+    """tests/c/abi_step_check.c: hipMalloc'd buffers, warm-up + compression
+    steps through the C ABI, compared with the oracle in the same process."""
+    from tests.c import build as cb
+    if not os.path.exists(cb.BIN):
+        cb.build()
+    r = subprocess.run([cb.BIN], capture_output=True, text=True, timeout=120)
+    assert r.returncode == 0 and r.stdout.strip() == "ok", (r.returncode, r.stdout, r.stderr)
+
+
+def test_step_replays_from_a_hip_graph(dev):
+    """onebit_step captured once in a graph and replayed gives the eager
+    result bit for bit, replay after replay (fresh gradients each time)."""
+    import paper_2102_02888_amd as ob
+    numel, n = [200_000, 3000, 64], 4
+    plan = ob.Plan(numel, n)
+    wl = synth.Workload(name="graph", numel=numel, n=n, warmup_steps=2, steps=0)
+    states = [ob.State(plan, dev), ob.State(plan, dev)]
+    x0 = torch.from_numpy(synth.host_params(wl, plan.D)).to(dev)
+    for st in states:
+        st.x.copy_(x0)
+    for t in (1, 2):
+        g = torch.from_numpy(synth.host_grads(wl, plan.D, plan.tensor_off, t)).to(dev)
+        for st in states:
+            st.grads.copy_(g)
+            st.warmup(wl.lr, wl.beta1, wl.beta2, wl.eps, t)
+            st.step(wl.lr, wl.beta1, wl.eps)  # first compression step, eager (fp32 momentum)
+    torch.cuda.synchronize()
+    eager, graphed = states
+    graph = torch.cuda.CUDAGraph()
+    # capture one packed-momentum step of the second state
+    snapshot = [t.clone() for t in (graphed.x, graphed.worker_err, graphed.worker_scales,
+                                    graphed.server_err, graphed.server_bits, graphed.server_scales)]
+    with torch.cuda.graph(graph):
+        graphed.step(wl.lr, wl.beta1, wl.eps)
+    # capture does not run the kernels; restore the state anyway to be sure
+    for dst, src in zip((graphed.x, graphed.worker_err, graphed.worker_scales,
+                         graphed.server_err, graphed.server_bits, graphed.server_scales), snapshot):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    for k in range(4):
+        g = torch.from_numpy(synth.host_grads(wl, plan.D, plan.tensor_off, 10 + k)).to(dev)
+        eager.grads.copy_(g)
+        graphed.grads.copy_(g)
+        eager.step(wl.lr, wl.beta1, wl.eps)
+        graph.replay()
+        torch.cuda.synchronize()
+        for name in ("x", "worker_err", "worker_bits", "worker_scales", "server_err",
+                     "server_bits", "server_scales"):
+            a, b = host(getattr(eager, name)), host(getattr(graphed, name))
+            assert a.tobytes() == b.tobytes(), (k, name)
+    plan.close()
+
+
+def test_argument_errors_on_device_buffers(dev):
+    """Misaligned or out-of-range arguments on real device buffers are refused
+    before any launch, and leave every buffer as it was."""
+    import paper_2102_02888_amd as ob
+    from paper_2102_02888_amd import _native
+    L = _native.lib()
+    numel, n = [1000, 64], 2
+    plan = ob.Plan(numel, n)
+    st = ob.State(plan, dev)
+    st.x.normal_()
+    st.grads.normal_()
+    before = st.x.clone()
+    vp = ctypes.c_void_p
+    s0 = vp(torch.cuda.current_stream().cuda_stream)
+
+    def p(t, byte_off=0):
+        return vp(t.data_ptr() + byte_off)
+
+    def step(**kw):
+        a = dict(x=p(st.x), m=p(st.m), v=p(st.v), g=p(st.grads), gd=0, gld=plan.D,
+                 we=p(st.worker_err), eld=plan.D, se=p(st.server_err), wb=p(st.worker_bits),
+                 ws=p(st.worker_scales), sb=p(st.server_bits), ss=p(st.server_scales),
+                 wsp=p(st.workspace))
+        a.update(kw)
+        return L.onebit_step(plan.handle, a["x"], a["m"], a["v"], a["g"], a["gd"], a["gld"],
+                             a["we"], a["eld"], a["se"], a["wb"], a["ws"], a["sb"], a["ss"],
+                             1e-3, 0.9, 1e-8, a["wsp"], s0)
+
+    assert step(x=p(st.x, 4)) == -2 and b"x" in L.onebit_last_error()
+    assert step(g=p(st.grads, 4)) == -2
+    assert step(gd=3) == -1
+    assert step(gld=plan.D - 4) == -1
+    assert step(eld=plan.D + 2) == -2
+    assert step(wb=p(st.worker_bits, 4)) == -2
+    assert step(wsp=p(st.workspace, 8)) == -2
+    assert step(ss=None) == -1
+    # chunk range and per-rank offsets of the server entry point
+    args = (p(st.worker_bits), plan.W, 0, p(st.worker_scales), plan.S, 0, p(st.server_err),
+            p(st.server_bits), p(st.server_scales), p(st.workspace), s0)
+    assert L.onebit_server_reduce_compress(plan.handle, 0, n + 1, *args) == -1
+    assert L.onebit_server_reduce_compress(plan.handle, 1, 1, *args) == -1
+    bad_base = (p(st.worker_bits), plan.W, plan.W + 1) + args[3:]
+    assert L.onebit_server_reduce_compress(plan.handle, 0, n, *bad_base) == -1
+    # n_local outside [1, n]
+    assert L.onebit_worker_compress(plan.handle, p(st.m), None, None, p(st.grads), 0, plan.D,
+                                    n + 1, p(st.worker_err), plan.D, p(st.worker_bits), plan.W,
+                                    p(st.worker_scales), plan.S, 0.9, p(st.workspace), s0) == -1
+    # warm-up step numbers are 1-based
+    assert L.onebit_warmup_adam_step(plan.handle, p(st.x), p(st.m), p(st.v), p(st.grads), 0,
+                                     plan.D, n, 1e-3, 0.9, 0.999, 1e-8, 0, 0, s0) == -1
+    torch.cuda.synchronize()
+    assert torch.equal(st.x, before)
+    # a correct call still goes through afterwards
+    assert step() == 0
+    torch.cuda.synchronize()
+    assert not torch.equal(st.x, before)
+    plan.close()
