@@ -105,23 +105,32 @@ def cpu_baseline(st, plan, wl, target_s=12.0, max_segments=3):
                       % (len(used), used, plan.S, done, n, spent)}
 
 
-def hbm_copy_probe(dev, nbytes=4 << 30, reps=10):
-    """Achievable HBM bandwidth of a plain device copy (read + write)."""
+def hbm_probe(dev, nbytes=2 << 30, reps=10):
+    """Achievable HBM bandwidth of two plain streaming kernels of torch: a
+    device copy (one read stream, one write stream) and an elementwise add
+    (two read streams, one write stream: the read/write mix of the worker
+    pass), each over `nbytes` per operand."""
     import torch
     a = torch.empty(nbytes // 4, dtype=torch.float32, device=dev)
     b = torch.empty_like(a)
-    a.fill_(1.0)
-    b.copy_(a)
-    torch.cuda.synchronize()
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    e0.record()
-    for _ in range(reps):
-        b.copy_(a)
-    e1.record()
-    torch.cuda.synchronize()
-    ms = e0.elapsed_time(e1) / reps
-    del a, b
-    return 2 * nbytes / (ms * 1e-3) / 1e9
+    c = torch.empty_like(a)
+    a.normal_()
+    b.normal_()
+    out = {}
+    for name, fn, streams in (("copy_1r1w", lambda: c.copy_(a), 2),
+                              ("add_2r1w", lambda: torch.add(a, b, out=c), 3)):
+        fn()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(reps):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1) / reps
+        out[name] = streams * nbytes / (ms * 1e-3) / 1e9
+    del a, b, c
+    return out
 
 
 def bench_variant(args, wl, plan, st, gbytes):
@@ -336,6 +345,7 @@ def main():
     part_ms = [sum(ev[j].elapsed_time(ev[j + 1]) for ev in events) / args.steps
                for j in range(3)]
     gpu_step_ms = sum(part_ms)
+    per_step = sorted(ev[0].elapsed_time(ev[3]) for ev in events)
 
     bw, bs, bu = algorithmic_bytes_per_param(n, gbytes)
     d = plan.d
@@ -366,6 +376,8 @@ def main():
         "bytes_per_param": {"worker": bw, "server": bs, "update": bu},
         "kernel_ms": {"worker_compress": part_ms[0], "server_reduce_compress": part_ms[1],
                       "decompress_update": part_ms[2], "sum": gpu_step_ms},
+        "gpu_step_ms": {"median": per_step[len(per_step) // 2], "min": per_step[0],
+                        "max": per_step[-1]},
         "warmup_adam_step_ms": sum(warm_ms[1:]) / max(1, len(warm_ms) - 1) if warm_ms else None,
         "roofline": {"bound": "hbm", "kernel": "worker_compress (k_worker_pass<true, GradF32>: packed momentum, fp32 gradients)",
                      "achieved": achieved, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
@@ -376,7 +388,7 @@ def main():
     }
     if not args.no_probe:
         del events
-        result["hbm_copy_probe_gbps"] = hbm_copy_probe(dev, nbytes=2 << 30)
+        result["hbm_probe_gbps"] = hbm_probe(dev)
     if not args.no_cpu_baseline:
         log("timing the oracle on sampled segments ...")
         result["cpu_baseline"] = cpu_baseline(st, plan, wl)

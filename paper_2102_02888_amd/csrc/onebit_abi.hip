@@ -363,9 +363,13 @@ int onebit_worker_compress(onebit_plan p, const float *m, const uint64_t *m_bits
     if (p->T == 0) return ONEBIT_OK;
     double *part = (double *)((char *)workspace + worker_partial_offset(p));
     hipStream_t s = (hipStream_t)stream;
+    // Packed momentum costs 1/8 byte per element to re-derive, so each wave
+    // takes one worker and the grid streams two rows at a time; an fp32
+    // momentum is read once per tile for all local workers instead.
+    const int group = m ? n_local : 1;
     TRY_HIP(onebit::launch_worker_pass(p->tb, p->T, m, m_bits, m_scales, grads, grad_dtype,
                                        grad_ld, worker_err, err_ld, worker_scales, scales_ld,
-                                       worker_bits, bits_ld, part, n_local, beta1, s),
+                                       worker_bits, bits_ld, part, n_local, group, beta1, s),
             "worker kernel launch");
     TRY_HIP(onebit::launch_finalize(p->tb, p->max_seg_tiles, (int64_t)n_local * p->S, p->S, 0,
                                     p->n, 0, 0, part, p->T, worker_scales, scales_ld, s),

@@ -42,12 +42,14 @@ hipError_t launch_warmup(const DeviceTables &tb, int64_t num_tiles, float *x, fl
                          float bc2, hipStream_t s);
 
 // m != NULL: fp32 momentum; m == NULL: momentum decoded from (m_bits, m_scales).
+// group: workers handled by one wave per tile (1..n_local); the grid runs
+// over groups first, then tiles.
 hipError_t launch_worker_pass(const DeviceTables &tb, int64_t num_tiles, const float *m,
                               const uint64_t *m_bits, const float *m_scales, const void *g,
                               int grad_dtype, int64_t g_ld, float *err, int64_t err_ld,
                               const float *scales, int64_t scales_ld, uint64_t *bits,
-                              int64_t bits_ld, double *partial, int n_local, float beta1,
-                              hipStream_t s);
+                              int64_t bits_ld, double *partial, int n_local, int group,
+                              float beta1, hipStream_t s);
 
 hipError_t launch_adam_message(const DeviceTables &tb, int64_t num_tiles, const uint64_t *bits,
                                const float *scales, float *x, float *m, float *v, float lr,

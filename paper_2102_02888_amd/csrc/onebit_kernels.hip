@@ -17,6 +17,7 @@
 // per-tile partial sums (fixed lane order, xor butterfly) are written to a
 // workspace and summed in a fixed order by a finalize kernel; no atomics.
 #include "onebit_internal.h"
+#include <algorithm>
 
 namespace onebit {
 namespace {
@@ -377,7 +378,14 @@ __global__ __launch_bounds__(kBlock) void k_warmup(
 // ---------------------------------------------------------------------------
 // Worker pass: for each local worker i, z_i = (beta1 m + (1-beta1) g_i) + delta_i,
 // sign words of z_i, per-tile partial sum of z_i^2, and z_i written back as the
-// new compensated error state.  m is read once per tile for all workers.
+// new compensated error state.
+//
+// A wave handles one tile for a group of consecutive workers, and the grid
+// runs group-major: all waves in flight work on the same few worker rows, so
+// the chip streams through 2 x group rows of (g, error state) at a time
+// instead of all 2n.  With one worker per group the momentum of a tile is
+// re-derived by every worker; in packed form that is 1/8 byte per element per
+// worker from a sign array small enough to stay in the last-level cache.
 // ---------------------------------------------------------------------------
 // The shared momentum m_{t-1} of the tile times beta1.  PACKED: m_{t-1} is
 // the previous step's gathered server message, decoded from its sign words
@@ -414,7 +422,7 @@ __device__ __forceinline__ void worker_tile(
     const uint64_t *__restrict__ m_bits, const float *__restrict__ m_scales,
     const typename G::T *__restrict__ g, int64_t g_ld, float *__restrict__ err, int64_t err_ld,
     const float *__restrict__ scales, int64_t scales_ld, uint64_t *__restrict__ bits,
-    int64_t bits_ld, double *__restrict__ partial, int n_local, float beta1, float omb1)
+    int64_t bits_ld, double *__restrict__ partial, int i0, int i1, float beta1, float omb1)
 {
     const int len = tile.len;
     const int64_t base = tile.start;
@@ -423,7 +431,7 @@ __device__ __forceinline__ void worker_tile(
     v4f bm[kSubBlocks];
     beta1_momentum<FULL, PACKED>(bm, tile, lane, m, m_bits, m_scales, beta1);
 
-    for (int i = 0; i < n_local; ++i) {
+    for (int i = i0; i < i1; ++i) {
         const float sp = scales[(int64_t)i * scales_ld + tile.seg];
         const typename G::T *gi = g + (int64_t)i * g_ld + base;
         float *ei = err + (int64_t)i * err_ld + base;
@@ -469,20 +477,27 @@ __global__ __launch_bounds__(kBlock) void k_worker_pass(
     const uint64_t *__restrict__ m_bits, const float *__restrict__ m_scales,
     const typename G::T *__restrict__ g, int64_t g_ld, float *__restrict__ err, int64_t err_ld,
     const float *__restrict__ scales, int64_t scales_ld, uint64_t *__restrict__ bits,
-    int64_t bits_ld, double *__restrict__ partial, int n_local, float beta1, float omb1)
+    int64_t bits_ld, double *__restrict__ partial, int n_local, int group, int64_t num_items,
+    float beta1, float omb1)
 {
     const int lane = threadIdx.x & (kWave - 1);
-    const int64_t t = (int64_t)blockIdx.x * kWavesPerBlock + (threadIdx.x >> 6);
-    if (t >= num_tiles) return;
-    const Tile tile = tiles[t];
-    if (tile.len == kTileElems)
-        worker_tile<true, PACKED, G>(tile, t, lane, num_tiles, m, m_bits, m_scales, g, g_ld, err,
-                                  err_ld, scales, scales_ld, bits, bits_ld, partial, n_local,
-                                  beta1, omb1);
-    else
-        worker_tile<false, PACKED, G>(tile, t, lane, num_tiles, m, m_bits, m_scales, g, g_ld, err,
-                                   err_ld, scales, scales_ld, bits, bits_ld, partial, n_local,
-                                   beta1, omb1);
+    const int64_t stride = (int64_t)gridDim.x * kWavesPerBlock;
+    for (int64_t item = (int64_t)blockIdx.x * kWavesPerBlock + (threadIdx.x >> 6);
+         item < num_items; item += stride) {
+        const int64_t grp = item / num_tiles;
+        const int64_t t = item - grp * num_tiles;
+        const int i0 = (int)grp * group;
+        const int i1 = min(n_local, i0 + group);
+        const Tile tile = tiles[t];
+        if (tile.len == kTileElems)
+            worker_tile<true, PACKED, G>(tile, t, lane, num_tiles, m, m_bits, m_scales, g, g_ld,
+                                         err, err_ld, scales, scales_ld, bits, bits_ld, partial,
+                                         i0, i1, beta1, omb1);
+        else
+            worker_tile<false, PACKED, G>(tile, t, lane, num_tiles, m, m_bits, m_scales, g, g_ld,
+                                          err, err_ld, scales, scales_ld, bits, bits_ld, partial,
+                                          i0, i1, beta1, omb1);
+    }
 }
 
 // ---------------------------------------------------------------------------
@@ -549,14 +564,19 @@ __global__ __launch_bounds__(kBlock) void k_finalize(
 // Each wave owns one tile and its own LDS region, so it synchronises only
 // with itself (no workgroup barrier); the tile's error-state loads are issued
 // first so that they overlap the sign-word traffic.  Incoming sign words are
-// staged in LDS 32 worker rows at a time with coalesced 128-byte row reads.  The average is an fp64 sum of +-scale over
-// the workers in worker order.  When every partial sum of the segment's
-// scales is exactly representable in fp64 (the scales' exponents span at most
-// 29 - ceil(log2 n) binades; true for any realistic message set) the sum is
-// exact, so it may be formed in any grouping: then each group of 4 workers
-// is one lookup in a 16-entry table of its signed scale sums, indexed by the
-// 4 workers' bits of the element (a 4x4 bit transpose of their nibbles).
-// Otherwise every worker is added one by one.  Both give the oracle's sum.
+// staged in LDS 32 worker rows at a time (coalesced 128-byte row reads),
+// transposed so that the words of consecutive workers for one 32-element
+// half-word are adjacent: one 128-bit LDS read returns 4 workers' bits.
+//
+// The average is an fp64 sum of +-scale over the workers in worker order.
+// When every partial sum of the segment's scales is exactly representable in
+// fp64 (the scales' exponents span at most 29 - ceil(log2 n) binades; true
+// for any realistic message set) the sum is exact, so it may be formed in any
+// grouping: then each group of 8 workers is one lookup in a 256-entry table
+// of its signed scale sums, indexed by the 8 workers' bits of the element (two
+// 4x4 bit transposes of their nibbles).  The 256-entry tables are sums of two
+// 16-entry tables, each built from 4 scales.  Otherwise every worker is added
+// one by one.  Both give the oracle's sum.
 // ---------------------------------------------------------------------------
 __device__ __forceinline__ uint32_t transpose4x4(uint32_t x)
 {
@@ -582,15 +602,29 @@ __device__ __forceinline__ int wave_min(int v)
     return v;
 }
 
-__global__ __launch_bounds__(kBlock) void k_server_pass(
+__device__ __forceinline__ void wave_sync()
+{
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+// LDS row stride (in 32-bit half-words) of the transposed sign staging: a
+// multiple of 4 keeps 128-bit reads aligned, and 36 puts the 8 half-words a
+// wave reads at once on disjoint banks.
+constexpr int kBitsStride = kServerRowBatch + 4;
+
+__global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))) void k_server_pass(
     const Tile *__restrict__ tiles, int64_t tile_begin, int64_t tile_count, int n,
     int grouping_limit, const uint64_t *__restrict__ wbits, int64_t bits_ld,
     int64_t bits_word_base, const float *__restrict__ wscales, int64_t scales_ld,
     int64_t scales_seg_base, float *__restrict__ serr, const float *__restrict__ sscales,
     uint64_t *__restrict__ sbits, double *__restrict__ partial)
 {
-    __shared__ uint32_t s_bits[kWavesPerBlock][kServerRowBatch][2 * kTileWords];
-    __shared__ double s_lut[kWavesPerBlock][kServerRowBatch / 4][16];
+    // s_bits[wave][half-word h of the tile][worker row r]
+    __shared__ __align__(16) uint32_t s_bits[kWavesPerBlock][2 * kTileWords][kBitsStride];
+    __shared__ double s_lut4[kWavesPerBlock][kServerRowBatch / 4][16];
+    __shared__ double s_lut8[kWavesPerBlock][2][256];
     __shared__ float s_scale[kWavesPerBlock][kServerRowBatch];
     const int lane = threadIdx.x & (kWave - 1);
     const int wv = threadIdx.x >> 6;
@@ -653,17 +687,19 @@ __global__ __launch_bounds__(kBlock) void k_server_pass(
     for (int r0 = 0; r0 < n; r0 += kServerRowBatch) {
         if (r0 > 0) load_batch(r0);
         const int rows = min(kServerRowBatch, n - r0);
-        const int rows4 = (rows + 3) & ~3;  // rows past the last worker hold zero words
+        const int rows8 = (rows + 7) & ~7;  // rows past the last worker hold zero words
 #pragma unroll
         for (int k = 0; k < kServerRowBatch / 4; ++k) {
             const int r = (lane >> 4) + 4 * k;
-            if (r < rows4 && wi < nwords) *(uint64_t *)&s_bits[wv][r][2 * wi] = stg[k];
+            if (r < rows8 && wi < nwords) {
+                s_bits[wv][2 * wi][r] = (uint32_t)stg[k];
+                s_bits[wv][2 * wi + 1][r] = (uint32_t)(stg[k] >> 32);
+            }
         }
         if (lane < rows) s_scale[wv][lane] = scl;
-        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-        __builtin_amdgcn_wave_barrier();
-        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+        wave_sync();
         if (grouped) {
+            // 16-entry tables of 4 workers (rows past the last worker add 0)
             for (int e = lane; e < 16 * (kServerRowBatch / 4); e += kWave) {
                 const int q = e >> 4, idx = e & 15;
                 double v = 0.0;
@@ -675,24 +711,40 @@ __global__ __launch_bounds__(kBlock) void k_server_pass(
                         v += ((idx >> k) & 1) ? sc : -sc;
                     }
                 }
-                s_lut[wv][q][idx] = v;
+                s_lut4[wv][q][idx] = v;
             }
-            __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-            __builtin_amdgcn_wave_barrier();
-            __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-            const int groups = (rows + 3) >> 2;
-            for (int q = 0; q < groups; ++q) {
+            wave_sync();
+            // two groups of 8 workers at a time
+            for (int g0 = 0; 8 * g0 < rows; g0 += 2) {
 #pragma unroll
-                for (int b = 0; b < kSubBlocks; ++b) {
-                    const int hw = 2 * (4 * b + (lane >> 4)) + half;
-                    uint32_t x = 0;
-#pragma unroll
-                    for (int k = 0; k < 4; ++k)
-                        x |= ((s_bits[wv][4 * q + k][hw] >> shift) & 0xFu) << (4 * k);
-                    const uint32_t y = transpose4x4(x);
-#pragma unroll
-                    for (int c = 0; c < 4; ++c) sum[b][c] += s_lut[wv][q][(y >> (4 * c)) & 0xFu];
+                for (int k = 0; k < 512 / kWave; ++k) {
+                    const int e = lane + kWave * k;
+                    const int g = e >> 8, idx = e & 255;
+                    const int q = 2 * (g0 + g);
+                    s_lut8[wv][g][idx] = s_lut4[wv][q][idx & 15] + s_lut4[wv][q + 1][idx >> 4];
                 }
+                wave_sync();
+                const int gcnt = min(2, ((rows + 7) >> 3) - g0);
+                for (int g = 0; g < gcnt; ++g) {
+                    const int r8 = 8 * (g0 + g);
+#pragma unroll
+                    for (int b = 0; b < kSubBlocks; ++b) {
+                        const int hw = 2 * (4 * b + (lane >> 4)) + half;
+                        const uint4 lo = *(const uint4 *)&s_bits[wv][hw][r8];
+                        const uint4 hi = *(const uint4 *)&s_bits[wv][hw][r8 + 4];
+                        const uint32_t xl = ((lo.x >> shift) & 0xFu) | (((lo.y >> shift) & 0xFu) << 4) |
+                                            (((lo.z >> shift) & 0xFu) << 8) | (((lo.w >> shift) & 0xFu) << 12);
+                        const uint32_t xh = ((hi.x >> shift) & 0xFu) | (((hi.y >> shift) & 0xFu) << 4) |
+                                            (((hi.z >> shift) & 0xFu) << 8) | (((hi.w >> shift) & 0xFu) << 12);
+                        const uint32_t yl = transpose4x4(xl), yh = transpose4x4(xh);
+#pragma unroll
+                        for (int c = 0; c < 4; ++c) {
+                            const uint32_t idx = ((yl >> (4 * c)) & 0xFu) | (((yh >> (4 * c)) & 0xFu) << 4);
+                            sum[b][c] += s_lut8[wv][g][idx];
+                        }
+                    }
+                }
+                wave_sync();
             }
         } else {
             for (int r = 0; r < rows; ++r) {
@@ -700,15 +752,13 @@ __global__ __launch_bounds__(kBlock) void k_server_pass(
                 const double sn = -sp;
 #pragma unroll
                 for (int b = 0; b < kSubBlocks; ++b) {
-                    const uint32_t nib = (s_bits[wv][r][2 * (4 * b + (lane >> 4)) + half] >> shift) & 0xFu;
+                    const uint32_t nib = (s_bits[wv][2 * (4 * b + (lane >> 4)) + half][r] >> shift) & 0xFu;
 #pragma unroll
                     for (int c = 0; c < 4; ++c) sum[b][c] += ((nib >> c) & 1u) ? sp : sn;
                 }
             }
         }
-        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-        __builtin_amdgcn_wave_barrier();
-        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+        wave_sync();
     }
     const double dn = (double)n;
     double acc = 0.0;
@@ -951,18 +1001,25 @@ hipError_t launch_warmup(const DeviceTables &tb, int64_t num_tiles, float *x, fl
     }
 }
 
+// Cap on the worker grid (waves loop over the rest): keeps the launch's
+// work-item count far below 2^32.
+constexpr int64_t kMaxWorkerBlocks = 1 << 22;
+
 template <bool PACKED, class G>
 static void launch_worker_t(const DeviceTables &tb, int64_t num_tiles, const float *m,
                             const uint64_t *m_bits, const float *m_scales, const void *g,
                             int64_t g_ld, float *err, int64_t err_ld, const float *scales,
                             int64_t scales_ld, uint64_t *bits, int64_t bits_ld, double *partial,
-                            int n_local, float beta1, hipStream_t s)
+                            int n_local, int group, float beta1, hipStream_t s)
 {
     const float omb1 = 1.0f - beta1;
-    hipLaunchKernelGGL((k_worker_pass<PACKED, G>), dim3(blocks_for(num_tiles)), dim3(kBlock), 0,
-                       s, tb.tiles, num_tiles, m, m_bits, m_scales, (const typename G::T *)g,
-                       g_ld, err, err_ld, scales, scales_ld, bits, bits_ld, partial, n_local,
-                       beta1, omb1);
+    const int64_t groups = (n_local + group - 1) / group;
+    const int64_t items = groups * num_tiles;
+    const int64_t blocks = std::min<int64_t>(blocks_for(items), kMaxWorkerBlocks);
+    hipLaunchKernelGGL((k_worker_pass<PACKED, G>), dim3((unsigned)blocks), dim3(kBlock), 0, s,
+                       tb.tiles, num_tiles, m, m_bits, m_scales, (const typename G::T *)g, g_ld,
+                       err, err_ld, scales, scales_ld, bits, bits_ld, partial, n_local, group,
+                       items, beta1, omb1);
 }
 
 template <class G>
@@ -970,35 +1027,41 @@ static void launch_worker_g(const DeviceTables &tb, int64_t num_tiles, const flo
                             const uint64_t *m_bits, const float *m_scales, const void *g,
                             int64_t g_ld, float *err, int64_t err_ld, const float *scales,
                             int64_t scales_ld, uint64_t *bits, int64_t bits_ld, double *partial,
-                            int n_local, float beta1, hipStream_t s)
+                            int n_local, int group, float beta1, hipStream_t s)
 {
     if (m)
         launch_worker_t<false, G>(tb, num_tiles, m, m_bits, m_scales, g, g_ld, err, err_ld,
-                                  scales, scales_ld, bits, bits_ld, partial, n_local, beta1, s);
+                                  scales, scales_ld, bits, bits_ld, partial, n_local, group,
+                                  beta1, s);
     else
         launch_worker_t<true, G>(tb, num_tiles, m, m_bits, m_scales, g, g_ld, err, err_ld,
-                                 scales, scales_ld, bits, bits_ld, partial, n_local, beta1, s);
+                                 scales, scales_ld, bits, bits_ld, partial, n_local, group,
+                                 beta1, s);
 }
 
 hipError_t launch_worker_pass(const DeviceTables &tb, int64_t num_tiles, const float *m,
                               const uint64_t *m_bits, const float *m_scales, const void *g,
                               int grad_dtype, int64_t g_ld, float *err, int64_t err_ld,
                               const float *scales, int64_t scales_ld, uint64_t *bits,
-                              int64_t bits_ld, double *partial, int n_local, float beta1,
-                              hipStream_t s)
+                              int64_t bits_ld, double *partial, int n_local, int group,
+                              float beta1, hipStream_t s)
 {
+    if (group < 1 || group > n_local) group = n_local;
     switch (grad_dtype) {
     case kGradBF16:
         launch_worker_g<GradBF16>(tb, num_tiles, m, m_bits, m_scales, g, g_ld, err, err_ld,
-                                  scales, scales_ld, bits, bits_ld, partial, n_local, beta1, s);
+                                  scales, scales_ld, bits, bits_ld, partial, n_local, group,
+                                  beta1, s);
         break;
     case kGradF16:
         launch_worker_g<GradF16>(tb, num_tiles, m, m_bits, m_scales, g, g_ld, err, err_ld,
-                                 scales, scales_ld, bits, bits_ld, partial, n_local, beta1, s);
+                                 scales, scales_ld, bits, bits_ld, partial, n_local, group,
+                                 beta1, s);
         break;
     default:
         launch_worker_g<GradF32>(tb, num_tiles, m, m_bits, m_scales, g, g_ld, err, err_ld,
-                                 scales, scales_ld, bits, bits_ld, partial, n_local, beta1, s);
+                                 scales, scales_ld, bits, bits_ld, partial, n_local, group,
+                                 beta1, s);
     }
     return hipGetLastError();
 }
