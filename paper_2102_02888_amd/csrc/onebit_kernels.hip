@@ -566,7 +566,10 @@ __global__ __launch_bounds__(kBlock) void k_finalize(
 // first so that they overlap the sign-word traffic.  Incoming sign words are
 // staged in LDS 32 worker rows at a time (coalesced 128-byte row reads),
 // transposed so that the words of consecutive workers for one 32-element
-// half-word are adjacent: one 128-bit LDS read returns 4 workers' bits.
+// half-word are adjacent.  For the table lookups each group of 8 workers is
+// then regrouped in place, one 8x8 nibble transpose per (half-word, group):
+// afterwards one 32-bit LDS word holds the 8 workers' bits of the 4 elements a
+// lane owns.
 //
 // The average is an fp64 sum of +-scale over the workers in worker order.
 // When every partial sum of the segment's scales is exactly representable in
@@ -609,10 +612,35 @@ __device__ __forceinline__ void wave_sync()
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
-// LDS row stride (in 32-bit half-words) of the transposed sign staging: a
-// multiple of 4 keeps 128-bit reads aligned, and 36 puts the 8 half-words a
-// wave reads at once on disjoint banks.
-constexpr int kBitsStride = kServerRowBatch + 4;
+// LDS row stride (in 32-bit words) of the sign staging: a multiple of 4 keeps
+// 128-bit accesses aligned, and 40 puts the 64 words a wave reads at once in
+// the accumulation on 64 different banks.
+constexpr int kBitsStride = kServerRowBatch + 8;
+
+// 8x8 transpose of 4-bit entries held in 8 words: nibble s of a[k] moves to
+// nibble k of a[s] (three rounds of block swaps: 4x4, 2x2, 1x1 nibbles).
+__device__ __forceinline__ void transpose_nibbles8(uint32_t (&a)[8])
+{
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+        const uint32_t t = ((a[k] >> 16) ^ a[k + 4]) & 0x0000FFFFu;
+        a[k] ^= t << 16;
+        a[k + 4] ^= t;
+    }
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const int k = (i & 1) + 4 * (i >> 1);  // 0, 1, 4, 5
+        const uint32_t t = ((a[k] >> 8) ^ a[k + 2]) & 0x00FF00FFu;
+        a[k] ^= t << 8;
+        a[k + 2] ^= t;
+    }
+#pragma unroll
+    for (int k = 0; k < 8; k += 2) {
+        const uint32_t t = ((a[k] >> 4) ^ a[k + 1]) & 0x0F0F0F0Fu;
+        a[k] ^= t << 4;
+        a[k + 1] ^= t;
+    }
+}
 
 __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))) void k_server_pass(
     const Tile *__restrict__ tiles, int64_t tile_begin, int64_t tile_count, int n,
@@ -713,6 +741,22 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))) voi
                 }
                 s_lut4[wv][q][idx] = v;
             }
+            // regroup each (half-word, group of 8 workers) block in place
+            const int groups8 = (rows + 7) >> 3;
+#pragma unroll 1
+            for (int k = 0; k < (2 * kTileWords) * (kServerRowBatch / 8) / kWave; ++k) {
+                const int blk = lane + kWave * k;
+                const int hwb = blk & (2 * kTileWords - 1), gb = blk / (2 * kTileWords);
+                if (gb < groups8) {
+                    uint32_t *p = &s_bits[wv][hwb][8 * gb];
+                    const uint4 u0 = *(const uint4 *)p;
+                    const uint4 u1 = *(const uint4 *)(p + 4);
+                    uint32_t a[8] = {u0.x, u0.y, u0.z, u0.w, u1.x, u1.y, u1.z, u1.w};
+                    transpose_nibbles8(a);
+                    *(uint4 *)p = make_uint4(a[0], a[1], a[2], a[3]);
+                    *(uint4 *)(p + 4) = make_uint4(a[4], a[5], a[6], a[7]);
+                }
+            }
             wave_sync();
             // two groups of 8 workers at a time
             for (int g0 = 0; 8 * g0 < rows; g0 += 2) {
@@ -727,21 +771,31 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))) voi
                 const int gcnt = min(2, ((rows + 7) >> 3) - g0);
                 for (int g = 0; g < gcnt; ++g) {
                     const int r8 = 8 * (g0 + g);
+                    // two sub-blocks at a time: their 8 table indices first,
+                    // then the 8 lookups, then the adds, so that the LDS round
+                    // trips overlap
 #pragma unroll
-                    for (int b = 0; b < kSubBlocks; ++b) {
-                        const int hw = 2 * (4 * b + (lane >> 4)) + half;
-                        const uint4 lo = *(const uint4 *)&s_bits[wv][hw][r8];
-                        const uint4 hi = *(const uint4 *)&s_bits[wv][hw][r8 + 4];
-                        const uint32_t xl = ((lo.x >> shift) & 0xFu) | (((lo.y >> shift) & 0xFu) << 4) |
-                                            (((lo.z >> shift) & 0xFu) << 8) | (((lo.w >> shift) & 0xFu) << 12);
-                        const uint32_t xh = ((hi.x >> shift) & 0xFu) | (((hi.y >> shift) & 0xFu) << 4) |
-                                            (((hi.z >> shift) & 0xFu) << 8) | (((hi.w >> shift) & 0xFu) << 12);
-                        const uint32_t yl = transpose4x4(xl), yh = transpose4x4(xh);
+                    for (int bh = 0; bh < kSubBlocks; bh += 2) {
+                        uint32_t idx[2][4];
 #pragma unroll
-                        for (int c = 0; c < 4; ++c) {
-                            const uint32_t idx = ((yl >> (4 * c)) & 0xFu) | (((yh >> (4 * c)) & 0xFu) << 4);
-                            sum[b][c] += s_lut8[wv][g][idx];
+                        for (int bb = 0; bb < 2; ++bb) {
+                            const int hw = 2 * (4 * (bh + bb) + (lane >> 4)) + half;
+                            // nibble k: worker r8 + k's bits of the lane's 4 elements
+                            const uint32_t x = s_bits[wv][hw][r8 + (lane & 7)];
+                            const uint32_t yl = transpose4x4(x & 0xFFFFu), yh = transpose4x4(x >> 16);
+#pragma unroll
+                            for (int c = 0; c < 4; ++c)
+                                idx[bb][c] = ((yl >> (4 * c)) & 0xFu) | (((yh >> (4 * c)) & 0xFu) << 4);
                         }
+                        double val[2][4];
+#pragma unroll
+                        for (int bb = 0; bb < 2; ++bb)
+#pragma unroll
+                            for (int c = 0; c < 4; ++c) val[bb][c] = s_lut8[wv][g][idx[bb][c]];
+#pragma unroll
+                        for (int bb = 0; bb < 2; ++bb)
+#pragma unroll
+                            for (int c = 0; c < 4; ++c) sum[bh + bb][c] += val[bb][c];
                     }
                 }
                 wave_sync();
@@ -760,7 +814,10 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))) voi
         }
         wave_sync();
     }
+    // sum / n rounded to fp64; for a power-of-two n that is an exact scaling
     const double dn = (double)n;
+    const bool pow2 = (n & (n - 1)) == 0;
+    const double inv_n = 1.0 / dn;
     double acc = 0.0;
 #pragma unroll
     for (int b = 0; b < kSubBlocks; ++b) {
@@ -769,7 +826,7 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))) voi
         uint32_t nib = 0;
 #pragma unroll
         for (int c = 0; c < 4; ++c) {
-            const float avg = (float)(sum[b][c] / dn);
+            const float avg = (float)(pow2 ? sum[b][c] * inv_n : sum[b][c] / dn);
             const float z = avg + error_of(cv[b][c], sprev);
             zv[c] = z;
             const bool valid = li + c < len;
