@@ -228,6 +228,12 @@ int onebit_plan_create(const int64_t *tensor_numel, int32_t num_tensors, int32_t
         delete p;
         return fail(ONEBIT_EINVAL, "too many segments");
     }
+    // one wave per tile must stay far inside a launch's 2^32 work items
+    if (p->T >= ((int64_t)1 << 25)) {
+        delete p;
+        return fail(ONEBIT_EINVAL, "%lld tiles: plans are limited to 2^25 tiles of %d elements",
+                    (long long)p->T, kTileElems);
+    }
 
     const size_t tiles_bytes = round_up(tiles.size() * sizeof(Tile) + 1, 256);
     const size_t seg_bytes = round_up((size_t)p->S * sizeof(int64_t), 256);

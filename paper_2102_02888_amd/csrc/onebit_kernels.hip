@@ -540,20 +540,25 @@ __global__ __launch_bounds__(kBlock) void k_finalize(
     int64_t scales_ld)
 {
     __shared__ double red[kBlock / kWave];
-    const int64_t p = (int64_t)blockIdx.x * (kBlock / THREADS) + threadIdx.x / THREADS;
-    if (p >= num_pairs) return;  // whole block or whole wave: uniform for THREADS
-    int64_t i, q;
-    if (server_form) {
-        const int cnt = je - jb;
-        i = 0;
-        q = (p / cnt) * n + jb + (p % cnt);
-    } else {
-        i = p / num_segments;
-        q = p % num_segments;
+    // THREADS lanes per pair; the grid may be smaller than the pair count, so
+    // each group of lanes strides over pairs (uniform per block or per wave)
+    const int64_t stride = (int64_t)gridDim.x * (kBlock / THREADS);
+    for (int64_t p = (int64_t)blockIdx.x * (kBlock / THREADS) + threadIdx.x / THREADS;
+         p < num_pairs; p += stride) {
+        int64_t i, q;
+        if (server_form) {
+            const int cnt = je - jb;
+            i = 0;
+            q = (p / cnt) * n + jb + (p % cnt);
+        } else {
+            i = p / num_segments;
+            q = p % num_segments;
+        }
+        const float s = finalize_one<THREADS>(partial + i * part_ld, tb.seg_tile_begin[q],
+                                              tb.seg_tile_end[q], tb.seg_len[q], red);
+        if (threadIdx.x % THREADS == 0) scales[i * scales_ld + q] = s;
+        if (THREADS > kWave) __syncthreads();  // red is reused by the next pair
     }
-    const float s = finalize_one<THREADS>(partial + i * part_ld, tb.seg_tile_begin[q],
-                                          tb.seg_tile_end[q], tb.seg_len[q], red);
-    if (threadIdx.x % THREADS == 0) scales[i * scales_ld + q] = s;
 }
 
 // ---------------------------------------------------------------------------
@@ -642,7 +647,7 @@ __device__ __forceinline__ void transpose_nibbles8(uint32_t (&a)[8])
     }
 }
 
-__global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))) void k_server_pass(
+__global__ __launch_bounds__(kBlock) void k_server_pass(
     const Tile *__restrict__ tiles, int64_t tile_begin, int64_t tile_count, int n,
     int grouping_limit, const uint64_t *__restrict__ wbits, int64_t bits_ld,
     int64_t bits_word_base, const float *__restrict__ wscales, int64_t scales_ld,
@@ -1020,10 +1025,15 @@ __global__ __launch_bounds__(kBlock) void k_l1_final(const double *__restrict__ 
     if (threadIdx.x == 0) out[0] = ((red[0] + red[1]) + red[2]) + red[3];
 }
 
-inline unsigned blocks_for(int64_t waves)
+// Workgroups for one wave per item.  Plans keep the tile count below 2^25, so
+// a grid of one wave per tile stays far below the 2^32 work-item limit;
+// kernels over larger item counts cap their grid and stride.
+inline int64_t blocks_for(int64_t waves)
 {
-    return (unsigned)((waves + kWavesPerBlock - 1) / kWavesPerBlock);
+    return (waves + kWavesPerBlock - 1) / kWavesPerBlock;
 }
+
+constexpr int64_t kMaxGridBlocks = 1 << 22;
 
 }  // namespace
 
@@ -1034,7 +1044,7 @@ static hipError_t launch_warmup_t(const DeviceTables &tb, int64_t num_tiles, flo
                                   float bc2, hipStream_t s)
 {
     const float omb1 = 1.0f - beta1, omb2 = 1.0f - beta2;
-    hipLaunchKernelGGL(k_warmup<G>, dim3(blocks_for(num_tiles)), dim3(kBlock), 0, s, tb.tiles,
+    hipLaunchKernelGGL(k_warmup<G>, dim3((unsigned)blocks_for(num_tiles)), dim3(kBlock), 0, s, tb.tiles,
                        num_tiles, x, m, v, (const typename G::T *)g, g_ld, n_grads, lr, beta1,
                        omb1, beta2, omb2, eps, use_bc, bc1, bc2);
     return hipGetLastError();
@@ -1058,10 +1068,6 @@ hipError_t launch_warmup(const DeviceTables &tb, int64_t num_tiles, float *x, fl
     }
 }
 
-// Cap on the worker grid (waves loop over the rest): keeps the launch's
-// work-item count far below 2^32.
-constexpr int64_t kMaxWorkerBlocks = 1 << 22;
-
 template <bool PACKED, class G>
 static void launch_worker_t(const DeviceTables &tb, int64_t num_tiles, const float *m,
                             const uint64_t *m_bits, const float *m_scales, const void *g,
@@ -1072,7 +1078,7 @@ static void launch_worker_t(const DeviceTables &tb, int64_t num_tiles, const flo
     const float omb1 = 1.0f - beta1;
     const int64_t groups = (n_local + group - 1) / group;
     const int64_t items = groups * num_tiles;
-    const int64_t blocks = std::min<int64_t>(blocks_for(items), kMaxWorkerBlocks);
+    const int64_t blocks = std::min(blocks_for(items), kMaxGridBlocks);
     hipLaunchKernelGGL((k_worker_pass<PACKED, G>), dim3((unsigned)blocks), dim3(kBlock), 0, s,
                        tb.tiles, num_tiles, m, m_bits, m_scales, (const typename G::T *)g, g_ld,
                        err, err_ld, scales, scales_ld, bits, bits_ld, partial, n_local, group,
@@ -1129,7 +1135,7 @@ hipError_t launch_adam_message(const DeviceTables &tb, int64_t num_tiles, const 
                                float bc2, hipStream_t s)
 {
     const float omb1 = 1.0f - beta1, omb2 = 1.0f - beta2;
-    hipLaunchKernelGGL(k_adam_message, dim3(blocks_for(num_tiles)), dim3(kBlock), 0, s,
+    hipLaunchKernelGGL(k_adam_message, dim3((unsigned)blocks_for(num_tiles)), dim3(kBlock), 0, s,
                        tb.tiles, num_tiles, bits, scales, x, m, v, lr, beta1, omb1, beta2, omb2,
                        eps, use_bc, bc1, bc2);
     return hipGetLastError();
@@ -1141,7 +1147,7 @@ static void launch_uncompressed_t(const DeviceTables &tb, int64_t num_tiles, flo
                                   float beta1, float eps, hipStream_t s)
 {
     const float omb1 = 1.0f - beta1;
-    hipLaunchKernelGGL(k_uncompressed<G>, dim3(blocks_for(num_tiles)), dim3(kBlock), 0, s,
+    hipLaunchKernelGGL(k_uncompressed<G>, dim3((unsigned)blocks_for(num_tiles)), dim3(kBlock), 0, s,
                        tb.tiles, num_tiles, x, m, v, (const typename G::T *)g, g_ld, n, lr, beta1,
                        omb1, eps);
 }
@@ -1167,7 +1173,7 @@ hipError_t launch_l1_norm(const DeviceTables &tb, int64_t num_tiles, const float
                           double *partial, double *out, hipStream_t s)
 {
     if (num_tiles > 0)
-        hipLaunchKernelGGL(k_l1_partial, dim3(blocks_for(num_tiles)), dim3(kBlock), 0, s,
+        hipLaunchKernelGGL(k_l1_partial, dim3((unsigned)blocks_for(num_tiles)), dim3(kBlock), 0, s,
                            tb.tiles, num_tiles, v, partial);
     hipLaunchKernelGGL(k_l1_final, dim3(1), dim3(kBlock), 0, s, partial, num_tiles, out);
     return hipGetLastError();
@@ -1176,7 +1182,7 @@ hipError_t launch_l1_norm(const DeviceTables &tb, int64_t num_tiles, const float
 hipError_t launch_decode(const DeviceTables &tb, int64_t num_tiles, const uint64_t *bits,
                          const float *scales, float *out, hipStream_t s)
 {
-    hipLaunchKernelGGL(k_decode, dim3(blocks_for(num_tiles)), dim3(kBlock), 0, s, tb.tiles,
+    hipLaunchKernelGGL(k_decode, dim3((unsigned)blocks_for(num_tiles)), dim3(kBlock), 0, s, tb.tiles,
                        num_tiles, bits, scales, out);
     return hipGetLastError();
 }
@@ -1188,11 +1194,14 @@ hipError_t launch_finalize(const DeviceTables &tb, int64_t max_seg_tiles, int64_
 {
     if (num_pairs <= 0) return hipSuccess;
     if (max_seg_tiles > 4 * kWave) {
-        hipLaunchKernelGGL(k_finalize<kBlock>, dim3((unsigned)num_pairs), dim3(kBlock), 0, s, tb,
+        hipLaunchKernelGGL(k_finalize<kBlock>, dim3((unsigned)std::min(num_pairs, kMaxGridBlocks)),
+                           dim3(kBlock), 0, s, tb,
                            num_pairs, num_segments, server_form, n, jb, je, partial, part_ld,
                            scales, scales_ld);
     } else {
-        hipLaunchKernelGGL(k_finalize<kWave>, dim3(blocks_for(num_pairs)), dim3(kBlock), 0, s,
+        hipLaunchKernelGGL(k_finalize<kWave>,
+                           dim3((unsigned)std::min(blocks_for(num_pairs), kMaxGridBlocks)),
+                           dim3(kBlock), 0, s,
                            tb, num_pairs, num_segments, server_form, n, jb, je, partial, part_ld,
                            scales, scales_ld);
     }
@@ -1208,7 +1217,7 @@ hipError_t launch_server_pass(const DeviceTables &tb, int64_t tile_begin, int64_
     int log2n = 0;
     while ((1 << log2n) < n) ++log2n;
     const int grouping_limit = 29 - log2n;
-    hipLaunchKernelGGL(k_server_pass, dim3(blocks_for(tile_count)), dim3(kBlock), 0, s,
+    hipLaunchKernelGGL(k_server_pass, dim3((unsigned)blocks_for(tile_count)), dim3(kBlock), 0, s,
                        tb.tiles, tile_begin, tile_count, n, grouping_limit, wbits, bits_ld,
                        bits_word_base, wscales, scales_ld, scales_seg_base, serr, sscales, sbits,
                        partial);
@@ -1219,7 +1228,7 @@ hipError_t launch_update(const DeviceTables &tb, int64_t num_tiles, const uint64
                          const float *sscales, float *x, float *m_out, const float *v,
                          float lr, float eps, hipStream_t s)
 {
-    hipLaunchKernelGGL(k_update, dim3(blocks_for(num_tiles)), dim3(kBlock), 0, s, tb.tiles,
+    hipLaunchKernelGGL(k_update, dim3((unsigned)blocks_for(num_tiles)), dim3(kBlock), 0, s, tb.tiles,
                        num_tiles, sbits, sscales, x, m_out, v, lr, eps);
     return hipGetLastError();
 }
@@ -1228,7 +1237,7 @@ hipError_t launch_materialize(const DeviceTables &tb, int64_t num_tiles, int row
                               const float *err, int64_t err_ld, const float *scales,
                               int64_t scales_ld, float *out, int64_t out_ld, hipStream_t s)
 {
-    hipLaunchKernelGGL(k_materialize, dim3(blocks_for(num_tiles)), dim3(kBlock), 0, s,
+    hipLaunchKernelGGL(k_materialize, dim3((unsigned)blocks_for(num_tiles)), dim3(kBlock), 0, s,
                        tb.tiles, num_tiles, rows, err, err_ld, scales, scales_ld, out, out_ld);
     return hipGetLastError();
 }

@@ -330,6 +330,15 @@ def test_free_running_ragged_edges(ob, dev, packed):
     _free_run(ob, dev, wl, packed=packed)
 
 
+def test_free_running_more_scale_pairs_than_grid(ob, dev):
+    """4,202 small tensors with n = 64: 64 x 268,928 (worker, segment) scale
+    reductions, more than one launch of the scale kernel covers in one pass
+    (its grid strides), and 63 of every 64 segments empty."""
+    wl = synth.Workload(name="pairs", numel=[64] * 4200 + [100, 3], n=64, warmup_steps=2,
+                        steps=3)
+    _free_run(ob, dev, wl)
+
+
 def test_free_running_single_worker(ob, dev):
     wl = synth.Workload(name="n1", numel=[70_000, 33], n=1, warmup_steps=2, steps=5)
     _free_run(ob, dev, wl)
