@@ -61,48 +61,111 @@ def measured_traffic(workload, kernel):
     return None if k is None else k["traffic_bytes"]
 
 
-def cpu_baseline(st, plan, wl, target_s=12.0, max_segments=3):
-    """Times the oracle (single thread) on whole segments of the workload:
-    every worker's pass over the segment, the owner's average and
-    recompression, and the update.  The oracle gets host copies of the
-    segment's device state."""
+def _host_segment(st, plan, q, b=None, e=None):
+    """Host copies of one segment's device state (or of its elements [b, e)),
+    as the oracle takes them."""
     import numpy as np
-
-    import oracle
-    segs = [0, plan.S - 1, plan.S // 2][:max_segments]
-    n = st.n_local
-    done, spent, used = 0, 0.0, []
-    for q in segs:
+    if b is None:
         b, e = int(plan.seg_begin[q]), int(plan.seg_end[q])
-        ln = e - b
-        if ln == 0:
-            continue
-        nw = (ln + 63) // 64
-        m = st.m[b:e].cpu().numpy().copy()
-        x = st.x[b:e].cpu().numpy().copy()
-        v = st.v[b:e].cpu().numpy().copy()
-        dbar = st.server_err[b:e].cpu().numpy().copy()
-        g = st.grads[:, b:e].cpu().numpy().copy()
-        delta = st.worker_err[:, b:e].cpu().numpy().copy()
-        wbits = np.zeros((n, nw), np.uint64)
-        wscales = np.zeros(n, np.float32)
-        sbits = np.zeros(nw, np.uint64)
-        z = np.zeros(ln, np.float32)
+    ln, n = e - b, st.n_local
+    nw = (ln + 63) // 64
+    return {"len": ln, "m": st.m[b:e].cpu().numpy().copy(), "x": st.x[b:e].cpu().numpy().copy(),
+            "v": st.v[b:e].cpu().numpy().copy(), "dbar": st.server_err[b:e].cpu().numpy().copy(),
+            "g": st.grads[:, b:e].cpu().numpy().copy(),
+            "delta": st.worker_err[:, b:e].cpu().numpy().copy(),
+            "wbits": np.zeros((n, nw), np.uint64), "wscales": np.zeros(n, np.float32),
+            "sbits": np.zeros(nw, np.uint64), "z": np.zeros(ln, np.float32)}
+
+
+def _oracle_segment(sd, wl):
+    """One compression step of the oracle over one segment: every worker's
+    pass, the owner's average and recompression, and the update."""
+    import oracle
+    ln, n = sd["len"], sd["g"].shape[0]
+    nw = sd["sbits"].shape[0]
+    for i in range(n):
+        sd["wscales"][i] = oracle.worker_segment(0, ln, wl.beta1, sd["m"], sd["g"][i],
+                                                 sd["delta"][i], sd["wbits"][i], sd["z"])
+    s = oracle.server_segment(0, ln, n, sd["wbits"].reshape(-1), nw, sd["wscales"], 1,
+                              sd["dbar"], sd["sbits"], sd["z"])
+    oracle.update_segment(0, ln, sd["sbits"], s, wl.lr, wl.eps, sd["x"], sd["m"], sd["v"])
+
+
+def cpu_baseline(st, plan, wl, target_s=10.0, threads=None, threaded_s=6.0):
+    """Times the oracle on the host cores over whole segments of the
+    workload (each segment: every worker's pass, the owner's average and
+    recompression, and the update; host copies of the device state).
+
+    Reported value: `threads` threads (the process's CPU share, at most 16),
+    each looping over its own pieces of chunk 0 for about `threaded_s`
+    seconds; the oracle releases the GIL, so the threads run in parallel.
+    Segments longer than chunk 0's length / (4 threads) are cut into
+    64-aligned slices, each run through the oracle's segment step (the same
+    per-element work; only the scale is taken over the slice).
+    Also reported: one thread over up to three whole segments."""
+    import threading
+
+    segs = [q for q in (0, plan.S - 1, plan.S // 2) if plan.seg_end[q] > plan.seg_begin[q]]
+    done1, spent1, used = 0, 0.0, []
+    for q in segs:
+        sd = _host_segment(st, plan, q)
         t0 = time.perf_counter()
-        for i in range(n):
-            wscales[i] = oracle.worker_segment(0, ln, wl.beta1, m, g[i], delta[i], wbits[i], z)
-        s = oracle.server_segment(0, ln, n, wbits.reshape(-1), nw, wscales, 1, dbar, sbits, z)
-        oracle.update_segment(0, ln, sbits, s, wl.lr, wl.eps, x, m, v)
-        spent += time.perf_counter() - t0
-        done += ln
+        _oracle_segment(sd, wl)
+        spent1 += time.perf_counter() - t0
+        done1 += sd["len"]
         used.append(q)
-        del g, delta
-        if spent >= target_s:
+        del sd
+        if spent1 >= target_s:
             break
-    return {"value": done / spent, "unit": "params/s", "cores": 1, "kind": "oracle",
-            "sample": "%d whole segment(s) %s of %d (%d params, all %d workers' passes, the "
-                      "chunk owner's average and recompression, and the update), %.1f s"
-                      % (len(used), used, plan.S, done, n, spent)}
+    single = {"value": done1 / spent1, "cores": 1,
+              "sample": "%d whole segment(s) %s of %d (%d params), %.1f s"
+                        % (len(used), used, plan.S, done1, spent1)}
+
+    if threads is None:
+        threads = max(1, min(16, len(os.sched_getaffinity(0))))
+    chunk0 = [q for q in range(0, plan.S, plan.n) if plan.seg_end[q] > plan.seg_begin[q]]
+    total = sum(int(plan.seg_end[q] - plan.seg_begin[q]) for q in chunk0)
+    piece = max(64, (total // (4 * threads)) // 64 * 64)
+    data = []
+    for q in chunk0:
+        for b in range(int(plan.seg_begin[q]), int(plan.seg_end[q]), piece):
+            data.append(_host_segment(st, plan, q, b, min(b + piece, int(plan.seg_end[q]))))
+    data.sort(key=lambda sd: -sd["len"])
+    share = [[] for _ in range(threads)]
+    load = [0] * threads
+    for sd in data:  # largest first onto the least loaded thread
+        k = load.index(min(load))
+        share[k].append(sd)
+        load[k] += sd["len"]
+    counts = [0] * threads
+    start = threading.Barrier(threads + 1)
+    t_end = [0.0]
+
+    def run(k):
+        start.wait()
+        while share[k] and time.perf_counter() < t_end[0]:
+            for sd in share[k]:
+                _oracle_segment(sd, wl)
+                counts[k] += sd["len"]
+                if time.perf_counter() >= t_end[0]:
+                    break
+
+    pool = [threading.Thread(target=run, args=(k,)) for k in range(threads)]
+    for th in pool:
+        th.start()
+    t0 = time.perf_counter()
+    t_end[0] = t0 + threaded_s
+    start.wait()
+    for th in pool:
+        th.join()
+    wall = time.perf_counter() - t0
+    return {"value": sum(counts) / wall, "unit": "params/s", "cores": threads, "kind": "oracle",
+            "sample": "%d threads looping over chunk 0 (%d segment(s), %d params, in %d "
+                      "pieces of at most %d; all %d workers' passes, the chunk owner's average "
+                      "and recompression, and the update) for %.1f s: %d params"
+                      % (threads, len(chunk0), total, len(data), piece, st.n_local, wall,
+                         sum(counts)),
+            "single_thread": single}
 
 
 def hbm_probe(dev, nbytes=2 << 30, reps=10):
