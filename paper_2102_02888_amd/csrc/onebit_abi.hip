@@ -9,6 +9,7 @@
 #include <cstdint>
 #include <cstdio>
 #include <cstring>
+#include <memory>
 #include <new>
 #include <vector>
 
@@ -26,7 +27,7 @@ struct onebit_plan_s {
     int64_t max_seg_tiles = 0;                          // most tiles in one segment
     std::vector<int64_t> tensor_off, seg_begin, seg_end;
     std::vector<int64_t> seg_tile_begin, seg_tile_end;  // [S]
-    std::vector<int64_t> chunk_tile_begin;              // [n+1]
+    std::vector<int64_t> chunk_tile_begin;              // [n+1], into chunk_tiles
     std::vector<int64_t> chunk_word_lo, chunk_word_hi;  // [n], words touched by chunk j
     void *dev_mem = nullptr;                            // one allocation for all tables
     DeviceTables tb{};
@@ -126,6 +127,134 @@ int64_t chunk_len(int64_t d, int32_t n)
     return per * 64;
 }
 
+// Builds the layout and tile tables of a plan (arguments already checked).
+// Host allocations may throw std::bad_alloc; the caller turns that into
+// ONEBIT_ENOMEM.
+int plan_create_impl(const int64_t *tensor_numel, int32_t num_tensors, int32_t n_workers,
+                     onebit_plan *out)
+{
+    std::unique_ptr<onebit_plan_s> owner(new onebit_plan_s);
+    onebit_plan_s *p = owner.get();
+    hipError_t e = hipGetDevice(&p->device);
+    if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+    const int32_t K = num_tensors, n = n_workers;
+    p->K = K;
+    p->n = n;
+    p->S = (int64_t)K * n;
+    p->tensor_off.resize(K);
+    p->seg_begin.resize(p->S);
+    p->seg_end.resize(p->S);
+    int64_t off = 0, d = 0;
+    for (int32_t k = 0; k < K; ++k) {
+        const int64_t dk = tensor_numel[k];
+        const int64_t c = chunk_len(dk, n);
+        p->tensor_off[k] = off;
+        for (int32_t j = 0; j < n; ++j) {
+            const int64_t b = std::min<int64_t>((int64_t)j * c, dk);
+            const int64_t en = std::min<int64_t>((int64_t)(j + 1) * c, dk);
+            p->seg_begin[(int64_t)k * n + j] = off + b;
+            p->seg_end[(int64_t)k * n + j] = off + en;
+        }
+        off += (dk + 63) / 64 * 64;
+        d += dk;
+        if (off >= ((int64_t)1 << 40))
+            return fail(ONEBIT_EINVAL, "padded length exceeds 2^40 elements");
+    }
+    p->d = d;
+    p->D = off;
+    p->W = off / 64;
+
+    // One wave per tile must stay far inside a launch's 2^32 work items.
+    int64_t tile_count = 0;
+    for (int64_t q = 0; q < p->S; ++q)
+        tile_count += (p->seg_end[q] - p->seg_begin[q] + kTileElems - 1) / kTileElems;
+    if (tile_count >= ((int64_t)1 << 25))
+        return fail(ONEBIT_EINVAL, "%lld tiles: plans are limited to 2^25 tiles of %d elements",
+                    (long long)tile_count, kTileElems);
+
+    // Tiles in address order (segment by segment), so that passes over all
+    // of d stream through memory; the tiles of chunk owner j are listed
+    // separately, chunk-major, as one contiguous range of chunk_tiles.
+    std::vector<Tile> tiles;
+    tiles.reserve(tile_count);
+    p->seg_tile_begin.assign(p->S, 0);
+    p->seg_tile_end.assign(p->S, 0);
+    p->chunk_tile_begin.assign(n + 1, 0);
+    p->chunk_word_lo.assign(n, INT64_MAX);
+    p->chunk_word_hi.assign(n, -1);
+    std::vector<int64_t> seg_len(p->S);
+    for (int64_t q = 0; q < p->S; ++q) {
+        const int64_t b = p->seg_begin[q], en = p->seg_end[q];
+        seg_len[q] = en - b;
+        p->seg_tile_begin[q] = (int64_t)tiles.size();
+        for (int64_t s = b; s < en; s += kTileElems) {
+            Tile t;
+            t.start = s;
+            t.len = (int32_t)std::min<int64_t>(kTileElems, en - s);
+            t.seg = (int32_t)q;
+            tiles.push_back(t);
+        }
+        p->seg_tile_end[q] = (int64_t)tiles.size();
+        p->max_seg_tiles = std::max(p->max_seg_tiles, p->seg_tile_end[q] - p->seg_tile_begin[q]);
+    }
+    std::vector<int32_t> chunk_tiles;
+    chunk_tiles.reserve(tiles.size());
+    for (int32_t j = 0; j < n; ++j) {
+        p->chunk_tile_begin[j] = (int64_t)chunk_tiles.size();
+        for (int32_t k = 0; k < K; ++k) {
+            const int64_t q = (int64_t)k * n + j;
+            for (int64_t t = p->seg_tile_begin[q]; t < p->seg_tile_end[q]; ++t)
+                chunk_tiles.push_back((int32_t)t);
+            const int64_t b = p->seg_begin[q], en = p->seg_end[q];
+            if (en > b) {
+                p->chunk_word_lo[j] = std::min(p->chunk_word_lo[j], b / 64);
+                p->chunk_word_hi[j] = std::max(p->chunk_word_hi[j], (en - 1) / 64);
+            }
+        }
+    }
+    p->chunk_tile_begin[n] = (int64_t)chunk_tiles.size();
+    p->T = (int64_t)tiles.size();
+
+    const size_t tiles_bytes = round_up(tiles.size() * sizeof(Tile) + 1, 256);
+    const size_t order_bytes = round_up(chunk_tiles.size() * sizeof(int32_t) + 1, 256);
+    const size_t seg_bytes = round_up((size_t)p->S * sizeof(int64_t), 256);
+    const size_t total = tiles_bytes + order_bytes + 3 * seg_bytes;
+    const size_t seg0 = tiles_bytes + order_bytes;
+    std::vector<char> host(total, 0);
+    if (!tiles.empty()) {
+        std::memcpy(host.data(), tiles.data(), tiles.size() * sizeof(Tile));
+        std::memcpy(host.data() + tiles_bytes, chunk_tiles.data(),
+                    chunk_tiles.size() * sizeof(int32_t));
+    }
+    std::memcpy(host.data() + seg0, p->seg_tile_begin.data(), p->S * sizeof(int64_t));
+    std::memcpy(host.data() + seg0 + seg_bytes, p->seg_tile_end.data(), p->S * sizeof(int64_t));
+    std::memcpy(host.data() + seg0 + 2 * seg_bytes, seg_len.data(), p->S * sizeof(int64_t));
+    // Every host allocation is done; from here on nothing throws.
+    e = hipMalloc(&p->dev_mem, total);
+    if (e != hipSuccess)
+        return fail(ONEBIT_ENOMEM, "hipMalloc of %zu bytes of plan tables: %s", total,
+                    hipGetErrorString(e));
+    e = hipMemcpy(p->dev_mem, host.data(), total, hipMemcpyHostToDevice);
+    if (e != hipSuccess) {
+        (void)hipFree(p->dev_mem);
+        return hip_fail(e, "hipMemcpy of plan tables");
+    }
+    char *base = (char *)p->dev_mem;
+    Tile *d_tiles = (Tile *)base;
+    int32_t *d_order = (int32_t *)(base + tiles_bytes);
+    int64_t *d_stb = (int64_t *)(base + seg0);
+    int64_t *d_ste = (int64_t *)(base + seg0 + seg_bytes);
+    int64_t *d_sl = (int64_t *)(base + seg0 + 2 * seg_bytes);
+    p->tb.tiles = d_tiles;
+    p->tb.chunk_tiles = d_order;
+    p->tb.seg_tile_begin = d_stb;
+    p->tb.seg_tile_end = d_ste;
+    p->tb.seg_len = d_sl;
+    p->workspace_bytes = server_partial_offset(p) + round_up((size_t)p->T * sizeof(double) + 1, 256);
+    *out = owner.release();
+    return ONEBIT_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -154,121 +283,14 @@ int onebit_plan_create(const int64_t *tensor_numel, int32_t num_tensors, int32_t
     if (n_workers < 1) return fail(ONEBIT_EINVAL, "n_workers < 1");
     for (int32_t k = 0; k < num_tensors; ++k)
         if (tensor_numel[k] < 0) return fail(ONEBIT_EINVAL, "tensor_numel[%d] < 0", k);
-
-    onebit_plan_s *p = new (std::nothrow) onebit_plan_s;
-    if (!p) return fail(ONEBIT_ENOMEM, "host allocation failed");
-    hipError_t e = hipGetDevice(&p->device);
-    if (e != hipSuccess) {
-        delete p;
-        return hip_fail(e, "hipGetDevice");
+    if ((int64_t)num_tensors * n_workers > INT32_MAX)
+        return fail(ONEBIT_EINVAL, "num_tensors * n_workers = %lld segments exceeds 2^31 - 1",
+                    (long long)num_tensors * n_workers);
+    try {
+        return plan_create_impl(tensor_numel, num_tensors, n_workers, out);
+    } catch (const std::bad_alloc &) {
+        return fail(ONEBIT_ENOMEM, "host allocation failed");
     }
-    const int32_t K = num_tensors, n = n_workers;
-    p->K = K;
-    p->n = n;
-    p->S = (int64_t)K * n;
-    p->tensor_off.resize(K);
-    p->seg_begin.resize(p->S);
-    p->seg_end.resize(p->S);
-    int64_t off = 0, d = 0;
-    for (int32_t k = 0; k < K; ++k) {
-        const int64_t dk = tensor_numel[k];
-        const int64_t c = chunk_len(dk, n);
-        p->tensor_off[k] = off;
-        for (int32_t j = 0; j < n; ++j) {
-            const int64_t b = std::min<int64_t>((int64_t)j * c, dk);
-            const int64_t en = std::min<int64_t>((int64_t)(j + 1) * c, dk);
-            p->seg_begin[(int64_t)k * n + j] = off + b;
-            p->seg_end[(int64_t)k * n + j] = off + en;
-        }
-        off += (dk + 63) / 64 * 64;
-        d += dk;
-        if (off >= ((int64_t)1 << 40)) {
-            delete p;
-            return fail(ONEBIT_EINVAL, "padded length exceeds 2^40 elements");
-        }
-    }
-    p->d = d;
-    p->D = off;
-    p->W = off / 64;
-
-    // Tiles in chunk-major order, so that the tiles of chunk owner j are one
-    // contiguous range.
-    std::vector<Tile> tiles;
-    p->seg_tile_begin.assign(p->S, 0);
-    p->seg_tile_end.assign(p->S, 0);
-    p->chunk_tile_begin.assign(n + 1, 0);
-    p->chunk_word_lo.assign(n, INT64_MAX);
-    p->chunk_word_hi.assign(n, -1);
-    std::vector<int64_t> seg_len(p->S);
-    for (int32_t j = 0; j < n; ++j) {
-        p->chunk_tile_begin[j] = (int64_t)tiles.size();
-        for (int32_t k = 0; k < K; ++k) {
-            const int64_t q = (int64_t)k * n + j;
-            const int64_t b = p->seg_begin[q], en = p->seg_end[q];
-            seg_len[q] = en - b;
-            p->seg_tile_begin[q] = (int64_t)tiles.size();
-            for (int64_t s = b; s < en; s += kTileElems) {
-                Tile t;
-                t.start = s;
-                t.len = (int32_t)std::min<int64_t>(kTileElems, en - s);
-                t.seg = (int32_t)q;
-                tiles.push_back(t);
-            }
-            p->seg_tile_end[q] = (int64_t)tiles.size();
-            p->max_seg_tiles = std::max(p->max_seg_tiles, p->seg_tile_end[q] - p->seg_tile_begin[q]);
-            if (en > b) {
-                p->chunk_word_lo[j] = std::min(p->chunk_word_lo[j], b / 64);
-                p->chunk_word_hi[j] = std::max(p->chunk_word_hi[j], (en - 1) / 64);
-            }
-        }
-    }
-    p->chunk_tile_begin[n] = (int64_t)tiles.size();
-    p->T = (int64_t)tiles.size();
-    if (p->S > INT32_MAX) {
-        delete p;
-        return fail(ONEBIT_EINVAL, "too many segments");
-    }
-    // one wave per tile must stay far inside a launch's 2^32 work items
-    if (p->T >= ((int64_t)1 << 25)) {
-        delete p;
-        return fail(ONEBIT_EINVAL, "%lld tiles: plans are limited to 2^25 tiles of %d elements",
-                    (long long)p->T, kTileElems);
-    }
-
-    const size_t tiles_bytes = round_up(tiles.size() * sizeof(Tile) + 1, 256);
-    const size_t seg_bytes = round_up((size_t)p->S * sizeof(int64_t), 256);
-    const size_t total = tiles_bytes + 3 * seg_bytes;
-    e = hipMalloc(&p->dev_mem, total);
-    if (e != hipSuccess) {
-        delete p;
-        return fail(ONEBIT_ENOMEM, "hipMalloc of %zu bytes of plan tables: %s", total,
-                    hipGetErrorString(e));
-    }
-    char *base = (char *)p->dev_mem;
-    Tile *d_tiles = (Tile *)base;
-    int64_t *d_stb = (int64_t *)(base + tiles_bytes);
-    int64_t *d_ste = (int64_t *)(base + tiles_bytes + seg_bytes);
-    int64_t *d_sl = (int64_t *)(base + tiles_bytes + 2 * seg_bytes);
-    std::vector<char> host(total, 0);
-    if (!tiles.empty()) std::memcpy(host.data(), tiles.data(), tiles.size() * sizeof(Tile));
-    std::memcpy(host.data() + tiles_bytes, p->seg_tile_begin.data(), p->S * sizeof(int64_t));
-    std::memcpy(host.data() + tiles_bytes + seg_bytes, p->seg_tile_end.data(),
-                p->S * sizeof(int64_t));
-    std::memcpy(host.data() + tiles_bytes + 2 * seg_bytes, seg_len.data(),
-                p->S * sizeof(int64_t));
-    e = hipMemcpy(p->dev_mem, host.data(), total, hipMemcpyHostToDevice);
-    if (e != hipSuccess) {
-        (void)hipFree(p->dev_mem);
-        delete p;
-        return hip_fail(e, "hipMemcpy of plan tables");
-    }
-    p->tb.tiles = d_tiles;
-    p->tb.seg_tile_begin = d_stb;
-    p->tb.seg_tile_end = d_ste;
-    p->tb.seg_len = d_sl;
-    p->workspace_bytes = server_partial_offset(p) + round_up((size_t)p->T * sizeof(double) + 1, 256);
-    *out = p;
-    return ONEBIT_OK;
 }
 
 int onebit_plan_destroy(onebit_plan p)

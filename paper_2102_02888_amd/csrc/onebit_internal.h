@@ -25,7 +25,8 @@ constexpr int kServerRowBatch = 32;                 // worker rows staged in LDS
 
 // Device-side layout tables owned by a plan.
 struct DeviceTables {
-    const Tile *tiles;             // [T], chunk-major order
+    const Tile *tiles;             // [T], in address (segment) order
+    const int32_t *chunk_tiles;    // [T], tile ids in chunk-major order
     const int64_t *seg_tile_begin; // [S]
     const int64_t *seg_tile_end;   // [S]
     const int64_t *seg_len;        // [S]

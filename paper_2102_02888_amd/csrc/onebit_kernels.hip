@@ -648,7 +648,8 @@ __device__ __forceinline__ void transpose_nibbles8(uint32_t (&a)[8])
 }
 
 __global__ __launch_bounds__(kBlock) void k_server_pass(
-    const Tile *__restrict__ tiles, int64_t tile_begin, int64_t tile_count, int n,
+    const Tile *__restrict__ tiles, const int32_t *__restrict__ chunk_tiles, int64_t tile_begin,
+    int64_t tile_count, int n,
     int grouping_limit, const uint64_t *__restrict__ wbits, int64_t bits_ld,
     int64_t bits_word_base, const float *__restrict__ wscales, int64_t scales_ld,
     int64_t scales_seg_base, float *__restrict__ serr, const float *__restrict__ sscales,
@@ -663,7 +664,7 @@ __global__ __launch_bounds__(kBlock) void k_server_pass(
     const int wv = threadIdx.x >> 6;
     const int64_t rel = (int64_t)blockIdx.x * kWavesPerBlock + wv;
     if (rel >= tile_count) return;
-    const int64_t t = tile_begin + rel;
+    const int64_t t = chunk_tiles[tile_begin + rel];
     const Tile tile = tiles[t];
     const int len = tile.len;
     const int64_t base = tile.start;
@@ -1218,7 +1219,8 @@ hipError_t launch_server_pass(const DeviceTables &tb, int64_t tile_begin, int64_
     while ((1 << log2n) < n) ++log2n;
     const int grouping_limit = 29 - log2n;
     hipLaunchKernelGGL(k_server_pass, dim3((unsigned)blocks_for(tile_count)), dim3(kBlock), 0, s,
-                       tb.tiles, tile_begin, tile_count, n, grouping_limit, wbits, bits_ld,
+                       tb.tiles, tb.chunk_tiles, tile_begin, tile_count, n, grouping_limit,
+                       wbits, bits_ld,
                        bits_word_base, wscales, scales_ld, scales_seg_base, serr, sscales, sbits,
                        partial);
     return hipGetLastError();
