@@ -699,14 +699,20 @@ __global__ __launch_bounds__(kBlock) void k_server_pass(
     };
     load_batch(0);
 
+    // exponent range of the segment's nonzero scales (one batch: the scales
+    // just loaded; more: read them all)
     int emax = 0, emin = 1 << 20;
-    for (int r = lane; r < n; r += kWave) {
-        const uint32_t u = __float_as_uint(wscales[(int64_t)r * scales_ld + sq]) & 0x7FFFFFFFu;
-        if (u == 0) continue;
+    auto widen = [&](float sc) {
+        const uint32_t u = __float_as_uint(sc) & 0x7FFFFFFFu;
+        if (u == 0) return;
         const int e = max((int)(u >> 23), 1);
         emax = max(emax, e);
         emin = min(emin, e);
-    }
+    };
+    if (n <= kServerRowBatch)
+        widen(scl);
+    else
+        for (int r = lane; r < n; r += kWave) widen(wscales[(int64_t)r * scales_ld + sq]);
     emax = wave_max(emax);
     emin = wave_min(emin);
     const bool grouped = emax < 255 && (emax == 0 || emax - emin <= grouping_limit);
@@ -733,8 +739,10 @@ __global__ __launch_bounds__(kBlock) void k_server_pass(
         if (lane < rows) s_scale[wv][lane] = scl;
         wave_sync();
         if (grouped) {
-            // 16-entry tables of 4 workers (rows past the last worker add 0)
-            for (int e = lane; e < 16 * (kServerRowBatch / 4); e += kWave) {
+            // 16-entry tables of 4 workers, two per group of 8 (rows past the
+            // last worker add 0)
+            const int groups8 = (rows + 7) >> 3;
+            for (int e = lane; e < 32 * groups8; e += kWave) {
                 const int q = e >> 4, idx = e & 15;
                 double v = 0.0;
 #pragma unroll
@@ -748,7 +756,6 @@ __global__ __launch_bounds__(kBlock) void k_server_pass(
                 s_lut4[wv][q][idx] = v;
             }
             // regroup each (half-word, group of 8 workers) block in place
-            const int groups8 = (rows + 7) >> 3;
 #pragma unroll 1
             for (int k = 0; k < (2 * kTileWords) * (kServerRowBatch / 8) / kWave; ++k) {
                 const int blk = lane + kWave * k;
@@ -766,15 +773,17 @@ __global__ __launch_bounds__(kBlock) void k_server_pass(
             wave_sync();
             // two groups of 8 workers at a time
             for (int g0 = 0; 8 * g0 < rows; g0 += 2) {
+                const int gcnt = min(2, groups8 - g0);
 #pragma unroll
                 for (int k = 0; k < 512 / kWave; ++k) {
                     const int e = lane + kWave * k;
-                    const int g = e >> 8, idx = e & 255;
-                    const int q = 2 * (g0 + g);
-                    s_lut8[wv][g][idx] = s_lut4[wv][q][idx & 15] + s_lut4[wv][q + 1][idx >> 4];
+                    const int g = e >> 8, idx = e & 255;  // g = k / 4: uniform
+                    if (g < gcnt) {
+                        const int q = 2 * (g0 + g);
+                        s_lut8[wv][g][idx] = s_lut4[wv][q][idx & 15] + s_lut4[wv][q + 1][idx >> 4];
+                    }
                 }
                 wave_sync();
-                const int gcnt = min(2, ((rows + 7) >> 3) - g0);
                 for (int g = 0; g < gcnt; ++g) {
                     const int r8 = 8 * (g0 + g);
                     // two sub-blocks at a time: their 8 table indices first,
