@@ -411,6 +411,9 @@ def main():
     per_step = sorted(ev[0].elapsed_time(ev[3]) for ev in events)
 
     bw, bs, bu = algorithmic_bytes_per_param(n, gbytes)
+    gname = {"f32": "GradF32", "bf16": "GradBF16", "f16": "GradF16"}[args.grad_dtype]
+    # the first warm-up step is a cold start; later ones are timed
+    warm_avg = sum(warm_ms[1:]) / (len(warm_ms) - 1) if len(warm_ms) > 1 else None
     d = plan.d
     step_bytes = d * (bw + bs + bu)
     worker_bytes = d * bw
@@ -441,13 +444,23 @@ def main():
                       "decompress_update": part_ms[2], "sum": gpu_step_ms},
         "gpu_step_ms": {"median": per_step[len(per_step) // 2], "min": per_step[0],
                         "max": per_step[-1]},
-        "warmup_adam_step_ms": sum(warm_ms[1:]) / max(1, len(warm_ms) - 1) if warm_ms else None,
-        "roofline": {"bound": "hbm", "kernel": "worker_compress (k_worker_pass<true, GradF32>: packed momentum, fp32 gradients)",
+        "warmup_adam_step_ms": warm_avg,
+        "roofline": {"bound": "hbm",
+                     "kernel": "worker_compress (k_worker_pass<true, %s>: packed momentum, %s "
+                               "gradients)" % (gname, args.grad_dtype),
                      "achieved": achieved, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
                      "frac": achieved / HBM_PEAK_GBPS,
-                     "traffic": (measured_traffic(wl.name, "k_worker_pass<true, GradF32>")
-                                 if args.grad_dtype == "f32" else None),
+                     "traffic": measured_traffic(wl.name, "k_worker_pass<true, %s>" % gname),
                      "algorithmic_bytes_per_launch": worker_bytes},
+        "kernels": {name: {"ms": ms, "algorithmic_bytes": nbytes,
+                           "gbps": nbytes / (ms * 1e-3) / 1e9,
+                           "frac": nbytes / (ms * 1e-3) / 1e9 / HBM_PEAK_GBPS}
+                    for name, ms, nbytes in (
+                        ("worker_compress", part_ms[0], worker_bytes),
+                        ("server_reduce_compress", part_ms[1], d * bs),
+                        ("decompress_update", part_ms[2], d * bu),
+                        ("warmup_adam_step", warm_avg, d * (n * gbytes + 24)))
+                    if ms},
     }
     if not args.no_probe:
         del events

@@ -70,6 +70,10 @@ def test_argument_errors_before_device(native):
     bad = (ctypes.c_int64 * 2)(10, -1)
     assert lib.onebit_plan_create(bad, 2, 4, ctypes.byref(out)) == -1
     assert b"tensor_numel[1]" in lib.onebit_last_error()
+    # K * n segments must fit in int32; refused before any device call
+    many = (ctypes.c_int64 * (1 << 20))()
+    assert lib.onebit_plan_create(many, 1 << 20, 1 << 12, ctypes.byref(out)) == -1
+    assert b"segments" in lib.onebit_last_error()
     for fn in ["onebit_plan_destroy"]:
         assert getattr(lib, fn)(None) == -1
     assert lib.onebit_plan_get_info(None, None) == -1

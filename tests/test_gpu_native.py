@@ -120,6 +120,11 @@ def test_argument_errors_on_device_buffers(dev):
     # warm-up step numbers are 1-based
     assert L.onebit_warmup_adam_step(plan.handle, p(st.x), p(st.m), p(st.v), p(st.grads), 0,
                                      plan.D, n, 1e-3, 0.9, 0.999, 1e-8, 0, 0, s0) == -1
+    # plans over 2^25 tiles are refused (one wave per tile must fit a launch)
+    huge = (ctypes.c_int64 * 1)(1 << 35)
+    out = ctypes.c_void_p()
+    assert L.onebit_plan_create(huge, 1, 1, ctypes.byref(out)) == -1
+    assert b"tiles" in L.onebit_last_error() and out.value is None
     torch.cuda.synchronize()
     assert torch.equal(st.x, before)
     # a correct call still goes through afterwards
