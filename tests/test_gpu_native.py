@@ -132,3 +132,46 @@ def test_argument_errors_on_device_buffers(dev):
     torch.cuda.synchronize()
     assert not torch.equal(st.x, before)
     plan.close()
+
+
+def test_one_plan_two_streams(dev):
+    """One plan driven from two streams at once, each state with its own
+    workspace, gives the same bits as running the two states one after the
+    other."""
+    import paper_2102_02888_amd as ob
+    numel, n = [300_000, 5000, 64], 4
+    plan = ob.Plan(numel, n)
+    wl = synth.Workload(name="streams", numel=numel, n=n, warmup_steps=2, steps=0)
+
+    def make():
+        st = ob.State(plan, dev)
+        st.x.copy_(torch.from_numpy(synth.host_params(wl, plan.D)).to(dev))
+        return st
+
+    states = [make() for _ in range(4)]  # [a, b] concurrent, [c, d] sequential
+    grads = [torch.from_numpy(synth.host_grads(wl, plan.D, plan.tensor_off, t)).to(dev)
+             for t in range(1, 6)]
+    torch.cuda.synchronize()
+    streams = [torch.cuda.Stream(), torch.cuda.Stream()]
+    for t, g in enumerate(grads, start=1):
+        for k, st in enumerate(states):
+            st.grads.copy_(g if k % 2 == 0 else g * 0.5)
+        torch.cuda.synchronize()
+        for k in (0, 1):
+            with torch.cuda.stream(streams[k]):
+                if t <= 2:
+                    states[k].warmup(wl.lr, wl.beta1, wl.beta2, wl.eps, t)
+                else:
+                    states[k].step(wl.lr, wl.beta1, wl.eps)
+        for k in (2, 3):
+            if t <= 2:
+                states[k].warmup(wl.lr, wl.beta1, wl.beta2, wl.eps, t)
+            else:
+                states[k].step(wl.lr, wl.beta1, wl.eps)
+        torch.cuda.synchronize()
+    for a, b in ((0, 2), (1, 3)):
+        for name in ("x", "worker_err", "worker_bits", "worker_scales", "server_err",
+                     "server_bits", "server_scales"):
+            assert host(getattr(states[a], name)).tobytes() == \
+                host(getattr(states[b], name)).tobytes(), (a, name)
+    plan.close()
