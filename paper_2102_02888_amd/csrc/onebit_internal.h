@@ -18,6 +18,9 @@ struct Tile {
 constexpr int kWave = 64;
 constexpr int kWavesPerBlock = 4;
 constexpr int kBlock = kWave * kWavesPerBlock;
+// The worker pass runs smaller workgroups (measured ~2% faster than 4 waves).
+constexpr int kWorkerWavesPerBlock = 2;
+constexpr int kWorkerBlock = kWave * kWorkerWavesPerBlock;
 constexpr int kSubBlocks = 4;                       // float4 loads per lane per array
 constexpr int kTileElems = kWave * 4 * kSubBlocks;  // 1024 elements = 16 sign words
 constexpr int kTileWords = kTileElems / 64;

@@ -472,7 +472,7 @@ __device__ __forceinline__ void worker_tile(
 }
 
 template <bool PACKED, class G>
-__global__ __launch_bounds__(kBlock) void k_worker_pass(
+__global__ __launch_bounds__(kWorkerBlock) void k_worker_pass(
     const Tile *__restrict__ tiles, int64_t num_tiles, const float *__restrict__ m,
     const uint64_t *__restrict__ m_bits, const float *__restrict__ m_scales,
     const typename G::T *__restrict__ g, int64_t g_ld, float *__restrict__ err, int64_t err_ld,
@@ -481,8 +481,8 @@ __global__ __launch_bounds__(kBlock) void k_worker_pass(
     float beta1, float omb1)
 {
     const int lane = threadIdx.x & (kWave - 1);
-    const int64_t stride = (int64_t)gridDim.x * kWavesPerBlock;
-    for (int64_t item = (int64_t)blockIdx.x * kWavesPerBlock + (threadIdx.x >> 6);
+    const int64_t stride = (int64_t)gridDim.x * kWorkerWavesPerBlock;
+    for (int64_t item = (int64_t)blockIdx.x * kWorkerWavesPerBlock + (threadIdx.x >> 6);
          item < num_items; item += stride) {
         const int64_t grp = item / num_tiles;
         const int64_t t = item - grp * num_tiles;
@@ -1088,8 +1088,9 @@ static void launch_worker_t(const DeviceTables &tb, int64_t num_tiles, const flo
     const float omb1 = 1.0f - beta1;
     const int64_t groups = (n_local + group - 1) / group;
     const int64_t items = groups * num_tiles;
-    const int64_t blocks = std::min(blocks_for(items), kMaxGridBlocks);
-    hipLaunchKernelGGL((k_worker_pass<PACKED, G>), dim3((unsigned)blocks), dim3(kBlock), 0, s,
+    const int64_t blocks =
+        std::min((items + kWorkerWavesPerBlock - 1) / kWorkerWavesPerBlock, kMaxGridBlocks);
+    hipLaunchKernelGGL((k_worker_pass<PACKED, G>), dim3((unsigned)blocks), dim3(kWorkerBlock), 0, s,
                        tb.tiles, num_tiles, m, m_bits, m_scales, (const typename G::T *)g, g_ld,
                        err, err_ld, scales, scales_ld, bits, bits_ld, partial, n_local, group,
                        items, beta1, omb1);
