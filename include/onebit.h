@@ -87,7 +87,7 @@ typedef struct {
     int32_t n_workers;       /* n                                           */
     int32_t tile_elems;      /* elements per full tile                      */
     size_t workspace_bytes;  /* workspace needed by the calls below         */
-} onebit_plan_info;
+} onebit_plan_sizes;
 
 /* Creates a plan for K = num_tensors tensors (tensor_numel[k] >= 0, host
  * array) and n = n_workers >= 1 workers on the current HIP device.  The plan
@@ -102,12 +102,19 @@ int onebit_plan_create(const int64_t *tensor_numel, int32_t num_tensors,
 int onebit_plan_destroy(onebit_plan plan);
 
 /* Copies the plan's sizes into *info (host struct). */
-int onebit_plan_get_info(onebit_plan plan, onebit_plan_info *info);
+int onebit_plan_get_info(onebit_plan plan, onebit_plan_sizes *info);
 
 /* Host copies of the layout: tensor_offset[K], seg_begin[S], seg_end[S]
  * (element indices into the padded buffer).  Any output may be NULL. */
 int onebit_plan_get_layout(onebit_plan plan, int64_t *tensor_offset,
                            int64_t *seg_begin, int64_t *seg_end);
+
+/* The sizes a caller allocates by, as separate host outputs (any may be
+ * NULL): D, W, S, the chunk length c_k of every tensor (chunk_len[K], see
+ * Layout above) and the workspace size in bytes for the calls below. */
+int onebit_plan_info(onebit_plan plan, int64_t *padded_len, int64_t *words,
+                     int64_t *num_segments, int64_t *chunk_len,
+                     size_t *workspace_bytes);
 
 /* Warm-up step: original Adam on the data-parallel average gradient
  * (eq. (alg:v), Section 3.2; Algorithm 1's warm-up stage):

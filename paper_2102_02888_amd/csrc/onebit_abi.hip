@@ -25,7 +25,7 @@ struct onebit_plan_s {
     int32_t K = 0, n = 0;
     int64_t d = 0, D = 0, W = 0, S = 0, T = 0;
     int64_t max_seg_tiles = 0;                          // most tiles in one segment
-    std::vector<int64_t> tensor_off, seg_begin, seg_end;
+    std::vector<int64_t> tensor_off, chunk_len, seg_begin, seg_end;
     std::vector<int64_t> seg_tile_begin, seg_tile_end;  // [S]
     std::vector<int64_t> chunk_tile_begin;              // [n+1], into chunk_tiles
     std::vector<int64_t> chunk_word_lo, chunk_word_hi;  // [n], words touched by chunk j
@@ -142,6 +142,7 @@ int plan_create_impl(const int64_t *tensor_numel, int32_t num_tensors, int32_t n
     p->n = n;
     p->S = (int64_t)K * n;
     p->tensor_off.resize(K);
+    p->chunk_len.resize(K);
     p->seg_begin.resize(p->S);
     p->seg_end.resize(p->S);
     int64_t off = 0, d = 0;
@@ -149,6 +150,7 @@ int plan_create_impl(const int64_t *tensor_numel, int32_t num_tensors, int32_t n
         const int64_t dk = tensor_numel[k];
         const int64_t c = chunk_len(dk, n);
         p->tensor_off[k] = off;
+        p->chunk_len[k] = c;
         for (int32_t j = 0; j < n; ++j) {
             const int64_t b = std::min<int64_t>((int64_t)j * c, dk);
             const int64_t en = std::min<int64_t>((int64_t)(j + 1) * c, dk);
@@ -306,7 +308,7 @@ int onebit_plan_destroy(onebit_plan p)
     return ONEBIT_OK;
 }
 
-int onebit_plan_get_info(onebit_plan p, onebit_plan_info *info)
+int onebit_plan_get_info(onebit_plan p, onebit_plan_sizes *info)
 {
     if (!p) return fail(ONEBIT_EINVAL, "plan is NULL");
     if (!info) return fail(ONEBIT_EINVAL, "info is NULL");
@@ -329,6 +331,18 @@ int onebit_plan_get_layout(onebit_plan p, int64_t *tensor_offset, int64_t *seg_b
     if (tensor_offset) std::memcpy(tensor_offset, p->tensor_off.data(), p->K * sizeof(int64_t));
     if (seg_begin) std::memcpy(seg_begin, p->seg_begin.data(), p->S * sizeof(int64_t));
     if (seg_end) std::memcpy(seg_end, p->seg_end.data(), p->S * sizeof(int64_t));
+    return ONEBIT_OK;
+}
+
+int onebit_plan_info(onebit_plan p, int64_t *padded_len, int64_t *words, int64_t *num_segments,
+                     int64_t *chunk_len, size_t *workspace_bytes)
+{
+    if (!p) return fail(ONEBIT_EINVAL, "plan is NULL");
+    if (padded_len) *padded_len = p->D;
+    if (words) *words = p->W;
+    if (num_segments) *num_segments = p->S;
+    if (chunk_len) std::memcpy(chunk_len, p->chunk_len.data(), p->K * sizeof(int64_t));
+    if (workspace_bytes) *workspace_bytes = p->workspace_bytes;
     return ONEBIT_OK;
 }
 

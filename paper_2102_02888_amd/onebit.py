@@ -84,6 +84,9 @@ class Plan:
         call("onebit_plan_get_layout", h, self.tensor_off.ctypes.data_as(ctypes.c_void_p),
              self.seg_begin.ctypes.data_as(ctypes.c_void_p),
              self.seg_end.ctypes.data_as(ctypes.c_void_p))
+        self.chunk_len = np.zeros(self.K, np.int64)
+        call("onebit_plan_info", h, None, None, None,
+             self.chunk_len.ctypes.data_as(ctypes.c_void_p), None)
         self.numel = numel
 
     @property

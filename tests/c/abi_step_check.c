@@ -65,7 +65,7 @@ int main(void)
 
     onebit_plan plan;
     CHECK_OB(onebit_plan_create(numel, K, n, &plan));
-    onebit_plan_info info;
+    onebit_plan_sizes info;
     CHECK_OB(onebit_plan_get_info(plan, &info));
     if (info.padded_len != D || info.num_segments != S) { fprintf(stderr, "layout differs\n"); return 4; }
 

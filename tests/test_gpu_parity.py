@@ -33,6 +33,7 @@ def _put(a, dev):
 
 def _layouts_agree(plan, L):
     assert plan.D == L.D and plan.W == L.W and plan.S == L.S
+    assert [int(c) for c in plan.chunk_len] == [L.chunk_len(k) for k in range(len(L.numel))]
     np.testing.assert_array_equal(plan.tensor_off, L.tensor_off)
     np.testing.assert_array_equal(plan.seg_begin, L.seg_begin)
     np.testing.assert_array_equal(plan.seg_end, L.seg_end)
