@@ -255,6 +255,32 @@ class State:
         self.packed_momentum = packed_momentum
         self.compression_steps = 0
 
+    # Everything a later step reads: parameters, moments, both error states
+    # with the scales that complete them, and the last server message (the
+    # packed momentum).  Gradients and worker sign words are per-step outputs.
+    STATE_KEYS = ("x", "m", "v", "worker_err", "worker_scales", "server_err", "server_bits",
+                  "server_scales")
+
+    def state_dict(self):
+        """Host copies of the state (CPU tensors; safetensors can store them)."""
+        out = {k: getattr(self, k).detach().cpu().clone() for k in self.STATE_KEYS}
+        out["compression_steps"] = torch.tensor([self.compression_steps], dtype=torch.int64)
+        out["packed_momentum"] = torch.tensor([int(self.packed_momentum)], dtype=torch.int64)
+        return out
+
+    def load_state_dict(self, sd):
+        """Restores a state_dict() into this state's device buffers (same plan
+        shape); the next step continues bit for bit."""
+        for k in self.STATE_KEYS:
+            dst = getattr(self, k)
+            src = sd[k]
+            if tuple(src.shape) != tuple(dst.shape) or src.dtype != dst.dtype:
+                raise ValueError("%s: expected %s %s, got %s %s" % (
+                    k, tuple(dst.shape), dst.dtype, tuple(src.shape), src.dtype))
+            dst.copy_(src)
+        self.compression_steps = int(sd["compression_steps"][0])
+        self.packed_momentum = bool(int(sd["packed_momentum"][0]))
+
     def warmup(self, lr, beta1, beta2, eps, step, bias_correction=0, stream=None):
         onebit_warmup_adam_step(self.plan, self.x, self.m, self.v, self.grads, lr, beta1,
                                 beta2, eps, bias_correction, step, stream=stream)

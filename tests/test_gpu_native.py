@@ -175,3 +175,48 @@ def test_one_plan_two_streams(dev):
             assert host(getattr(states[a], name)).tobytes() == \
                 host(getattr(states[b], name)).tobytes(), (a, name)
     plan.close()
+
+
+@pytest.mark.parametrize("packed", [True, False])
+def test_checkpoint_resume_bit_exact(dev, tmp_path, packed):
+    """2 warm-up + 3 compression steps, state saved to a safetensors file and
+    loaded into a fresh plan and state, 3 more steps: identical to 6 straight
+    compression steps (the errors and the last server message are state)."""
+    from safetensors.torch import load_file, save_file
+    import paper_2102_02888_amd as ob
+    numel, n = [100_000, 3000, 64, 0, 777], 4
+    wl = synth.Workload(name="ckpt", numel=numel, n=n, warmup_steps=2, steps=6)
+
+    def run(st, t0, t1):
+        for t in range(t0, t1):
+            g = synth.host_grads(wl, st.plan.D, st.plan.tensor_off, t)
+            st.grads.copy_(torch.from_numpy(g))
+            if t <= wl.warmup_steps:
+                st.warmup(wl.lr, wl.beta1, wl.beta2, wl.eps, t)
+            else:
+                st.step(wl.lr, wl.beta1, wl.eps)
+
+    plan = ob.Plan(numel, n)
+    x0 = torch.from_numpy(synth.host_params(wl, plan.D))
+    straight = ob.State(plan, dev, packed_momentum=packed)
+    straight.x.copy_(x0)
+    run(straight, 1, 9)
+    first = ob.State(plan, dev, packed_momentum=packed)
+    first.x.copy_(x0)
+    run(first, 1, 6)
+    torch.cuda.synchronize()
+    path = str(tmp_path / "state.safetensors")
+    save_file(first.state_dict(), path)
+    plan2 = ob.Plan(numel, n)
+    resumed = ob.State(plan2, dev, packed_momentum=not packed)  # flag restored from the file
+    resumed.load_state_dict(load_file(path))
+    assert resumed.packed_momentum == packed and resumed.compression_steps == 3
+    run(resumed, 6, 9)
+    torch.cuda.synchronize()
+    for name in ("x", "worker_err", "worker_bits", "worker_scales", "server_err", "server_bits",
+                 "server_scales"):
+        assert host(getattr(resumed, name)).tobytes() == \
+            host(getattr(straight, name)).tobytes(), name
+    assert host(resumed.momentum()).tobytes() == host(straight.momentum()).tobytes()
+    plan.close()
+    plan2.close()

@@ -408,3 +408,132 @@ def test_identity_compressor_is_preconditioned_momentum_sgd():
         opt.step()
     assert_close_scaled(m[:4000], opt.state[y]["momentum_buffer"].numpy(), 1e-5)
     assert_close_scaled(x[:4000], y.detach().numpy() * p, 1e-6)
+
+
+# ---------------------------------------------------------------------------
+# Exact rational references (fractions.Fraction): the oracle's fp64 paths
+# give the correctly rounded fp32 value of the exact quantity
+# ---------------------------------------------------------------------------
+
+def _nearest_f32(q):
+    """The fp32 value nearest to the rational q (ties to even mantissa)."""
+    from fractions import Fraction
+    c = np.float32(float(q))
+    cands = [np.nextafter(c, np.float32(-np.inf)), c, np.nextafter(c, np.float32(np.inf))]
+    best = min(cands, key=lambda a: (abs(Fraction(float(a)) - q),
+                                     int(np.float32(a).view(np.uint32)) & 1))
+    return np.float32(best)
+
+
+def _sqrt_nearest_f32(q):
+    """The fp32 value nearest to sqrt(q) for a rational q >= 0, decided
+    exactly: sqrt(q) lies below the midpoint mid of two neighbours iff
+    q < mid^2."""
+    from fractions import Fraction
+    c = np.float32(math.sqrt(float(q)))
+    lo = np.nextafter(c, np.float32(-np.inf))
+    hi = np.nextafter(c, np.float32(np.inf))
+    pts = [lo, c, hi]
+    # walk to the pair of neighbours that brackets sqrt(q)
+    best = c
+    for a, b in zip(pts, pts[1:]):
+        if Fraction(float(a)) ** 2 <= q <= Fraction(float(b)) ** 2:
+            mid = (Fraction(float(a)) + Fraction(float(b))) / 2
+            if q < mid * mid:
+                best = a
+            elif q > mid * mid:
+                best = b
+            else:
+                best = a if (int(np.float32(a).view(np.uint32)) & 1) == 0 else b
+    return np.float32(best)
+
+
+@pytest.mark.parametrize("n", [1, 2, 3, 5, 8, 32])
+def test_server_average_is_correctly_rounded_exact_mean(n):
+    """With a zero server error, the compensated server value is the exact
+    mean of the n decoded messages (+-scale), rounded once to fp32."""
+    from fractions import Fraction
+    rng = np.random.default_rng(100 + n)
+    ln = 200
+    nw = (ln + 63) // 64
+    wbits = rng.integers(0, 2 ** 63, size=(n, nw), dtype=np.uint64) * np.uint64(2) + \
+        rng.integers(0, 2, size=(n, nw), dtype=np.uint64)
+    wscale = rng.lognormal(-7.0, 1.5, size=n).astype(np.float32)
+    dbar = np.zeros(ln, np.float32)
+    z = np.zeros(ln, np.float32)
+    sbits = np.zeros(nw, np.uint64)
+    oracle.server_segment(0, ln, n, wbits.reshape(-1), nw, wscale, 1, dbar, sbits, z)
+    for e in range(ln):
+        tot = Fraction(0)
+        for i in range(n):
+            bit = (int(wbits[i, e // 64]) >> (e % 64)) & 1
+            tot += Fraction(float(wscale[i])) * (1 if bit else -1)
+        assert z[e] == _nearest_f32(tot / n), (n, e)
+
+
+@pytest.mark.parametrize("length", [1, 3, 64, 100, 200])
+def test_scale_is_correctly_rounded_rms(length):
+    """scale = sqrt(sum z^2 / len) rounded once to fp32 (the fp64 path is
+    exact up to a final rounding for these sizes)."""
+    from fractions import Fraction
+    rng = np.random.default_rng(length)
+    for trial in range(20):
+        z = (rng.standard_normal(length) * 10.0 ** rng.uniform(-6, 2)).astype(np.float32)
+        _, s = oracle.compress(z)
+        q = sum(Fraction(float(v)) ** 2 for v in z) / length
+        assert s == _sqrt_nearest_f32(q), (length, trial)
+
+
+@pytest.mark.parametrize("length", [64, 128, 1024])
+def test_equal_magnitudes_compress_exactly(length):
+    """|z| constant (signs arbitrary, power-of-two length): the scale is |c|
+    exactly, C[z] = z and the new error is exactly zero."""
+    rng = np.random.default_rng(length)
+    c = np.float32(0.3721)
+    z = (c * rng.choice([-1.0, 1.0], size=length)).astype(np.float32)
+    m = np.zeros(length, np.float32)
+    delta = np.zeros(length, np.float32)
+    bits = np.zeros((length + 63) // 64, np.uint64)
+    zs = np.zeros(length, np.float32)
+    s = oracle.worker_segment(0, length, 0.0, m, z, delta, bits, zs)  # beta1 = 0: momentum = g
+    assert s == c
+    assert not delta.any()  # delta = z - C[z] = 0
+    signs = np.array([(int(bits[e // 64]) >> (e % 64)) & 1 for e in range(length)])
+    assert np.array_equal(signs == 1, z >= 0)
+
+
+def test_state_resumes_bit_exactly_from_a_copy():
+    """Checkpoint/resume: the state (x, m, v, every worker error, the server
+    error) is complete; 3 + 3 steps through a serialised copy equal 6
+    straight steps."""
+    import io
+    wl = synth.Workload(name="ckpt", numel=[3000, 64, 1000], n=3, warmup_steps=0, steps=6)
+    L = oracle.Layout(wl.numel, wl.n)
+    x = synth.host_params(wl, L.D)
+    x[~L.real_mask()] = 0
+    rng = np.random.default_rng(5)
+    m = (rng.standard_normal(L.D) * 1e-4).astype(np.float32)
+    v = (rng.random(L.D) * 1e-7).astype(np.float32)
+    grads = [synth.host_grads(wl, L.D, L.tensor_off, t) for t in range(1, 7)]
+    straight = oracle.State(L, x.copy(), m.copy(), v.copy())
+    for g in grads:
+        straight.step(g, LR, BETA1, EPS)
+    first = oracle.State(L, x.copy(), m.copy(), v.copy())
+    for g in grads[:3]:
+        first.step(g, LR, BETA1, EPS)
+    buf = io.BytesIO()
+    np.savez(buf, x=first.x, m=first.m, v=first.v, delta=first.delta, delta_bar=first.delta_bar)
+    buf.seek(0)
+    saved = np.load(buf)
+    resumed = oracle.State(L, saved["x"].copy(), saved["m"].copy(), saved["v"].copy())
+    resumed.delta[...] = saved["delta"]
+    resumed.delta_bar[...] = saved["delta_bar"]
+    for g in grads[3:]:
+        resumed.step(g, LR, BETA1, EPS)
+    for name in ("x", "m", "delta", "delta_bar", "wbits", "sbits", "wscales", "sscales"):
+        assert np.array_equal(getattr(resumed, name), getattr(straight, name)), name
+    # dropping the errors (a plausible incomplete checkpoint) changes the result
+    lossy = oracle.State(L, saved["x"].copy(), saved["m"].copy(), saved["v"].copy())
+    for g in grads[3:]:
+        lossy.step(g, LR, BETA1, EPS)
+    assert not np.array_equal(lossy.x, straight.x)
