@@ -1,7 +1,9 @@
 // gfx950 kernels of the 1-bit Adam hot path (arXiv 2102.02888).
 //
-// Every kernel is a bandwidth-bound stream over the flat parameter buffer; no
-// MFMA (nothing here is a dense contraction).  Work is cut into tiles of up
+// Every kernel streams over the flat parameter buffer and, except for the
+// chunk owners' decode-and-average (bound by vector ALU issue), is bound by
+// HBM bandwidth; no MFMA (nothing here is a dense contraction).  Work is cut
+// into tiles of up
 // to 1024 elements that never cross a segment; one wavefront (64 lanes) owns
 // one tile, each lane holding 4 sub-blocks x float4 = 16 elements, so every
 // global load/store is a 128-bit access and a wave moves 1 KiB per
