@@ -583,18 +583,29 @@ __global__ __launch_bounds__(kBlock) void k_finalize(
 // fp64 (the scales' exponents span at most 29 - ceil(log2 n) binades; true
 // for any realistic message set) the sum is exact, so it may be formed in any
 // grouping: then each group of 8 workers is one lookup in a 256-entry table
-// of its signed scale sums, indexed by the 8 workers' bits of the element (two
-// 4x4 bit transposes of their nibbles).  The 256-entry tables are sums of two
+// of its signed scale sums, indexed by the 8 workers' bits of the element (a
+// bit permutation of their nibbles).  The 256-entry tables are sums of two
 // 16-entry tables, each built from 4 scales.  Otherwise every worker is added
 // one by one.  Both give the oracle's sum.
 // ---------------------------------------------------------------------------
-__device__ __forceinline__ uint32_t transpose4x4(uint32_t x)
+// Delta swap: exchanges the bits of x selected by m with the bits d places
+// above them.
+__device__ __forceinline__ uint32_t delta_swap(uint32_t x, int d, uint32_t m)
 {
-    // x bit 4k+c (worker k, element c) -> bit 4c+k
-    uint32_t t = (x ^ (x >> 3)) & 0x0A0Au;
-    x ^= t ^ (t << 3);
-    t = (x ^ (x >> 6)) & 0x00CCu;
-    x ^= t ^ (t << 6);
+    const uint32_t t = ((x >> d) ^ x) & m;
+    return x ^ t ^ (t << d);
+}
+
+// x holds 8 nibbles, nibble k = worker k's sign bits of 4 elements (bit c =
+// element c), i.e. bit 4k+c.  Returns byte c = the 8 workers' bits of element
+// c, i.e. bit 8c+k: the bit index (k2 k1 k0 c1 c0) rotated to (c1 c0 k2 k1 k0),
+// done as four swaps of index bits (4<->1, 3<->0, 2<->1, 1<->0).
+__device__ __forceinline__ uint32_t nibbles_to_bytes(uint32_t x)
+{
+    x = delta_swap(x, 14, 0x0000CCCCu);
+    x = delta_swap(x, 7, 0x00AA00AAu);
+    x = delta_swap(x, 2, 0x0C0C0C0Cu);
+    x = delta_swap(x, 1, 0x22222222u);
     return x;
 }
 
@@ -797,12 +808,11 @@ __global__ __launch_bounds__(kBlock) void k_server_pass(
 #pragma unroll
                         for (int bb = 0; bb < 2; ++bb) {
                             const int hw = 2 * (4 * (bh + bb) + (lane >> 4)) + half;
-                            // nibble k: worker r8 + k's bits of the lane's 4 elements
-                            const uint32_t x = s_bits[wv][hw][r8 + (lane & 7)];
-                            const uint32_t yl = transpose4x4(x & 0xFFFFu), yh = transpose4x4(x >> 16);
+                            // nibble k: worker r8 + k's bits of the lane's 4 elements;
+                            // byte c of y: element c's 8 worker bits (the table index)
+                            const uint32_t y = nibbles_to_bytes(s_bits[wv][hw][r8 + (lane & 7)]);
 #pragma unroll
-                            for (int c = 0; c < 4; ++c)
-                                idx[bb][c] = ((yl >> (4 * c)) & 0xFu) | (((yh >> (4 * c)) & 0xFu) << 4);
+                            for (int c = 0; c < 4; ++c) idx[bb][c] = (y >> (8 * c)) & 0xFFu;
                         }
                         double val[2][4];
 #pragma unroll
