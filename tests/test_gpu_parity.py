@@ -246,7 +246,7 @@ def _lowp(g, dtype):
 
 
 def _free_run(ob, dev, wl, numel=None, warm=None, steps=None, packed=True,
-              grad_dtype=torch.float32):
+              grad_dtype=torch.float32, perturb=None, final_check=None):
     numel = wl.numel if numel is None else numel
     n = wl.n
     warm = wl.warmup_steps if warm is None else warm
@@ -275,6 +275,8 @@ def _free_run(ob, dev, wl, numel=None, warm=None, steps=None, packed=True,
     scale_ulps = 0
     for t in range(warm + 1, warm + steps + 1):
         g = synth.host_grads(wl, L.D, L.tensor_off, t)
+        if perturb is not None:
+            perturb(t - warm, g, L)
         gt, g = _lowp(g, grad_dtype)
         ref.step(g, wl.lr, wl.beta1, wl.eps)
         st.grads.copy_(gt.to(dev))
@@ -293,6 +295,8 @@ def _free_run(ob, dev, wl, numel=None, warm=None, steps=None, packed=True,
                                   mask=mask)
     print("%s: scales differing by 1 ulp: %d; bit-identical fractions %s"
           % (wl.name, scale_ulps, ex))
+    if final_check is not None:
+        final_check(st, ref, L)
     plan.close()
     return ex
 
@@ -338,6 +342,30 @@ def test_free_running_more_scale_pairs_than_grid(ob, dev):
     wl = synth.Workload(name="pairs", numel=[64] * 4200 + [100, 3], n=64, warmup_steps=2,
                         steps=3)
     _free_run(ob, dev, wl)
+
+
+def test_free_running_nonfinite_gradients(ob, dev):
+    """A NaN and an infinity in two workers' gradients at the second
+    compression step: the affected segments turn non-finite the same way on
+    both sides (NaN scales take the one-by-one server path), the others stay
+    finite and equal."""
+    wl = synth.Workload(name="nonfinite", numel=[5000, 3000, 700], n=4, warmup_steps=2,
+                        steps=4)
+
+    def perturb(step, g, L):
+        if step == 2:
+            g[1, L.tensor_off[0] + 17] = np.nan
+            g[2, L.tensor_off[1] + 900] = np.inf
+
+    def final_check(st, ref, L):
+        # the two hit segments went non-finite, the third tensor did not
+        # element 900 of tensor 1 is in its chunk 1 (chunks of 768): segment n + 1
+        assert np.isnan(ref.sscales[0]) and not np.isfinite(ref.sscales[wl.n + 1])
+        assert np.isfinite(ref.sscales[2 * wl.n:]).all()
+        assert np.isnan(host(st.x)[L.tensor_off[0]:L.tensor_off[0] + 64]).all()
+        assert np.isfinite(host(st.x)[L.tensor_off[2]:L.tensor_off[2] + 700]).all()
+
+    _free_run(ob, dev, wl, perturb=perturb, final_check=final_check)
 
 
 def test_free_running_single_worker(ob, dev):
