@@ -10,4 +10,5 @@ from .onebit import (  # noqa: F401
     onebit_worker_compress, onebit_uncompressed_step, onebit_adam_message_step, onebit_l1_norm,
 )
 from .freeze import VarianceFreezeDetector  # noqa: F401
+from .optimizer import OnebitAdam  # noqa: F401
 from ._native import OnebitError, lib  # noqa: F401

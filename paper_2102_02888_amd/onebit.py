@@ -321,6 +321,8 @@ class State:
         if not hasattr(self, "_norm"):
             self._norm = torch.zeros(1, dtype=torch.float64, device=self.v.device)
         onebit_l1_norm(self.plan, self.v, self.workspace, self._norm, stream=stream)
+        if stream is not None:
+            stream.synchronize()
         return float(self._norm.item())
 
     def momentum(self):
