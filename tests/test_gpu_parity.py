@@ -456,3 +456,32 @@ def test_server_received_chunk_form(ob, dev):
     assert not sb[:w0].any() and not sb[w1:].any()
     assert np.count_nonzero(res[0][2]) == 1
     plan.close()
+
+
+def test_hand_worked_example_on_gpu(ob, dev):
+    """The two hand-worked compression steps of tests/golden/ through the
+    ABI (first step with the fp32 momentum, second with it packed)."""
+    import json
+    import os
+    gd = json.load(open(os.path.join(os.path.dirname(__file__), "golden",
+                                     "hand_worked_two_steps.json")))
+    su = gd["setup"]
+    plan = ob.Plan(su["tensor_numel"], su["n_workers"])
+    st = ob.State(plan, dev)
+    st.x[:2] = torch.tensor(su["x"])
+    st.m[:2] = torch.tensor(su["m"])
+    st.v[:2] = torch.tensor(su["v_frozen"])
+    for sd in gd["steps"]:
+        st.grads.zero_()
+        st.grads[:, :2] = torch.tensor(sd["grads"])
+        st.step(su["lr"], su["beta1"], su["eps"])
+        torch.cuda.synchronize()
+        assert host(st.worker_scales)[:, 0].tolist() == sd["worker_scales_chunk0"]
+        assert [int(w) for w in host(st.worker_bits)[:, 0]] == sd["worker_bits_word0"]
+        assert host(st.worker_delta())[:, :2].tolist() == sd["worker_delta"]
+        assert float(host(st.server_scales)[0]) == sd["server_scale_chunk0"]
+        assert int(host(st.server_bits)[0]) == sd["server_bits_word0"]
+        assert host(st.server_delta())[:2].tolist() == sd["server_delta"]
+        assert host(st.x)[:2].tolist() == sd["x"]
+        assert host(st.momentum())[:2].tolist() == sd["m"]
+    plan.close()

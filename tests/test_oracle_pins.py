@@ -129,47 +129,40 @@ def test_empty_segment_scale_zero():
 
 
 # ---------------------------------------------------------------------------
-# Hand-worked two-step example (Algorithm 1, exact dyadic arithmetic)
-# d = 2, n = 2, beta1 = 1/2, lr = 1/2, eps = 0, v = [4, 16], x0 = [1, 1], m0 = 0
-#  step 1: g0 = [28, -4], g1 = [48, 48]
-#    worker 0: z = [14, -2], s = sqrt(200/2) = 10, bits [1,0], m_hat [10,-10], delta0 = [4, 8]
-#    worker 1: z = [24, 24], s = 24, bits [1,1], m_hat [24, 24], delta1 = [0, 0]
-#    server : avg = [17, 7], z_bar = [17, 7], s_bar = sqrt(338/2) = 13, bits [1,1],
-#             m_bar = [13, 13], delta_bar = [4, -6]
-#    update : x = [1 - 0.5*13/2, 1 - 0.5*13/4] = [-2.25, -0.625], m = [13, 13]
-#  step 2: g0 = [-23, -15], g1 = [-27, -11]
-#    worker 0: z = 6.5 + g/2 + [4, 8] = [-1, 7], s = 5, bits [0,1], m_hat [-5, 5], delta0 = [4, 2]
-#    worker 1: z = 6.5 + g/2 + [0, 0] = [-7, 1], s = 5, bits [0,1], m_hat [-5, 5], delta1 = [-2, -4]
-#    server : avg = [-5, 5], z_bar = [-1, -1], s_bar = 1, bits [0,0], m_bar = [-1,-1], delta_bar = 0
-#    update : x = [-2.25 + 0.25, -0.625 + 0.125] = [-2, -0.5], m = [-1, -1]
+# Hand-worked two-step example (Algorithm 1, exact dyadic arithmetic; the
+# inputs, results and derivation are in tests/golden/hand_worked_two_steps.json)
 # ---------------------------------------------------------------------------
 
+def _golden(name):
+    import json
+    import os
+    return json.load(open(os.path.join(os.path.dirname(__file__), "golden", name)))
+
+
 def test_hand_worked_two_steps():
-    L = oracle.Layout([2], 2)
+    """tests/golden/hand_worked_two_steps.json: two compression steps of
+    Algorithm 1 worked by hand in exact dyadic arithmetic."""
+    gd = _golden("hand_worked_two_steps.json")
+    su = gd["setup"]
+    L = oracle.Layout(su["tensor_numel"], su["n_workers"])
     assert L.D == 64 and L.segments() == [(0, 2), (2, 2)]
-    x = np.zeros(64, np.float32); x[:2] = 1.0
-    v = np.zeros(64, np.float32); v[:2] = [4.0, 16.0]
-    st = oracle.State(L, x, np.zeros(64, np.float32), v)
+    x = np.zeros(64, np.float32); x[:2] = su["x"]
+    m = np.zeros(64, np.float32); m[:2] = su["m"]
+    v = np.zeros(64, np.float32); v[:2] = su["v_frozen"]
+    st = oracle.State(L, x, m, v)
     g = np.zeros((2, 64), np.float32)
-    g[0, :2] = [28, -4]; g[1, :2] = [48, 48]
-    st.step(g, lr=0.5, beta1=0.5, eps=0.0)
-    np.testing.assert_array_equal(st.wscales[:, 0], [10, 24])
-    np.testing.assert_array_equal(st.wscales[:, 1], [0, 0])
-    assert [int(w) for w in st.wbits[:, 0]] == [0b01, 0b11]
-    np.testing.assert_array_equal(st.delta[:, :2], [[4, 8], [0, 0]])
-    assert st.sscales[0] == 13 and st.sscales[1] == 0 and int(st.sbits[0]) == 0b11
-    np.testing.assert_array_equal(st.delta_bar[:2], [4, -6])
-    np.testing.assert_array_equal(st.x[:2], [-2.25, -0.625])
-    np.testing.assert_array_equal(st.m[:2], [13, 13])
-    g[0, :2] = [-23, -15]; g[1, :2] = [-27, -11]
-    st.step(g, lr=0.5, beta1=0.5, eps=0.0)
-    np.testing.assert_array_equal(st.wscales[:, 0], [5, 5])
-    assert [int(w) for w in st.wbits[:, 0]] == [0b10, 0b10]
-    np.testing.assert_array_equal(st.delta[:, :2], [[4, 2], [-2, -4]])
-    assert st.sscales[0] == 1 and int(st.sbits[0]) == 0
-    np.testing.assert_array_equal(st.delta_bar[:2], [0, 0])
-    np.testing.assert_array_equal(st.x[:2], [-2.0, -0.5])
-    np.testing.assert_array_equal(st.m[:2], [-1, -1])
+    for sd in gd["steps"]:
+        g[:, :2] = sd["grads"]
+        st.step(g, lr=su["lr"], beta1=su["beta1"], eps=su["eps"])
+        np.testing.assert_array_equal(st.wscales[:, 0], sd["worker_scales_chunk0"])
+        np.testing.assert_array_equal(st.wscales[:, 1], [0, 0])
+        assert [int(w) for w in st.wbits[:, 0]] == sd["worker_bits_word0"]
+        np.testing.assert_array_equal(st.delta[:, :2], sd["worker_delta"])
+        assert st.sscales[0] == sd["server_scale_chunk0"] and st.sscales[1] == 0
+        assert int(st.sbits[0]) == sd["server_bits_word0"]
+        np.testing.assert_array_equal(st.delta_bar[:2], sd["server_delta"])
+        np.testing.assert_array_equal(st.x[:2], sd["x"])
+        np.testing.assert_array_equal(st.m[:2], sd["m"])
     # padding untouched
     assert not st.x[2:].any() and not st.delta[:, 2:].any()
 
@@ -537,3 +530,18 @@ def test_state_resumes_bit_exactly_from_a_copy():
     for g in grads[3:]:
         lossy.step(g, LR, BETA1, EPS)
     assert not np.array_equal(lossy.x, straight.x)
+
+
+def test_oracle_matches_its_recorded_reference_run():
+    """Regression guard: the oracle reproduces the state digests that
+    tests/golden/make_oracle_reference.py recorded (re-run that script only
+    with a change to the oracle's arithmetic that the paper justifies)."""
+    import importlib.util
+    import os
+    path = os.path.join(os.path.dirname(__file__), "golden", "make_oracle_reference.py")
+    spec = importlib.util.spec_from_file_location("make_oracle_reference", path)
+    mod = importlib.util.module_from_spec(spec)
+    spec.loader.exec_module(mod)
+    gd = _golden("oracle_reference_run.json")
+    assert gd["workload"] == mod.WORKLOAD
+    assert mod.digests(mod.run()) == gd["sha256"]
