@@ -26,7 +26,11 @@ def _stream(stream):
     return ctypes.c_void_p(s.cuda_stream)
 
 
-def _ptr(t, dtype, name):
+def _ptr(t, dtype, name, cols=None, rows=1):
+    """Device pointer of a tensor after checking its type, device and layout.
+    With `cols`, the tensor must also cover what the kernels touch: `rows`
+    rows of `cols` elements (a 1-D tensor is one row), so that a short
+    buffer is refused here instead of being read or written out of bounds."""
     if t is None:
         return None
     if not isinstance(t, torch.Tensor):
@@ -35,19 +39,35 @@ def _ptr(t, dtype, name):
         raise TypeError("%s must be %s, got %s" % (name, dtype, t.dtype))
     if t.device.type != "cuda":
         raise ValueError("%s must be a GPU tensor" % name)
+    if t.dim() > 2:
+        raise ValueError("%s must be 1-D or 2-D" % name)
     if t.dim() >= 1 and t.stride(-1) != 1:
         raise ValueError("%s must have unit stride in its last dimension" % name)
+    if cols is not None:
+        have_rows, have_cols = (t.shape[0], t.shape[1]) if t.dim() == 2 else (1, t.numel())
+        if have_rows < rows or have_cols < cols:
+            raise ValueError("%s is %s; the call needs %d row(s) of at least %d elements"
+                             % (name, tuple(t.shape), rows, cols))
     return ctypes.c_void_p(t.data_ptr())
+
+
+def _flat(t, dtype, name, need):
+    """Pointer of a buffer addressed through an explicit leading dimension:
+    it must hold at least `need` elements."""
+    p = _ptr(t, dtype, name)
+    if t.numel() < need:
+        raise ValueError("%s has %d elements; the call reads %d" % (name, t.numel(), need))
+    return p
 
 
 _GRAD_DTYPES = {torch.float32: 0, torch.bfloat16: 1, torch.float16: 2}
 
 
-def _grads(t):
+def _grads(t, cols, rows):
     """(pointer, ONEBIT_GRAD_* code) of a gradient tensor."""
     if not isinstance(t, torch.Tensor) or t.dtype not in _GRAD_DTYPES:
         raise TypeError("grads must be a float32, bfloat16 or float16 tensor")
-    return _ptr(t, t.dtype, "grads"), _GRAD_DTYPES[t.dtype]
+    return _ptr(t, t.dtype, "grads", cols, rows), _GRAD_DTYPES[t.dtype]
 
 
 def _ld(t):
@@ -90,6 +110,23 @@ class Plan:
         self.numel = numel
 
     @property
+    def workspace_words(self):
+        return (self.workspace_bytes + 7) // 8
+
+    def chunk_extent(self, server_begin, server_end):
+        """(lowest word, highest word, highest segment) touched by the chunk
+        owners [server_begin, server_end); words are -1 if all are empty."""
+        wlo, whi = -1, -1
+        for k in range(self.K):
+            for j in range(server_begin, server_end):
+                q = k * self.n + j
+                b, e = int(self.seg_begin[q]), int(self.seg_end[q])
+                if e > b:
+                    wlo = b // 64 if wlo < 0 else min(wlo, b // 64)
+                    whi = max(whi, (e - 1) // 64)
+        return wlo, whi, (self.K - 1) * self.n + server_end - 1
+
+    @property
     def handle(self):
         if self._h is None:
             raise ValueError("plan is closed")
@@ -120,9 +157,10 @@ def onebit_warmup_adam_step(plan, x, m, v, grads, lr, beta1, beta2, eps,
     n = _rows(grads) if n_grads is None else n_grads
     if _rows(grads) < n:
         raise ValueError("grads has fewer than %d rows" % n)
-    call("onebit_warmup_adam_step", plan.handle, _ptr(x, torch.float32, "x"),
-         _ptr(m, torch.float32, "m"), _ptr(v, torch.float32, "v"),
-         *_grads(grads), _ld(grads), n, lr, beta1, beta2, eps,
+    D = plan.D
+    call("onebit_warmup_adam_step", plan.handle, _ptr(x, torch.float32, "x", D),
+         _ptr(m, torch.float32, "m", D), _ptr(v, torch.float32, "v", D),
+         *_grads(grads, D, n), _ld(grads), n, lr, beta1, beta2, eps,
          int(bias_correction), int(step), _stream(stream))
 
 
@@ -133,61 +171,80 @@ def onebit_worker_compress(plan, m, grads, worker_err, worker_bits, worker_scale
     n = _rows(grads) if n_local is None else n_local
     if min(_rows(grads), _rows(worker_err), _rows(worker_bits), _rows(worker_scales)) < n:
         raise ValueError("grads, worker_err, worker_bits, worker_scales need %d rows" % n)
-    call("onebit_worker_compress", plan.handle, _ptr(m, torch.float32, "m"),
-         _ptr(m_bits, torch.int64, "m_bits"), _ptr(m_scales, torch.float32, "m_scales"),
-         *_grads(grads), _ld(grads), n,
-         _ptr(worker_err, torch.float32, "worker_err"), _ld(worker_err),
-         _ptr(worker_bits, torch.int64, "worker_bits"), _ld(worker_bits),
-         _ptr(worker_scales, torch.float32, "worker_scales"), _ld(worker_scales),
-         beta1, _ptr(workspace, torch.float64, "workspace"), _stream(stream))
+    D, W, S = plan.D, plan.W, plan.S
+    call("onebit_worker_compress", plan.handle, _ptr(m, torch.float32, "m", D),
+         _ptr(m_bits, torch.int64, "m_bits", W), _ptr(m_scales, torch.float32, "m_scales", S),
+         *_grads(grads, D, n), _ld(grads), n,
+         _ptr(worker_err, torch.float32, "worker_err", D, n), _ld(worker_err),
+         _ptr(worker_bits, torch.int64, "worker_bits", W, n), _ld(worker_bits),
+         _ptr(worker_scales, torch.float32, "worker_scales", S, n), _ld(worker_scales),
+         beta1, _ptr(workspace, torch.float64, "workspace", plan.workspace_words),
+         _stream(stream))
 
 
 def onebit_server_reduce_compress(plan, server_begin, server_end, worker_bits, worker_scales,
                                   server_err, server_bits, server_scales, workspace,
                                   bits_word_base=0, scales_seg_base=0, bits_ld=None,
                                   scales_ld=None, stream=None):
-    if _rows(worker_bits) < plan.n or (scales_ld is None and _rows(worker_scales) < plan.n):
-        raise ValueError("incoming bits and scales need one row per worker (%d)" % plan.n)
-    if scales_ld is not None and worker_scales.numel() < (plan.n - 1) * scales_ld + 1:
-        raise ValueError("worker_scales too small for %d rows of stride %d" % (plan.n, scales_ld))
+    """Chunk owners [server_begin, server_end).  worker_bits / worker_scales
+    are n rows, either the plan-wide arrays (row stride from the tensor) or
+    received buffers whose first column is word `bits_word_base` / segment
+    `scales_seg_base`, with an explicit row stride bits_ld / scales_ld."""
+    n = plan.n
+    wlo, whi, qhi = plan.chunk_extent(int(server_begin), int(server_end))
+    wcols = whi + 1 - int(bits_word_base) if whi >= 0 else 0
+    scols = qhi + 1 - int(scales_seg_base)
+    if bits_ld is None:
+        bp, bld = _ptr(worker_bits, torch.int64, "worker_bits", wcols, n), _ld(worker_bits)
+    else:
+        bp, bld = _flat(worker_bits, torch.int64, "worker_bits", (n - 1) * bits_ld + wcols), bits_ld
+    if scales_ld is None:
+        sp, sld = _ptr(worker_scales, torch.float32, "worker_scales", scols, n), _ld(worker_scales)
+    else:
+        sp, sld = (_flat(worker_scales, torch.float32, "worker_scales",
+                         (n - 1) * scales_ld + scols), scales_ld)
     call("onebit_server_reduce_compress", plan.handle, int(server_begin), int(server_end),
-         _ptr(worker_bits, torch.int64, "worker_bits"),
-         _ld(worker_bits) if bits_ld is None else bits_ld, int(bits_word_base),
-         _ptr(worker_scales, torch.float32, "worker_scales"),
-         _ld(worker_scales) if scales_ld is None else scales_ld, int(scales_seg_base),
-         _ptr(server_err, torch.float32, "server_err"),
-         _ptr(server_bits, torch.int64, "server_bits"),
-         _ptr(server_scales, torch.float32, "server_scales"),
-         _ptr(workspace, torch.float64, "workspace"), _stream(stream))
+         bp, bld, int(bits_word_base), sp, sld, int(scales_seg_base),
+         _ptr(server_err, torch.float32, "server_err", plan.D),
+         _ptr(server_bits, torch.int64, "server_bits", plan.W),
+         _ptr(server_scales, torch.float32, "server_scales", plan.S),
+         _ptr(workspace, torch.float64, "workspace", plan.workspace_words), _stream(stream))
 
 
 def onebit_decompress_update(plan, server_bits, server_scales, x, m_out, v_frozen, lr, eps,
                              stream=None):
-    call("onebit_decompress_update", plan.handle, _ptr(server_bits, torch.int64, "server_bits"),
-         _ptr(server_scales, torch.float32, "server_scales"), _ptr(x, torch.float32, "x"),
-         _ptr(m_out, torch.float32, "m_out"), _ptr(v_frozen, torch.float32, "v_frozen"),
-         lr, eps, _stream(stream))
+    D = plan.D
+    call("onebit_decompress_update", plan.handle,
+         _ptr(server_bits, torch.int64, "server_bits", plan.W),
+         _ptr(server_scales, torch.float32, "server_scales", plan.S),
+         _ptr(x, torch.float32, "x", D), _ptr(m_out, torch.float32, "m_out", D),
+         _ptr(v_frozen, torch.float32, "v_frozen", D), lr, eps, _stream(stream))
 
 
 def onebit_step(plan, x, m, v_frozen, grads, worker_err, server_err, worker_bits,
                 worker_scales, server_bits, server_scales, lr, beta1, eps, workspace,
                 stream=None):
-    if min(_rows(grads), _rows(worker_err), _rows(worker_bits), _rows(worker_scales)) < plan.n:
-        raise ValueError("grads, worker_err, worker_bits, worker_scales need %d rows" % plan.n)
-    call("onebit_step", plan.handle, _ptr(x, torch.float32, "x"), _ptr(m, torch.float32, "m"),
-         _ptr(v_frozen, torch.float32, "v_frozen"), *_grads(grads),
-         _ld(grads), _ptr(worker_err, torch.float32, "worker_err"), _ld(worker_err),
-         _ptr(server_err, torch.float32, "server_err"),
-         _ptr(worker_bits, torch.int64, "worker_bits"),
-         _ptr(worker_scales, torch.float32, "worker_scales"),
-         _ptr(server_bits, torch.int64, "server_bits"),
-         _ptr(server_scales, torch.float32, "server_scales"), lr, beta1, eps,
-         _ptr(workspace, torch.float64, "workspace"), _stream(stream))
+    n, D, W, S = plan.n, plan.D, plan.W, plan.S
+    # the step addresses worker_bits / worker_scales with row strides W and S
+    for t, name, cols in ((worker_bits, "worker_bits", W), (worker_scales, "worker_scales", S)):
+        if t is not None and t.dim() == 2 and t.stride(0) != cols:
+            raise ValueError("%s must be contiguous [n, %d] for onebit_step" % (name, cols))
+    call("onebit_step", plan.handle, _ptr(x, torch.float32, "x", D),
+         _ptr(m, torch.float32, "m", D), _ptr(v_frozen, torch.float32, "v_frozen", D),
+         *_grads(grads, D, n), _ld(grads),
+         _ptr(worker_err, torch.float32, "worker_err", D, n), _ld(worker_err),
+         _ptr(server_err, torch.float32, "server_err", D),
+         _ptr(worker_bits, torch.int64, "worker_bits", W, n),
+         _ptr(worker_scales, torch.float32, "worker_scales", S, n),
+         _ptr(server_bits, torch.int64, "server_bits", W),
+         _ptr(server_scales, torch.float32, "server_scales", S), lr, beta1, eps,
+         _ptr(workspace, torch.float64, "workspace", plan.workspace_words), _stream(stream))
 
 
 def onebit_decode(plan, bits, scales, out, stream=None):
-    call("onebit_decode", plan.handle, _ptr(bits, torch.int64, "bits"),
-         _ptr(scales, torch.float32, "scales"), _ptr(out, torch.float32, "out"), _stream(stream))
+    call("onebit_decode", plan.handle, _ptr(bits, torch.int64, "bits", plan.W),
+         _ptr(scales, torch.float32, "scales", plan.S), _ptr(out, torch.float32, "out", plan.D),
+         _stream(stream))
 
 
 def onebit_uncompressed_step(plan, x, m, v_frozen, grads, lr, beta1, eps, n_grads=None,
@@ -195,33 +252,35 @@ def onebit_uncompressed_step(plan, x, m, v_frozen, grads, lr, beta1, eps, n_grad
     n = _rows(grads) if n_grads is None else n_grads
     if _rows(grads) < n:
         raise ValueError("grads has fewer than %d rows" % n)
-    call("onebit_uncompressed_step", plan.handle, _ptr(x, torch.float32, "x"),
-         _ptr(m, torch.float32, "m"), _ptr(v_frozen, torch.float32, "v_frozen"), *_grads(grads),
-         _ld(grads), n, lr, beta1, eps, _stream(stream))
+    D = plan.D
+    call("onebit_uncompressed_step", plan.handle, _ptr(x, torch.float32, "x", D),
+         _ptr(m, torch.float32, "m", D), _ptr(v_frozen, torch.float32, "v_frozen", D),
+         *_grads(grads, D, n), _ld(grads), n, lr, beta1, eps, _stream(stream))
 
 
 def onebit_adam_message_step(plan, x, m, v, bits, scales, lr, beta1, beta2, eps, bias_correction,
                              step, stream=None):
-    call("onebit_adam_message_step", plan.handle, _ptr(x, torch.float32, "x"),
-         _ptr(m, torch.float32, "m"), _ptr(v, torch.float32, "v"),
-         _ptr(bits, torch.int64, "bits"), _ptr(scales, torch.float32, "scales"), lr, beta1, beta2,
-         eps, int(bias_correction), int(step), _stream(stream))
+    D = plan.D
+    call("onebit_adam_message_step", plan.handle, _ptr(x, torch.float32, "x", D),
+         _ptr(m, torch.float32, "m", D), _ptr(v, torch.float32, "v", D),
+         _ptr(bits, torch.int64, "bits", plan.W), _ptr(scales, torch.float32, "scales", plan.S),
+         lr, beta1, beta2, eps, int(bias_correction), int(step), _stream(stream))
 
 
 def onebit_l1_norm(plan, v, workspace, out, stream=None):
     """||v||_1 over the real elements into out (a one-element float64 GPU tensor)."""
-    call("onebit_l1_norm", plan.handle, _ptr(v, torch.float32, "v"),
-         _ptr(workspace, torch.float64, "workspace"), _ptr(out, torch.float64, "out"),
-         _stream(stream))
+    call("onebit_l1_norm", plan.handle, _ptr(v, torch.float32, "v", plan.D),
+         _ptr(workspace, torch.float64, "workspace", plan.workspace_words),
+         _ptr(out, torch.float64, "out", 1), _stream(stream))
 
 
 def onebit_error_materialize(plan, err_state, scales, delta_out, rows=None, stream=None):
     r = _rows(err_state) if rows is None else rows
-    if _rows(scales) < r or _rows(delta_out) < r or _rows(err_state) < r:
-        raise ValueError("err_state, scales and delta_out need %d rows" % r)
-    call("onebit_error_materialize", plan.handle, _ptr(err_state, torch.float32, "err_state"),
-         _ld(err_state), _ptr(scales, torch.float32, "scales"), _ld(scales), r,
-         _ptr(delta_out, torch.float32, "delta_out"), _ld(delta_out), _stream(stream))
+    D = plan.D
+    call("onebit_error_materialize", plan.handle,
+         _ptr(err_state, torch.float32, "err_state", D, r), _ld(err_state),
+         _ptr(scales, torch.float32, "scales", plan.S, r), _ld(scales), r,
+         _ptr(delta_out, torch.float32, "delta_out", D, r), _ld(delta_out), _stream(stream))
 
 
 class State:

@@ -220,3 +220,31 @@ def test_checkpoint_resume_bit_exact(dev, tmp_path, packed):
     assert host(resumed.momentum()).tobytes() == host(straight.momentum()).tobytes()
     plan.close()
     plan2.close()
+
+
+def test_binding_refuses_short_buffers(dev):
+    """The Python binding checks every buffer against the plan's sizes, so a
+    short tensor raises instead of reaching a kernel."""
+    import paper_2102_02888_amd as ob
+    plan = ob.Plan([5000, 64], 4)
+    st = ob.State(plan, dev)
+    short = torch.zeros(plan.D - 64, device=dev)
+    with pytest.raises(ValueError, match="x"):
+        ob.onebit_decompress_update(plan, st.server_bits, st.server_scales, short, None, st.v,
+                                    1e-3, 1e-8)
+    with pytest.raises(ValueError, match="grads"):
+        ob.onebit_worker_compress(plan, st.m, st.grads[:, :plan.D - 64], st.worker_err,
+                                  st.worker_bits, st.worker_scales, 0.9, st.workspace)
+    with pytest.raises(ValueError, match="worker_bits"):
+        ob.onebit_server_reduce_compress(plan, 0, 4, st.worker_bits[:3], st.worker_scales,
+                                         st.server_err, st.server_bits, st.server_scales,
+                                         st.workspace)
+    with pytest.raises(ValueError, match="workspace"):
+        ob.onebit_l1_norm(plan, st.v, st.workspace[:4], torch.zeros(1, dtype=torch.float64,
+                                                                     device=dev))
+    with pytest.raises(ValueError, match="worker_scales"):
+        ob.onebit_server_reduce_compress(plan, 0, 4, st.worker_bits, st.worker_scales.reshape(-1),
+                                         st.server_err, st.server_bits, st.server_scales,
+                                         st.workspace, scales_ld=plan.S + 1)
+    torch.cuda.synchronize()
+    plan.close()
