@@ -454,12 +454,15 @@ def main():
                      "algorithmic_bytes_per_launch": worker_bytes},
         "kernels": {name: {"ms": ms, "algorithmic_bytes": nbytes,
                            "gbps": nbytes / (ms * 1e-3) / 1e9,
-                           "frac": nbytes / (ms * 1e-3) / 1e9 / HBM_PEAK_GBPS}
-                    for name, ms, nbytes in (
-                        ("worker_compress", part_ms[0], worker_bytes),
-                        ("server_reduce_compress", part_ms[1], d * bs),
-                        ("decompress_update", part_ms[2], d * bu),
-                        ("warmup_adam_step", warm_avg, d * (n * gbytes + 24)))
+                           "frac": nbytes / (ms * 1e-3) / 1e9 / HBM_PEAK_GBPS,
+                           "traffic": measured_traffic(wl.name, kname)}
+                    for name, ms, nbytes, kname in (
+                        ("worker_compress", part_ms[0], worker_bytes,
+                         "k_worker_pass<true, %s>" % gname),
+                        ("server_reduce_compress", part_ms[1], d * bs, "k_server_pass"),
+                        ("decompress_update", part_ms[2], d * bu, "k_update"),
+                        ("warmup_adam_step", warm_avg, d * (n * gbytes + 24),
+                         "k_warmup<%s>" % gname))
                     if ms},
     }
     if not args.no_probe:
