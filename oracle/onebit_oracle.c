@@ -31,6 +31,25 @@
  *     NaN gives 0); bits of padding elements are 0;
  *   - an empty segment has scale 0.
  * Padding elements are never read or written.
+ *
+ * What pins each function (tests/test_oracle_pins.py, tests/test_freeze_cpu.py;
+ * none is "parity unpinned"):
+ *   orc_chunk_len, orc_layout  brute-force chunk membership, the BERT sizes
+ *   orc_compress               numpy.packbits, numpy.linalg.norm, the
+ *                              correctly rounded fp32 of the exact rational
+ *                              root mean square, +-0/NaN/empty segments,
+ *                              equal-magnitude inputs (exact, zero error)
+ *   orc_decode(_range)         the hand-worked example's decoded momentum
+ *   orc_warmup_range           torch.optim.Adam (with and without bias
+ *                              correction), a constant-gradient closed form,
+ *                              the variance's closed form
+ *   orc_l1_norm_range          an exact (fractions) sum
+ *   orc_worker_segment,        the hand-worked two-step example, the
+ *   orc_server_segment,        error-feedback identity, the appendix's
+ *   orc_update_segment,        telescoping form, identical workers, n = 1,
+ *   orc_step                   chunk independence, the exact rational mean
+ *                              of the decoded messages, a checkpoint resume
+ *   orc_step_uncompressed_range  torch.optim.SGD momentum (change of variables)
  */
 #include <math.h>
 #include <stdint.h>
