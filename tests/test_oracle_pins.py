@@ -545,3 +545,74 @@ def test_oracle_matches_its_recorded_reference_run():
     gd = _golden("oracle_reference_run.json")
     assert gd["workload"] == mod.WORKLOAD
     assert mod.digests(mod.run()) == gd["sha256"]
+
+
+# ---------------------------------------------------------------------------
+# Brute force on tiny sizes: the whole compression step written again with
+# numpy scalar semantics (fp32 operations one at a time, fp64 reductions),
+# over sizes that cross word and chunk boundaries and special values
+# ---------------------------------------------------------------------------
+
+def _numpy_step(L, x, m, v, delta, dbar, g, lr, beta1, eps):
+    f32 = np.float32
+    n = L.n
+    omb1 = f32(f32(1.0) - f32(beta1))
+    b1 = f32(beta1)
+    segs = L.segments()
+    wsign = np.zeros((n, L.D), bool)
+    wscale = np.zeros((n, len(segs)), np.float32)
+    for i in range(n):
+        for q, (b, e) in enumerate(segs):
+            if e == b:
+                continue
+            z = [f32(f32(f32(b1 * m[k]) + f32(omb1 * g[i, k])) + delta[i, k]) for k in range(b, e)]
+            s = f32(math.sqrt(sum(float(t) * float(t) for t in z) / (e - b)))
+            wscale[i, q] = s
+            for k, t in zip(range(b, e), z):
+                wsign[i, k] = t >= 0
+                delta[i, k] = f32(t - s) if t >= 0 else f32(t + s)
+    for q, (b, e) in enumerate(segs):
+        if e == b:
+            continue
+        zb = []
+        for k in range(b, e):
+            acc = 0.0
+            for i in range(n):
+                acc += float(wscale[i, q]) if wsign[i, k] else -float(wscale[i, q])
+            zb.append(f32(f32(acc / n) + dbar[k]))
+        s = f32(math.sqrt(sum(float(t) * float(t) for t in zb) / (e - b)))
+        for k, t in zip(range(b, e), zb):
+            mb = s if t >= 0 else f32(-s)
+            dbar[k] = f32(t - mb)
+            x[k] = f32(x[k] - f32(f32(lr) * f32(mb / f32(math.sqrt(f32(v[k] + f32(eps)))))))
+            m[k] = mb
+
+
+@pytest.mark.parametrize("numel,n", [([1], 1), ([63, 64, 65], 2), ([130, 7], 3), ([200], 4),
+                                     ([129, 0, 64], 8), ([1, 2, 3, 190], 4)])
+def test_brute_force_tiny_step_against_numpy(numel, n):
+    L = oracle.Layout(numel, n)
+    rng = np.random.default_rng(sum(numel) + n)
+    mask = L.real_mask()
+    x = (rng.standard_normal(L.D) * 0.02).astype(np.float32)
+    m = (rng.standard_normal(L.D) * 1e-3).astype(np.float32)
+    v = (rng.random(L.D) * 1e-5).astype(np.float32)
+    for a in (x, m, v):
+        a[~mask] = 0
+    st = oracle.State(L, x, m, v)
+    X, M, V = x.copy(), m.copy(), v.copy()
+    delta = np.zeros((n, L.D), np.float32)
+    dbar = np.zeros(L.D, np.float32)
+    for t in range(3):
+        g = (rng.standard_normal((n, L.D)) * 1e-3).astype(np.float32)
+        g[:, ::11] = 0.0                 # exact zeros
+        g[:, 5::13] = -0.0
+        if t == 1:
+            g[:, :] = g[0]              # all workers equal for one step
+        g[:, ~mask] = 0
+        st.step(g, LR, BETA1, EPS)
+        _numpy_step(L, X, M, V, delta, dbar, g, LR, BETA1, EPS)
+        assert np.array_equal(st.x[mask], X[mask]), t
+        assert np.array_equal(st.m[mask], M[mask]), t
+        assert np.array_equal(st.delta[:, mask], delta[:, mask]), t
+        assert np.array_equal(st.delta_bar[mask], dbar[mask]), t
