@@ -39,7 +39,9 @@
  *   pass over the buffer.  All-zero buffers and scales mean delta = 0.  To
  *   load an explicit delta, write it into the error buffer and zero the
  *   matching scales; onebit_error_materialize() produces explicit delta.
- * Pointers.  Every buffer pointer is a device pointer on the plan's device.
+ * Pointers.  Every buffer pointer is a device pointer on the plan's device;
+ *   element buffers (sized by D or W) may be NULL only when the plan has no
+ *   elements (D = 0), where calls touch nothing but the segment scales.
  *   fp32 buffers must be 16-byte aligned and leading dimensions (in elements)
  *   multiples of 4; uint64 bit buffers 8-byte aligned.  The caller owns every
  *   buffer; calls never allocate, never synchronize the host and never read

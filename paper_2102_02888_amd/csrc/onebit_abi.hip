@@ -75,25 +75,27 @@ int check_plan(const onebit_plan_s *p)
     return ONEBIT_OK;
 }
 
-int check_f32(const void *ptr, const char *name)
+// Element buffers ([D] floats, rows of D, [W] words, rows of W): NULL is
+// accepted only for a plan with no elements (D = 0, nothing is touched).
+int check_f32(const onebit_plan_s *p, const void *ptr, const char *name)
 {
-    if (!ptr) return fail(ONEBIT_EINVAL, "%s is NULL", name);
+    if (!ptr) return p->D == 0 ? ONEBIT_OK : fail(ONEBIT_EINVAL, "%s is NULL", name);
     if (!aligned(ptr, 16)) return fail(ONEBIT_EALIGN, "%s is not 16-byte aligned", name);
     return ONEBIT_OK;
 }
 
-int check_u64(const void *ptr, const char *name)
+int check_u64(const onebit_plan_s *p, const void *ptr, const char *name)
 {
-    if (!ptr) return fail(ONEBIT_EINVAL, "%s is NULL", name);
+    if (!ptr) return p->D == 0 ? ONEBIT_OK : fail(ONEBIT_EINVAL, "%s is NULL", name);
     if (!aligned(ptr, 8)) return fail(ONEBIT_EALIGN, "%s is not 8-byte aligned", name);
     return ONEBIT_OK;
 }
 
-int check_grads(const void *g, int32_t dtype)
+int check_grads(const onebit_plan_s *p, const void *g, int32_t dtype)
 {
-    if (!g) return fail(ONEBIT_EINVAL, "grads is NULL");
     if (dtype != ONEBIT_GRAD_F32 && dtype != ONEBIT_GRAD_BF16 && dtype != ONEBIT_GRAD_F16)
         return fail(ONEBIT_EINVAL, "grad_dtype %d is not one of ONEBIT_GRAD_*", dtype);
+    if (!g) return p->D == 0 ? ONEBIT_OK : fail(ONEBIT_EINVAL, "grads is NULL");
     const size_t need = dtype == ONEBIT_GRAD_F32 ? 16 : 8;
     if (!aligned(g, need)) return fail(ONEBIT_EALIGN, "grads is not %zu-byte aligned", need);
     return ONEBIT_OK;
@@ -103,7 +105,7 @@ int check_ld(int64_t ld, int64_t need, bool mult4, const char *name)
 {
     if (ld < need) return fail(ONEBIT_EINVAL, "%s = %lld is below %lld", name, (long long)ld,
                                (long long)need);
-    if (mult4 && ld % 4 != 0) return fail(ONEBIT_EALIGN, "%s = %lld is not a multiple of 4",
+    if (mult4 && need > 0 && ld % 4 != 0) return fail(ONEBIT_EALIGN, "%s = %lld is not a multiple of 4",
                                           name, (long long)ld);
     return ONEBIT_OK;
 }
@@ -353,10 +355,10 @@ int onebit_warmup_adam_step(onebit_plan p, float *x, float *m, float *v, const v
                             onebit_stream stream)
 {
     TRY(check_plan(p));
-    TRY(check_f32(x, "x"));
-    TRY(check_f32(m, "m"));
-    TRY(check_f32(v, "v"));
-    TRY(check_grads(grads, grad_dtype));
+    TRY(check_f32(p, x, "x"));
+    TRY(check_f32(p, m, "m"));
+    TRY(check_f32(p, v, "v"));
+    TRY(check_grads(p, grads, grad_dtype));
     if (n_grads < 1) return fail(ONEBIT_EINVAL, "n_grads < 1");
     if (step < 1) return fail(ONEBIT_EINVAL, "step < 1 (steps are 1-based)");
     TRY(check_ld(grad_ld, p->D, n_grads > 1, "grad_ld"));
@@ -383,15 +385,15 @@ int onebit_worker_compress(onebit_plan p, const float *m, const uint64_t *m_bits
 {
     TRY(check_plan(p));
     if (m) {
-        TRY(check_f32(m, "m"));
+        TRY(check_f32(p, m, "m"));
     } else {
-        TRY(check_u64(m_bits, "m_bits (m is NULL)"));
+        TRY(check_u64(p, m_bits, "m_bits (m is NULL)"));
         if (!m_scales) return fail(ONEBIT_EINVAL, "m_scales is NULL (m is NULL)");
         if (!aligned(m_scales, 4)) return fail(ONEBIT_EALIGN, "m_scales misaligned");
     }
-    TRY(check_grads(grads, grad_dtype));
-    TRY(check_f32(worker_err, "worker_err"));
-    TRY(check_u64(worker_bits, "worker_bits"));
+    TRY(check_grads(p, grads, grad_dtype));
+    TRY(check_f32(p, worker_err, "worker_err"));
+    TRY(check_u64(p, worker_bits, "worker_bits"));
     if (!worker_scales) return fail(ONEBIT_EINVAL, "worker_scales is NULL");
     if (!aligned(worker_scales, 4)) return fail(ONEBIT_EALIGN, "worker_scales misaligned");
     if (!workspace) return fail(ONEBIT_EINVAL, "workspace is NULL");
@@ -402,14 +404,14 @@ int onebit_worker_compress(onebit_plan p, const float *m, const uint64_t *m_bits
     TRY(check_ld(err_ld, p->D, n_local > 1, "err_ld"));
     TRY(check_ld(bits_ld, p->W, false, "bits_ld"));
     TRY(check_ld(scales_ld, p->S, false, "scales_ld"));
-    if (p->T == 0) return ONEBIT_OK;
     double *part = (double *)((char *)workspace + worker_partial_offset(p));
     hipStream_t s = (hipStream_t)stream;
     // Packed momentum costs 1/8 byte per element to re-derive, so each wave
     // takes one worker and the grid streams two rows at a time; an fp32
     // momentum is read once per tile for all local workers instead.
     const int group = m ? n_local : 1;
-    TRY_HIP(onebit::launch_worker_pass(p->tb, p->T, m, m_bits, m_scales, grads, grad_dtype,
+    if (p->T > 0)
+        TRY_HIP(onebit::launch_worker_pass(p->tb, p->T, m, m_bits, m_scales, grads, grad_dtype,
                                        grad_ld, worker_err, err_ld, worker_scales, scales_ld,
                                        worker_bits, bits_ld, part, n_local, group, beta1, s),
             "worker kernel launch");
@@ -427,11 +429,11 @@ int onebit_server_reduce_compress(onebit_plan p, int32_t server_begin, int32_t s
                                   onebit_stream stream)
 {
     TRY(check_plan(p));
-    TRY(check_u64(worker_bits, "worker_bits"));
+    TRY(check_u64(p, worker_bits, "worker_bits"));
     if (!worker_scales) return fail(ONEBIT_EINVAL, "worker_scales is NULL");
     if (!aligned(worker_scales, 4)) return fail(ONEBIT_EALIGN, "worker_scales misaligned");
-    TRY(check_f32(server_err, "server_err"));
-    TRY(check_u64(server_bits, "server_bits"));
+    TRY(check_f32(p, server_err, "server_err"));
+    TRY(check_u64(p, server_bits, "server_bits"));
     if (!server_scales) return fail(ONEBIT_EINVAL, "server_scales is NULL");
     if (!aligned(server_scales, 4)) return fail(ONEBIT_EALIGN, "server_scales misaligned");
     if (!workspace) return fail(ONEBIT_EINVAL, "workspace is NULL");
@@ -479,12 +481,12 @@ int onebit_decompress_update(onebit_plan p, const uint64_t *server_bits,
                              const float *v_frozen, float lr, float eps, onebit_stream stream)
 {
     TRY(check_plan(p));
-    TRY(check_u64(server_bits, "server_bits"));
+    TRY(check_u64(p, server_bits, "server_bits"));
     if (!server_scales) return fail(ONEBIT_EINVAL, "server_scales is NULL");
     if (!aligned(server_scales, 4)) return fail(ONEBIT_EALIGN, "server_scales misaligned");
-    TRY(check_f32(x, "x"));
-    if (m_out) TRY(check_f32(m_out, "m_out"));
-    TRY(check_f32(v_frozen, "v_frozen"));
+    TRY(check_f32(p, x, "x"));
+    if (m_out) TRY(check_f32(p, m_out, "m_out"));
+    TRY(check_f32(p, v_frozen, "v_frozen"));
     if (p->T == 0) return ONEBIT_OK;
     TRY_HIP(onebit::launch_update(p->tb, p->T, server_bits, server_scales, x, m_out, v_frozen,
                                   lr, eps, (hipStream_t)stream),
@@ -500,11 +502,11 @@ int onebit_step(onebit_plan p, float *x, float *m, const float *v_frozen, const 
 {
     TRY(check_plan(p));
     // Validate everything before the first launch so that an error writes nothing.
-    TRY(check_f32(x, "x"));
-    if (m) TRY(check_f32(m, "m"));
-    TRY(check_f32(v_frozen, "v_frozen"));
-    TRY(check_f32(server_err, "server_err"));
-    TRY(check_u64(server_bits, "server_bits"));
+    TRY(check_f32(p, x, "x"));
+    if (m) TRY(check_f32(p, m, "m"));
+    TRY(check_f32(p, v_frozen, "v_frozen"));
+    TRY(check_f32(p, server_err, "server_err"));
+    TRY(check_u64(p, server_bits, "server_bits"));
     if (!server_scales) return fail(ONEBIT_EINVAL, "server_scales is NULL");
     if (!aligned(server_scales, 4)) return fail(ONEBIT_EALIGN, "server_scales misaligned");
     TRY(onebit_worker_compress(p, m, server_bits, server_scales, grads, grad_dtype, grad_ld, p->n,
@@ -522,10 +524,10 @@ int onebit_adam_message_step(onebit_plan p, float *x, float *m, float *v, const 
                              int32_t bias_correction, int64_t step, onebit_stream stream)
 {
     TRY(check_plan(p));
-    TRY(check_f32(x, "x"));
-    TRY(check_f32(m, "m"));
-    TRY(check_f32(v, "v"));
-    TRY(check_u64(bits, "bits"));
+    TRY(check_f32(p, x, "x"));
+    TRY(check_f32(p, m, "m"));
+    TRY(check_f32(p, v, "v"));
+    TRY(check_u64(p, bits, "bits"));
     if (!scales) return fail(ONEBIT_EINVAL, "scales is NULL");
     if (!aligned(scales, 4)) return fail(ONEBIT_EALIGN, "scales misaligned");
     if (step < 1) return fail(ONEBIT_EINVAL, "step < 1 (steps are 1-based)");
@@ -547,10 +549,10 @@ int onebit_uncompressed_step(onebit_plan p, float *x, float *m, const float *v_f
                              onebit_stream stream)
 {
     TRY(check_plan(p));
-    TRY(check_f32(x, "x"));
-    TRY(check_f32(m, "m"));
-    TRY(check_f32(v_frozen, "v_frozen"));
-    TRY(check_grads(grads, grad_dtype));
+    TRY(check_f32(p, x, "x"));
+    TRY(check_f32(p, m, "m"));
+    TRY(check_f32(p, v_frozen, "v_frozen"));
+    TRY(check_grads(p, grads, grad_dtype));
     if (n_grads < 1) return fail(ONEBIT_EINVAL, "n_grads < 1");
     TRY(check_ld(grad_ld, p->D, n_grads > 1, "grad_ld"));
     if (p->T == 0) return ONEBIT_OK;
@@ -564,7 +566,7 @@ int onebit_l1_norm(onebit_plan p, const float *v, void *workspace, double *out,
                    onebit_stream stream)
 {
     TRY(check_plan(p));
-    TRY(check_f32(v, "v"));
+    TRY(check_f32(p, v, "v"));
     if (!workspace) return fail(ONEBIT_EINVAL, "workspace is NULL");
     if (!aligned(workspace, 256)) return fail(ONEBIT_EALIGN, "workspace is not 256-byte aligned");
     if (!out) return fail(ONEBIT_EINVAL, "out is NULL");
@@ -579,10 +581,10 @@ int onebit_decode(onebit_plan p, const uint64_t *bits, const float *scales, floa
                   onebit_stream stream)
 {
     TRY(check_plan(p));
-    TRY(check_u64(bits, "bits"));
+    TRY(check_u64(p, bits, "bits"));
     if (!scales) return fail(ONEBIT_EINVAL, "scales is NULL");
     if (!aligned(scales, 4)) return fail(ONEBIT_EALIGN, "scales misaligned");
-    TRY(check_f32(out, "out"));
+    TRY(check_f32(p, out, "out"));
     if (p->T == 0) return ONEBIT_OK;
     TRY_HIP(onebit::launch_decode(p->tb, p->T, bits, scales, out, (hipStream_t)stream),
             "decode kernel launch");
@@ -594,8 +596,8 @@ int onebit_error_materialize(onebit_plan p, const float *err_state, int64_t err_
                              float *delta_out, int64_t out_ld, onebit_stream stream)
 {
     TRY(check_plan(p));
-    TRY(check_f32(err_state, "err_state"));
-    TRY(check_f32(delta_out, "delta_out"));
+    TRY(check_f32(p, err_state, "err_state"));
+    TRY(check_f32(p, delta_out, "delta_out"));
     if (!scales) return fail(ONEBIT_EINVAL, "scales is NULL");
     if (!aligned(scales, 4)) return fail(ONEBIT_EALIGN, "scales misaligned");
     if (rows < 1) return fail(ONEBIT_EINVAL, "rows < 1");

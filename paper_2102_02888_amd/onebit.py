@@ -227,7 +227,7 @@ def onebit_step(plan, x, m, v_frozen, grads, worker_err, server_err, worker_bits
     n, D, W, S = plan.n, plan.D, plan.W, plan.S
     # the step addresses worker_bits / worker_scales with row strides W and S
     for t, name, cols in ((worker_bits, "worker_bits", W), (worker_scales, "worker_scales", S)):
-        if t is not None and t.dim() == 2 and t.stride(0) != cols:
+        if t is not None and t.dim() == 2 and cols > 0 and t.stride(0) != cols:
             raise ValueError("%s must be contiguous [n, %d] for onebit_step" % (name, cols))
     call("onebit_step", plan.handle, _ptr(x, torch.float32, "x", D),
          _ptr(m, torch.float32, "m", D), _ptr(v_frozen, torch.float32, "v_frozen", D),

@@ -248,3 +248,25 @@ def test_binding_refuses_short_buffers(dev):
                                          st.workspace, scales_ld=plan.S + 1)
     torch.cuda.synchronize()
     plan.close()
+
+
+def test_plan_without_elements(dev):
+    """Only empty tensors (d = 0): every call succeeds without touching an
+    element buffer (zero-size tensors pass NULL), and every segment's scale
+    is 0."""
+    import paper_2102_02888_amd as ob
+    plan = ob.Plan([0, 0], 3)
+    assert (plan.d, plan.D, plan.W, plan.S, plan.T) == (0, 0, 0, 6, 0)
+    st = ob.State(plan, dev)
+    st.worker_scales.fill_(7.0)
+    st.server_scales.fill_(7.0)
+    for t in (1, 2):
+        st.warmup(1e-3, 0.9, 0.999, 1e-8, t)
+    for _ in range(3):
+        st.step(1e-3, 0.9, 1e-8)
+    st.step_uncompressed(1e-3, 0.9, 1e-8)
+    assert st.variance_l1_norm() == 0.0
+    torch.cuda.synchronize()
+    assert not host(st.worker_scales).any() and not host(st.server_scales).any()
+    assert st.momentum().numel() == 0 and st.worker_delta().numel() == 0
+    plan.close()
