@@ -485,3 +485,24 @@ def test_hand_worked_example_on_gpu(ob, dev):
         assert host(st.x)[:2].tolist() == sd["x"]
         assert host(st.momentum())[:2].tolist() == sd["m"]
     plan.close()
+
+
+def _random_config(seed):
+    rng = np.random.default_rng(1000 + seed)
+    k = int(rng.integers(1, 21))
+    numel = [int(v) for v in np.exp(rng.uniform(0, np.log(50_000), size=k)).astype(np.int64)]
+    numel[int(rng.integers(0, k))] = 0 if k > 1 else numel[0]
+    n = int(rng.choice([1, 2, 3, 5, 8, 16, 33]))
+    packed = bool(rng.integers(0, 2))
+    gdt = [torch.float32, torch.bfloat16, torch.float16][int(rng.integers(0, 3))]
+    return numel, n, packed, gdt
+
+
+@pytest.mark.parametrize("seed", range(8))
+def test_free_running_random_configs(ob, dev, seed):
+    """Seeded random layouts (1-20 tensors of 1-50,000 elements, one of them
+    possibly empty), worker counts, momentum forms and gradient types."""
+    numel, n, packed, gdt = _random_config(seed)
+    wl = synth.Workload(name="random%d" % seed, numel=numel, n=n, warmup_steps=2, steps=3,
+                        seed_grads=50 + seed)
+    _free_run(ob, dev, wl, packed=packed, grad_dtype=gdt)
