@@ -1,0 +1,44 @@
+"""Host-side pieces of bench.py: the algorithmic byte counts behind the
+roofline figures and the guard on recorded counter traffic."""
+import json
+import os
+
+import bench
+
+
+def test_algorithmic_bytes_per_param():
+    # BERT-Large, n = 32, fp32 gradients: worker 1/8 + 32 * (4 + 4 + 4 + 1/8)
+    assert bench.algorithmic_bytes_per_param(32) == (388.125, 12.125, 12.125)
+    # 16-bit gradients cut 2 bytes per worker row
+    w, s, u = bench.algorithmic_bytes_per_param(32, 2)
+    assert w == 388.125 - 64 and (s, u) == (12.125, 12.125)
+    # the server reads n sign bits per element
+    assert bench.algorithmic_bytes_per_param(256)[1] == 256 / 8 + 8.125
+
+
+def test_measured_traffic_requires_matching_kernel_source(tmp_path, monkeypatch):
+    prof = tmp_path / "profiles"
+    prof.mkdir()
+    src = tmp_path / "paper_2102_02888_amd" / "csrc"
+    src.mkdir(parents=True)
+    (src / "onebit_kernels.hip").write_text("// kernels v1\n")
+    import hashlib
+    sha = hashlib.sha256(b"// kernels v1\n").hexdigest()
+    info = {"kernels_source_sha256": sha,
+            "kernels": {"k_update": {"traffic_bytes": 123.0}}}
+    (prof / "pmc_traffic_w.md").write_text("x\n```json\n%s\n```\n" % json.dumps(info))
+    monkeypatch.setattr(bench, "ROOT", str(tmp_path))
+    assert bench.measured_traffic("w", "k_update") == 123.0
+    assert bench.measured_traffic("w", "k_other") is None
+    assert bench.measured_traffic("missing", "k_update") is None
+    (src / "onebit_kernels.hip").write_text("// kernels v2\n")
+    assert bench.measured_traffic("w", "k_update") is None
+
+
+def test_multi_gpu_request_is_refused():
+    import subprocess
+    import sys
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    r = subprocess.run([sys.executable, os.path.join(root, "bench.py"), "--gpus", "2"],
+                       capture_output=True, text=True, timeout=120)
+    assert r.returncode == 2 and "one GPU" in r.stderr
