@@ -109,6 +109,14 @@ def test_bert_large_full_size_bf16_grads(ob, dev):
                       grad_dtype=torch.bfloat16)
 
 
+def test_bert_base_full_size_fp16_grads(ob, dev):
+    """BERT-Base with float16 gradients: the per-tensor gradient scale puts
+    many of them in fp16's subnormal range, which the widening keeps exact:
+    chunk 3."""
+    _free_run_sampled(ob, dev, synth.get("bert_base"), warm=1, steps=2, sample_segs=[3],
+                      grad_dtype=torch.float16)
+
+
 def test_bert_base_full_size(ob, dev):
     """d = 108,888,576, n = 16: the last chunk is the short one."""
     _free_run_sampled(ob, dev, synth.get("bert_base"), warm=2, steps=3, sample_segs=[0, 15])
