@@ -630,6 +630,47 @@ __device__ __forceinline__ void wave_sync()
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
+// Last part of the server pass for one tile: average, add the server error,
+// store the new compensated error state, the sign words and the tile's sum of
+// squares.
+template <bool FULL, bool POW2>
+__device__ __forceinline__ void server_epilogue(const double (&sum)[kSubBlocks][4],
+                                                const v4f (&cv)[kSubBlocks], float sprev, int n,
+                                                int lane, const Tile &tile, int64_t t,
+                                                float *__restrict__ serr,
+                                                uint64_t *__restrict__ sbits,
+                                                double *__restrict__ partial)
+{
+    const int len = tile.len;
+    const int64_t base = tile.start;
+    const int nwords = (len + 63) >> 6;
+    const double dn = (double)n;
+    const double inv_n = 1.0 / dn;
+    double acc = 0.0;
+#pragma unroll
+    for (int b = 0; b < kSubBlocks; ++b) {
+        const int li = b * (kWave * 4) + 4 * lane;
+        v4f zv;
+        uint32_t nib = 0;
+#pragma unroll
+        for (int c = 0; c < 4; ++c) {
+            const float avg = (float)(POW2 ? sum[b][c] * inv_n : sum[b][c] / dn);
+            const float z = avg + error_of(cv[b][c], sprev);
+            zv[c] = z;
+            const bool valid = FULL || li + c < len;
+            const double zd = valid ? (double)z : 0.0;
+            acc += zd * zd;
+            nib |= (valid && z >= 0.f) ? (1u << c) : 0u;
+        }
+        st4<FULL>(serr + base, li, len, zv);
+        const uint64_t word = row_sign_word(nib, lane);
+        const int w = 4 * b + (lane >> 4);
+        if ((lane & 15) == 0 && (FULL || w < nwords)) sbits[(base >> 6) + w] = word;
+    }
+    acc = wave_sum(acc);
+    if (lane == 0) partial[t] = acc;
+}
+
 // LDS row stride (in 32-bit words) of the sign staging: a multiple of 4 keeps
 // 128-bit accesses aligned, and 40 puts the 64 words a wave reads at once in
 // the accumulation on 64 different banks.
@@ -841,33 +882,20 @@ __global__ __launch_bounds__(kBlock) void k_server_pass(
         }
         wave_sync();
     }
-    // sum / n rounded to fp64; for a power-of-two n that is an exact scaling
-    const double dn = (double)n;
-    const bool pow2 = (n & (n - 1)) == 0;
-    const double inv_n = 1.0 / dn;
-    double acc = 0.0;
-#pragma unroll
-    for (int b = 0; b < kSubBlocks; ++b) {
-        const int li = b * (kWave * 4) + 4 * lane;
-        v4f zv;
-        uint32_t nib = 0;
-#pragma unroll
-        for (int c = 0; c < 4; ++c) {
-            const float avg = (float)(pow2 ? sum[b][c] * inv_n : sum[b][c] / dn);
-            const float z = avg + error_of(cv[b][c], sprev);
-            zv[c] = z;
-            const bool valid = li + c < len;
-            const double zd = valid ? (double)z : 0.0;
-            acc += zd * zd;
-            nib |= (valid && z >= 0.f) ? (1u << c) : 0u;
-        }
-        if (full) st4<true>(serr + base, li, len, zv); else st4<false>(serr + base, li, len, zv);
-        const uint64_t word = row_sign_word(nib, lane);
-        const int w = 4 * b + (lane >> 4);
-        if ((lane & 15) == 0 && w < nwords) sbits[(base >> 6) + w] = word;
+    // avg = sum / n rounded to fp32 (for a power-of-two n, sum * (1/n) is the
+    // same exact scaling), then the compensated value, its sign word and
+    // square; FULL and POW2 are wave-uniform, so each wave runs one variant
+    if (full) {
+        if ((n & (n - 1)) == 0)
+            server_epilogue<true, true>(sum, cv, sprev, n, lane, tile, t, serr, sbits, partial);
+        else
+            server_epilogue<true, false>(sum, cv, sprev, n, lane, tile, t, serr, sbits, partial);
+    } else {
+        if ((n & (n - 1)) == 0)
+            server_epilogue<false, true>(sum, cv, sprev, n, lane, tile, t, serr, sbits, partial);
+        else
+            server_epilogue<false, false>(sum, cv, sprev, n, lane, tile, t, serr, sbits, partial);
     }
-    acc = wave_sum(acc);
-    if (lane == 0) partial[t] = acc;
 }
 
 
