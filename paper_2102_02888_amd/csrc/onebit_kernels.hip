@@ -609,19 +609,21 @@ __device__ __forceinline__ uint32_t nibbles_to_bytes(uint32_t x)
     return x;
 }
 
+// Wave-wide max of an int through DPP: shifts within each 16-lane row, then
+// row broadcasts carry the row maxima up to lane 63, which every lane reads.
 __device__ __forceinline__ int wave_max(int v)
 {
-#pragma unroll
-    for (int off = 32; off >= 1; off >>= 1) v = max(v, __shfl_xor(v, off, kWave));
-    return v;
+    constexpr int lo = INT32_MIN;
+    v = max(v, __builtin_amdgcn_update_dpp(lo, v, 0x111, 0xF, 0xF, false));  // row_shr 1
+    v = max(v, __builtin_amdgcn_update_dpp(lo, v, 0x112, 0xF, 0xF, false));  // row_shr 2
+    v = max(v, __builtin_amdgcn_update_dpp(lo, v, 0x114, 0xF, 0xF, false));  // row_shr 4
+    v = max(v, __builtin_amdgcn_update_dpp(lo, v, 0x118, 0xF, 0xF, false));  // row_shr 8
+    v = max(v, __builtin_amdgcn_update_dpp(lo, v, 0x142, 0xA, 0xF, false));  // row_bcast 15
+    v = max(v, __builtin_amdgcn_update_dpp(lo, v, 0x143, 0xC, 0xF, false));  // row_bcast 31
+    return __builtin_amdgcn_readlane(v, kWave - 1);
 }
 
-__device__ __forceinline__ int wave_min(int v)
-{
-#pragma unroll
-    for (int off = 32; off >= 1; off >>= 1) v = min(v, __shfl_xor(v, off, kWave));
-    return v;
-}
+__device__ __forceinline__ int wave_min(int v) { return -wave_max(-v); }
 
 __device__ __forceinline__ void wave_sync()
 {
