@@ -16,7 +16,7 @@
 // onebit.h): fp32 values, one rounding per operation (built with
 // -ffp-contract=off), correctly rounded sqrt and division, fp64 reductions
 // rounded once to fp32.  Reductions over a segment are deterministic:
-// per-tile partial sums (fixed lane order, xor butterfly) are written to a
+// per-tile partial sums (a fixed DPP reduction tree) are written to a
 // workspace and summed in a fixed order by a finalize kernel; no atomics.
 #include "onebit_internal.h"
 #include <algorithm>
@@ -132,12 +132,29 @@ __device__ __forceinline__ uint64_t row_sign_word(uint32_t nib, int lane)
     return ((uint64_t)row_or16(hi) << 32) | (uint64_t)row_or16(lo);
 }
 
-// Deterministic wave-wide fp64 sum (every lane gets the same value).
+// DPP move of an fp64 value (both 32-bit halves); lanes the pattern does not
+// reach get 0.0.
+template <int CTRL, int ROW_MASK>
+__device__ __forceinline__ double dpp_f64(double v)
+{
+    const int lo = __builtin_amdgcn_update_dpp(0, __double2loint(v), CTRL, ROW_MASK, 0xF, false);
+    const int hi = __builtin_amdgcn_update_dpp(0, __double2hiint(v), CTRL, ROW_MASK, 0xF, false);
+    return __hiloint2double(hi, lo);
+}
+
+// Deterministic wave-wide fp64 sum (every lane gets the same value): a fixed
+// tree of DPP row shifts and row broadcasts, read from lane 63.
 __device__ __forceinline__ double wave_sum(double a)
 {
-#pragma unroll
-    for (int off = 32; off >= 1; off >>= 1) a += __shfl_xor(a, off, kWave);
-    return a;
+    a += dpp_f64<0x111, 0xF>(a);  // row_shr 1
+    a += dpp_f64<0x112, 0xF>(a);  // row_shr 2
+    a += dpp_f64<0x114, 0xF>(a);  // row_shr 4
+    a += dpp_f64<0x118, 0xF>(a);  // row_shr 8
+    a += dpp_f64<0x142, 0xA>(a);  // row_bcast 15
+    a += dpp_f64<0x143, 0xC>(a);  // row_bcast 31
+    const int lo = __builtin_amdgcn_readlane(__double2loint(a), kWave - 1);
+    const int hi = __builtin_amdgcn_readlane(__double2hiint(a), kWave - 1);
+    return __hiloint2double(hi, lo);
 }
 
 // Error from the compensated form: z - C[z] given z and its segment scale s.
