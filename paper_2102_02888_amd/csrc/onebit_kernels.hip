@@ -603,41 +603,19 @@ __global__ __launch_bounds__(kBlock) void k_finalize(
 // staged in LDS 32 worker rows at a time (coalesced 128-byte row reads),
 // transposed so that the words of consecutive workers for one 32-element
 // half-word are adjacent.  For the table lookups each group of 8 workers is
-// then regrouped in place, one 8x8 nibble transpose per (half-word, group):
-// afterwards one 32-bit LDS word holds the 8 workers' bits of the 4 elements a
-// lane owns.
+// then regrouped in place, four 8x8 bit transposes per (half-word, group):
+// afterwards each LDS byte holds the 8 workers' bits of one element, the
+// element's table index.
 //
 // The average is an fp64 sum of +-scale over the workers in worker order.
 // When every partial sum of the segment's scales is exactly representable in
 // fp64 (the scales' exponents span at most 29 - ceil(log2 n) binades; true
 // for any realistic message set) the sum is exact, so it may be formed in any
 // grouping: then each group of 8 workers is one lookup in a 256-entry table
-// of its signed scale sums, indexed by the 8 workers' bits of the element (a
-// bit permutation of their nibbles).  The 256-entry tables are sums of two
+// of its signed scale sums, indexed by the 8 workers' bits of the element.  The 256-entry tables are sums of two
 // 16-entry tables, each built from 4 scales.  Otherwise every worker is added
 // one by one.  Both give the oracle's sum.
 // ---------------------------------------------------------------------------
-// Delta swap: exchanges the bits of x selected by m with the bits d places
-// above them.
-__device__ __forceinline__ uint32_t delta_swap(uint32_t x, int d, uint32_t m)
-{
-    const uint32_t t = ((x >> d) ^ x) & m;
-    return x ^ t ^ (t << d);
-}
-
-// x holds 8 nibbles, nibble k = worker k's sign bits of 4 elements (bit c =
-// element c), i.e. bit 4k+c.  Returns byte c = the 8 workers' bits of element
-// c, i.e. bit 8c+k: the bit index (k2 k1 k0 c1 c0) rotated to (c1 c0 k2 k1 k0),
-// done as four swaps of index bits (4<->1, 3<->0, 2<->1, 1<->0).
-__device__ __forceinline__ uint32_t nibbles_to_bytes(uint32_t x)
-{
-    x = delta_swap(x, 14, 0x0000CCCCu);
-    x = delta_swap(x, 7, 0x00AA00AAu);
-    x = delta_swap(x, 2, 0x0C0C0C0Cu);
-    x = delta_swap(x, 1, 0x22222222u);
-    return x;
-}
-
 // Wave-wide max of an int through DPP: shifts within each 16-lane row, then
 // row broadcasts carry the row maxima up to lane 63, which every lane reads.
 __device__ __forceinline__ int wave_max(int v)
@@ -707,27 +685,28 @@ __device__ __forceinline__ void server_epilogue(const double (&sum)[kSubBlocks][
 // the accumulation on 64 different banks.
 constexpr int kBitsStride = kServerRowBatch + 8;
 
-// 8x8 transpose of 4-bit entries held in 8 words: nibble s of a[k] moves to
-// nibble k of a[s] (three rounds of block swaps: 4x4, 2x2, 1x1 nibbles).
-__device__ __forceinline__ void transpose_nibbles8(uint32_t (&a)[8])
+// 8x8 bit transposes of the four byte columns of 8 words: bit j of byte b of
+// a[k] moves to bit k of byte b of a[j] (three rounds of block swaps: 4x4,
+// 2x2, 1x1 bits, each on all four bytes at once).
+__device__ __forceinline__ void transpose_bits8x8(uint32_t (&a)[8])
 {
 #pragma unroll
     for (int k = 0; k < 4; ++k) {
-        const uint32_t t = ((a[k] >> 16) ^ a[k + 4]) & 0x0000FFFFu;
-        a[k] ^= t << 16;
+        const uint32_t t = ((a[k] >> 4) ^ a[k + 4]) & 0x0F0F0F0Fu;
+        a[k] ^= t << 4;
         a[k + 4] ^= t;
     }
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
         const int k = (i & 1) + 4 * (i >> 1);  // 0, 1, 4, 5
-        const uint32_t t = ((a[k] >> 8) ^ a[k + 2]) & 0x00FF00FFu;
-        a[k] ^= t << 8;
+        const uint32_t t = ((a[k] >> 2) ^ a[k + 2]) & 0x33333333u;
+        a[k] ^= t << 2;
         a[k + 2] ^= t;
     }
 #pragma unroll
     for (int k = 0; k < 8; k += 2) {
-        const uint32_t t = ((a[k] >> 4) ^ a[k + 1]) & 0x0F0F0F0Fu;
-        a[k] ^= t << 4;
+        const uint32_t t = ((a[k] >> 1) ^ a[k + 1]) & 0x55555555u;
+        a[k] ^= t << 1;
         a[k + 1] ^= t;
     }
 }
@@ -840,7 +819,8 @@ __global__ __launch_bounds__(kBlock) void k_server_pass(
                 }
                 s_lut4[wv][q][idx] = v;
             }
-            // regroup each (half-word, group of 8 workers) block in place
+            // regroup each (half-word, group of 8 workers) block in place:
+            // afterwards byte e>>3 of word r8 + (e&7) is element e's table index
 #pragma unroll 1
             for (int k = 0; k < (2 * kTileWords) * (kServerRowBatch / 8) / kWave; ++k) {
                 const int blk = lane + kWave * k;
@@ -850,7 +830,7 @@ __global__ __launch_bounds__(kBlock) void k_server_pass(
                     const uint4 u0 = *(const uint4 *)p;
                     const uint4 u1 = *(const uint4 *)(p + 4);
                     uint32_t a[8] = {u0.x, u0.y, u0.z, u0.w, u1.x, u1.y, u1.z, u1.w};
-                    transpose_nibbles8(a);
+                    transpose_bits8x8(a);
                     *(uint4 *)p = make_uint4(a[0], a[1], a[2], a[3]);
                     *(uint4 *)(p + 4) = make_uint4(a[4], a[5], a[6], a[7]);
                 }
@@ -880,11 +860,12 @@ __global__ __launch_bounds__(kBlock) void k_server_pass(
 #pragma unroll
                         for (int bb = 0; bb < 2; ++bb) {
                             const int hw = 2 * (4 * (bh + bb) + (lane >> 4)) + half;
-                            // nibble k: worker r8 + k's bits of the lane's 4 elements;
-                            // byte c of y: element c's 8 worker bits (the table index)
-                            const uint32_t y = nibbles_to_bytes(s_bits[wv][hw][r8 + (lane & 7)]);
+                            // the lane's elements e = 4 (lane & 7) + c of the half-word:
+                            // byte e >> 3 of word e & 7 holds the 8 workers' bits of e
+                            const uint8_t *blk = (const uint8_t *)&s_bits[wv][hw][r8];
+                            const int o = 16 * (lane & 1) + ((lane & 7) >> 1);
 #pragma unroll
-                            for (int c = 0; c < 4; ++c) idx[bb][c] = (y >> (8 * c)) & 0xFFu;
+                            for (int c = 0; c < 4; ++c) idx[bb][c] = blk[o + 4 * c];
                         }
                         double val[2][4];
 #pragma unroll
