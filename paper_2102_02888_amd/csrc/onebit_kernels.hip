@@ -752,12 +752,19 @@ __global__ __launch_bounds__(kBlock) void k_server_pass(
     float scl = 0.f;
     auto load_batch = [&](int r0) {
         const int rows = min(kServerRowBatch, n - r0);
+        // row r0 + (lane >> 4) + 4k of the lane's word wi
+        const uint64_t *p = wbits + (int64_t)(r0 + (lane >> 4)) * bits_ld + w0 + wi;
+        const int64_t step = 4 * bits_ld;
+        if (full && rows == kServerRowBatch) {  // wave-uniform: every load in range
 #pragma unroll
-        for (int k = 0; k < kServerRowBatch / 4; ++k) {
-            const int r = (lane >> 4) + 4 * k;
-            stg[k] = (r < rows && wi < nwords)
-                         ? __builtin_nontemporal_load(wbits + (int64_t)(r0 + r) * bits_ld + w0 + wi)
-                         : 0ull;
+            for (int k = 0; k < kServerRowBatch / 4; ++k)
+                stg[k] = __builtin_nontemporal_load(p + k * step);
+        } else {
+#pragma unroll
+            for (int k = 0; k < kServerRowBatch / 4; ++k) {
+                const int r = (lane >> 4) + 4 * k;
+                stg[k] = (r < rows && wi < nwords) ? __builtin_nontemporal_load(p + k * step) : 0ull;
+            }
         }
         scl = lane < rows ? wscales[(int64_t)(r0 + lane) * scales_ld + sq] : 0.f;
     };
@@ -792,12 +799,21 @@ __global__ __launch_bounds__(kBlock) void k_server_pass(
         if (r0 > 0) load_batch(r0);
         const int rows = min(kServerRowBatch, n - r0);
         const int rows8 = (rows + 7) & ~7;  // rows past the last worker hold zero words
+        if (full && rows == kServerRowBatch) {  // wave-uniform
 #pragma unroll
-        for (int k = 0; k < kServerRowBatch / 4; ++k) {
-            const int r = (lane >> 4) + 4 * k;
-            if (r < rows8 && wi < nwords) {
+            for (int k = 0; k < kServerRowBatch / 4; ++k) {
+                const int r = (lane >> 4) + 4 * k;
                 s_bits[wv][2 * wi][r] = (uint32_t)stg[k];
                 s_bits[wv][2 * wi + 1][r] = (uint32_t)(stg[k] >> 32);
+            }
+        } else {
+#pragma unroll
+            for (int k = 0; k < kServerRowBatch / 4; ++k) {
+                const int r = (lane >> 4) + 4 * k;
+                if (r < rows8 && wi < nwords) {
+                    s_bits[wv][2 * wi][r] = (uint32_t)stg[k];
+                    s_bits[wv][2 * wi + 1][r] = (uint32_t)(stg[k] >> 32);
+                }
             }
         }
         if (lane < rows) s_scale[wv][lane] = scl;
