@@ -668,7 +668,9 @@ __device__ __forceinline__ void server_epilogue(const double (&sum)[kSubBlocks][
             zv[c] = z;
             const bool valid = FULL || li + c < len;
             const double zd = valid ? (double)z : 0.0;
-            acc += zd * zd;
+            // zd * zd is exact in fp64 (a 24-bit significand squared), so the
+            // fused form rounds exactly as the separate multiply and add would
+            acc = __builtin_fma(zd, zd, acc);
             nib |= (valid && z >= 0.f) ? (1u << c) : 0u;
         }
         st4<FULL>(serr + base, li, len, zv);
