@@ -168,10 +168,16 @@ int plan_create_impl(const int64_t *tensor_numel, int32_t num_tensors, int32_t n
     p->D = off;
     p->W = off / 64;
 
+    // Tiles are cut at multiples of kTileElems of the flat index (a segment
+    // that starts or ends between two such points gets a short tile there),
+    // so that every full tile's sign words are 128-byte aligned.
+    auto tiles_of = [](int64_t b, int64_t e) -> int64_t {
+        if (e <= b) return 0;
+        return (e - 1) / kTileElems - b / kTileElems + 1;
+    };
     // One wave per tile must stay far inside a launch's 2^32 work items.
     int64_t tile_count = 0;
-    for (int64_t q = 0; q < p->S; ++q)
-        tile_count += (p->seg_end[q] - p->seg_begin[q] + kTileElems - 1) / kTileElems;
+    for (int64_t q = 0; q < p->S; ++q) tile_count += tiles_of(p->seg_begin[q], p->seg_end[q]);
     if (tile_count >= ((int64_t)1 << 25))
         return fail(ONEBIT_EINVAL, "%lld tiles: plans are limited to 2^25 tiles of %d elements",
                     (long long)tile_count, kTileElems);
@@ -191,12 +197,14 @@ int plan_create_impl(const int64_t *tensor_numel, int32_t num_tensors, int32_t n
         const int64_t b = p->seg_begin[q], en = p->seg_end[q];
         seg_len[q] = en - b;
         p->seg_tile_begin[q] = (int64_t)tiles.size();
-        for (int64_t s = b; s < en; s += kTileElems) {
+        for (int64_t s = b; s < en;) {
+            const int64_t next = std::min<int64_t>(en, (s / kTileElems + 1) * kTileElems);
             Tile t;
             t.start = s;
-            t.len = (int32_t)std::min<int64_t>(kTileElems, en - s);
+            t.len = (int32_t)(next - s);
             t.seg = (int32_t)q;
             tiles.push_back(t);
+            s = next;
         }
         p->seg_tile_end[q] = (int64_t)tiles.size();
         p->max_seg_tiles = std::max(p->max_seg_tiles, p->seg_tile_end[q] - p->seg_tile_begin[q]);
