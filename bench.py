@@ -40,6 +40,16 @@ def algorithmic_bytes_per_param(n, grad_bytes=4):
     return worker, server, update
 
 
+def kernels_source_sha256():
+    """Digest of the sources that decide what the kernels touch: the kernels
+    and the plan (tile) construction."""
+    import hashlib
+    h = hashlib.sha256()
+    for f in ("onebit_kernels.hip", "onebit_abi.hip"):
+        h.update(open(os.path.join(ROOT, "paper_2102_02888_amd", "csrc", f), "rb").read())
+    return h.hexdigest()
+
+
 def measured_traffic(workload, kernel):
     """HBM bytes per launch of `kernel` from the committed rocprofv3 counter
     summary (FETCH_SIZE + WRITE_SIZE, each calibrated on a plain device copy),
@@ -54,8 +64,7 @@ def measured_traffic(workload, kernel):
     if not m:
         return None
     info = json.loads(m.group(1))
-    src = os.path.join(ROOT, "paper_2102_02888_amd", "csrc", "onebit_kernels.hip")
-    if hashlib.sha256(open(src, "rb").read()).hexdigest() != info.get("kernels_source_sha256"):
+    if kernels_source_sha256() != info.get("kernels_source_sha256"):
         return None
     k = info["kernels"].get(kernel)
     return None if k is None else k["traffic_bytes"]
