@@ -100,6 +100,18 @@ def _oracle_segment(sd, wl):
     oracle.update_segment(0, ln, sd["sbits"], s, wl.lr, wl.eps, sd["x"], sd["m"], sd["v"])
 
 
+def _cpu_model():
+    """The host CPU's model name from /proc/cpuinfo, or None."""
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return None
+
+
 def cpu_baseline(st, plan, wl, target_s=10.0, threads=None, threaded_s=6.0):
     """Times the oracle on the host cores over whole segments of the
     workload (each segment: every worker's pass, the owner's average and
@@ -169,6 +181,7 @@ def cpu_baseline(st, plan, wl, target_s=10.0, threads=None, threaded_s=6.0):
         th.join()
     wall = time.perf_counter() - t0
     return {"value": sum(counts) / wall, "unit": "params/s", "cores": threads, "kind": "oracle",
+            "cpu_model": _cpu_model(),
             "sample": "%d threads looping over chunk 0 (%d segment(s), %d params, in %d "
                       "pieces of at most %d; all %d workers' passes, the chunk owner's average "
                       "and recompression, and the update) for %.1f s: %d params"

@@ -43,3 +43,8 @@ def test_multi_gpu_request_is_refused():
     r = subprocess.run([sys.executable, os.path.join(root, "bench.py"), "--gpus", "2"],
                        capture_output=True, text=True, timeout=120)
     assert r.returncode == 2 and "one GPU" in r.stderr
+
+
+def test_cpu_model_is_named():
+    name = bench._cpu_model()
+    assert name is None or (isinstance(name, str) and name)
