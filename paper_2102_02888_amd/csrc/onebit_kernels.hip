@@ -169,6 +169,18 @@ __device__ __forceinline__ double wave_sum_dpp(double a)
     return __hiloint2double(hi, lo);
 }
 
+// Workgroups are dispatched to the chip's 8 XCDs round-robin (block b runs on
+// XCD (b + c) % 8 for a fixed c), and each XCD has its own L2.  Grids are
+// launched as multiples of 8 blocks and renumbered so that each XCD takes one
+// contiguous eighth of the logical blocks: every XCD then streams its own
+// address range instead of all eight interleaving 128-byte pieces of one.
+constexpr int kXcds = 8;
+__device__ __forceinline__ int64_t xcd_block()
+{
+    const int64_t per = gridDim.x / kXcds;
+    return (int64_t)(blockIdx.x % kXcds) * per + blockIdx.x / kXcds;
+}
+
 // Error from the compensated form: z - C[z] given z and its segment scale s.
 __device__ __forceinline__ float error_of(float z, float s) { return z >= 0.f ? z - s : z + s; }
 
@@ -299,7 +311,7 @@ __global__ __launch_bounds__(kBlock) void k_adam_message(
     int use_bc, float bc1, float bc2)
 {
     const int lane = threadIdx.x & (kWave - 1);
-    const int64_t t = (int64_t)blockIdx.x * kWavesPerBlock + (threadIdx.x >> 6);
+    const int64_t t = xcd_block() * kWavesPerBlock + (threadIdx.x >> 6);
     if (t >= num_tiles) return;
     const Tile tile = tiles[t];
     const float s = scales[tile.seg];
@@ -378,7 +390,7 @@ __global__ __launch_bounds__(kBlock) void k_uncompressed(
     int64_t g_ld, int n, float lr, float beta1, float omb1, float eps)
 {
     const int lane = threadIdx.x & (kWave - 1);
-    const int64_t t = (int64_t)blockIdx.x * kWavesPerBlock + (threadIdx.x >> 6);
+    const int64_t t = xcd_block() * kWavesPerBlock + (threadIdx.x >> 6);
     if (t >= num_tiles) return;
     const Tile tile = tiles[t];
     if (tile.len == kTileElems)
@@ -395,7 +407,7 @@ __global__ __launch_bounds__(kBlock) void k_warmup(
     int use_bc, float bc1, float bc2)
 {
     const int lane = threadIdx.x & (kWave - 1);
-    const int64_t t = (int64_t)blockIdx.x * kWavesPerBlock + (threadIdx.x >> 6);
+    const int64_t t = xcd_block() * kWavesPerBlock + (threadIdx.x >> 6);
     if (t >= num_tiles) return;
     const Tile tile = tiles[t];
     if (tile.len == kTileElems)
@@ -411,12 +423,13 @@ __global__ __launch_bounds__(kBlock) void k_warmup(
 // sign words of z_i, per-tile partial sum of z_i^2, and z_i written back as the
 // new compensated error state.
 //
-// A wave handles one tile for a group of consecutive workers, and the grid
-// runs group-major: all waves in flight work on the same few worker rows, so
-// the chip streams through 2 x group rows of (g, error state) at a time
-// instead of all 2n.  With one worker per group the momentum of a tile is
-// re-derived by every worker; in packed form that is 1/8 byte per element per
-// worker from a sign array small enough to stay in the last-level cache.
+// A wave handles one tile for a group of consecutive workers, and the items
+// run group-major, split into one contiguous eighth per XCD: the waves in
+// flight on an XCD work on the same few worker rows, so each XCD streams
+// through 2 x group rows of (g, error state) at a time instead of all 2n.
+// With one worker per group the momentum of a tile is re-derived by every
+// worker; in packed form that is 1/8 byte per element per worker from a sign
+// array small enough to stay in the last-level cache.
 // ---------------------------------------------------------------------------
 // The shared momentum m_{t-1} of the tile times beta1.  PACKED: m_{t-1} is
 // the previous step's gathered server message, decoded from its sign words
@@ -512,9 +525,15 @@ __global__ __launch_bounds__(kWorkerBlock) void k_worker_pass(
     float beta1, float omb1)
 {
     const int lane = threadIdx.x & (kWave - 1);
-    const int64_t stride = (int64_t)gridDim.x * kWorkerWavesPerBlock;
-    for (int64_t item = (int64_t)blockIdx.x * kWorkerWavesPerBlock + (threadIdx.x >> 6);
-         item < num_items; item += stride) {
+    // each XCD walks one contiguous eighth of the items (a grid smaller than
+    // the item count strides within that eighth)
+    const int64_t per_xcd = (num_items + kXcds - 1) / kXcds;
+    const int64_t begin = (int64_t)(blockIdx.x % kXcds) * per_xcd;
+    const int64_t end = min(num_items, begin + per_xcd);
+    const int64_t stride = (int64_t)(gridDim.x / kXcds) * kWorkerWavesPerBlock;
+    for (int64_t item = begin + (int64_t)(blockIdx.x / kXcds) * kWorkerWavesPerBlock +
+                        (threadIdx.x >> 6);
+         item < end; item += stride) {
         const int64_t grp = item / num_tiles;
         const int64_t t = item - grp * num_tiles;
         const int i0 = (int)grp * group;
@@ -728,7 +747,7 @@ __global__ __launch_bounds__(kBlock) void k_server_pass(
     __shared__ float s_scale[kWavesPerBlock][kServerRowBatch];
     const int lane = threadIdx.x & (kWave - 1);
     const int wv = threadIdx.x >> 6;
-    const int64_t rel = (int64_t)blockIdx.x * kWavesPerBlock + wv;
+    const int64_t rel = xcd_block() * kWavesPerBlock + wv;
     if (rel >= tile_count) return;
     const int64_t t = chunk_tiles[tile_begin + rel];
     const Tile tile = tiles[t];
@@ -980,7 +999,7 @@ __global__ __launch_bounds__(kBlock) void k_update(
     const float *__restrict__ v, float lr, float eps)
 {
     const int lane = threadIdx.x & (kWave - 1);
-    const int64_t t = (int64_t)blockIdx.x * kWavesPerBlock + (threadIdx.x >> 6);
+    const int64_t t = xcd_block() * kWavesPerBlock + (threadIdx.x >> 6);
     if (t >= num_tiles) return;
     const Tile tile = tiles[t];
     const float s = sscales[tile.seg];
@@ -997,7 +1016,7 @@ __global__ __launch_bounds__(kBlock) void k_materialize(
     int64_t out_ld)
 {
     const int lane = threadIdx.x & (kWave - 1);
-    const int64_t t = (int64_t)blockIdx.x * kWavesPerBlock + (threadIdx.x >> 6);
+    const int64_t t = xcd_block() * kWavesPerBlock + (threadIdx.x >> 6);
     if (t >= num_tiles) return;
     const Tile tile = tiles[t];
     const int len = tile.len;
@@ -1050,7 +1069,7 @@ __global__ __launch_bounds__(kBlock) void k_decode(const Tile *__restrict__ tile
                                                    float *__restrict__ out)
 {
     const int lane = threadIdx.x & (kWave - 1);
-    const int64_t t = (int64_t)blockIdx.x * kWavesPerBlock + (threadIdx.x >> 6);
+    const int64_t t = xcd_block() * kWavesPerBlock + (threadIdx.x >> 6);
     if (t >= num_tiles) return;
     const Tile tile = tiles[t];
     const float s = scales[tile.seg];
@@ -1085,7 +1104,7 @@ __global__ __launch_bounds__(kBlock) void k_l1_partial(const Tile *__restrict__ 
                                                        double *__restrict__ partial)
 {
     const int lane = threadIdx.x & (kWave - 1);
-    const int64_t t = (int64_t)blockIdx.x * kWavesPerBlock + (threadIdx.x >> 6);
+    const int64_t t = xcd_block() * kWavesPerBlock + (threadIdx.x >> 6);
     if (t >= num_tiles) return;
     const Tile tile = tiles[t];
     double acc = tile.len == kTileElems ? l1_tile<true>(tile, lane, v) : l1_tile<false>(tile, lane, v);
@@ -1110,10 +1129,13 @@ __global__ __launch_bounds__(kBlock) void k_l1_final(const double *__restrict__ 
 // kernels over larger item counts cap their grid and stride.
 inline int64_t blocks_for(int64_t waves)
 {
-    return (waves + kWavesPerBlock - 1) / kWavesPerBlock;
+    return ((waves + kWavesPerBlock - 1) / kWavesPerBlock + kXcds - 1) / kXcds * kXcds;
 }
 
 constexpr int64_t kMaxGridBlocks = 1 << 22;
+// The worker grid (128-thread blocks) may reach 2^24 blocks, 2^31 threads,
+// so that a BERT-Large-sized pass (n = 32) runs one item per wave.
+constexpr int64_t kMaxWorkerGridBlocks = 1 << 24;
 
 }  // namespace
 
@@ -1159,7 +1181,8 @@ static void launch_worker_t(const DeviceTables &tb, int64_t num_tiles, const flo
     const int64_t groups = (n_local + group - 1) / group;
     const int64_t items = groups * num_tiles;
     const int64_t blocks =
-        std::min((items + kWorkerWavesPerBlock - 1) / kWorkerWavesPerBlock, kMaxGridBlocks);
+        (std::min((items + kWorkerWavesPerBlock - 1) / kWorkerWavesPerBlock, kMaxWorkerGridBlocks) +
+         kXcds - 1) / kXcds * kXcds;
     hipLaunchKernelGGL((k_worker_pass<PACKED, G>), dim3((unsigned)blocks), dim3(kWorkerBlock), 0, s,
                        tb.tiles, num_tiles, m, m_bits, m_scales, (const typename G::T *)g, g_ld,
                        err, err_ld, scales, scales_ld, bits, bits_ld, partial, n_local, group,
