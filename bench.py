@@ -40,12 +40,16 @@ def algorithmic_bytes_per_param(n, grad_bytes=4):
     return worker, server, update
 
 
+# The sources that decide what the kernels touch: the kernels, the plan (tile)
+# construction, the shared constants and the launch shapes.
+KERNEL_SOURCES = ("onebit_kernels.hip", "onebit_abi.hip", "onebit_internal.h", "onebit_grid.h")
+
+
 def kernels_source_sha256():
-    """Digest of the sources that decide what the kernels touch: the kernels
-    and the plan (tile) construction."""
+    """Digest of KERNEL_SOURCES, in that order."""
     import hashlib
     h = hashlib.sha256()
-    for f in ("onebit_kernels.hip", "onebit_abi.hip"):
+    for f in KERNEL_SOURCES:
         h.update(open(os.path.join(ROOT, "paper_2102_02888_amd", "csrc", f), "rb").read())
     return h.hexdigest()
 

@@ -1,0 +1,85 @@
+// Launch shapes of the tile kernels and the order in which their waves take
+// work.  Integer arithmetic only, with no HIP dependency, so that a host
+// program can enumerate a whole launch and check that every tile or item is
+// taken by exactly one wave.
+#pragma once
+
+#include <stdint.h>
+
+#if defined(__HIPCC__)
+#define ONEBIT_HD __host__ __device__
+#else
+#define ONEBIT_HD
+#endif
+
+namespace onebit {
+
+constexpr int kWave = 64;
+constexpr int kWavesPerBlock = 4;
+constexpr int kBlock = kWave * kWavesPerBlock;
+// The worker pass runs smaller workgroups (measured ~2% faster than 4 waves).
+constexpr int kWorkerWavesPerBlock = 2;
+constexpr int kWorkerBlock = kWave * kWorkerWavesPerBlock;
+
+// Workgroups are dispatched to the chip's 8 XCDs round-robin (block b runs on
+// XCD (b + c) % 8 for a fixed c), and each XCD has its own L2.  Grids are
+// launched as multiples of 8 blocks and renumbered so that each XCD takes one
+// contiguous eighth of the work: every XCD then streams its own address range
+// instead of all eight interleaving pieces of the same streams.
+constexpr int kXcds = 8;
+
+// Plans keep the tile count below 2^25, so a grid of one wave per tile stays
+// far below the 2^32 work-item limit.  Kernels over larger pair counts cap
+// their grid at kMaxGridBlocks and stride.  The worker grid (128-thread
+// blocks) may reach 2^24 blocks, 2^31 work-items, so that a BERT-Large-sized
+// pass (n = 32) runs one item per wave.
+constexpr int64_t kMaxGridBlocks = (int64_t)1 << 22;
+constexpr int64_t kMaxWorkerGridBlocks = (int64_t)1 << 24;
+
+// Blocks for one wave per item at waves_per_block waves per block, rounded up
+// to a multiple of kXcds (0 for no items).
+ONEBIT_HD inline int64_t xcd_grid(int64_t waves, int waves_per_block)
+{
+    const int64_t blocks = (waves + waves_per_block - 1) / waves_per_block;
+    return (blocks + kXcds - 1) / kXcds * kXcds;
+}
+
+// Logical block of physical block b in a grid of `grid` blocks (a multiple of
+// kXcds): the blocks of XCD x are logical blocks [x, x + 1) * grid / kXcds.
+ONEBIT_HD inline int64_t xcd_block_of(int64_t b, int64_t grid)
+{
+    return (b % kXcds) * (grid / kXcds) + b / kXcds;
+}
+
+// Worker pass: items [0, num_items) are cut into kXcds contiguous ranges and
+// XCD x walks range x with its grid / kXcds blocks; a grid smaller than the
+// item count strides within the range.  Wave w of physical block b takes
+// items first, first + stride, ... below end.
+struct ItemWalk {
+    int64_t first;
+    int64_t end;
+    int64_t stride;
+};
+
+ONEBIT_HD inline ItemWalk xcd_item_walk(int64_t b, int64_t grid, int w, int waves_per_block,
+                                        int64_t num_items)
+{
+    const int64_t per_xcd = (num_items + kXcds - 1) / kXcds;
+    const int64_t begin = (b % kXcds) * per_xcd;
+    ItemWalk r;
+    r.first = begin + (b / kXcds) * waves_per_block + w;
+    r.end = begin + per_xcd < num_items ? begin + per_xcd : num_items;
+    r.stride = (grid / kXcds) * waves_per_block;
+    return r;
+}
+
+// Worker grid: one wave per item, at most max_blocks blocks, rounded up to a
+// multiple of kXcds.
+ONEBIT_HD inline int64_t worker_grid(int64_t items, int waves_per_block, int64_t max_blocks)
+{
+    int64_t blocks = (items + waves_per_block - 1) / waves_per_block;
+    if (blocks > max_blocks) blocks = max_blocks;
+    return (blocks + kXcds - 1) / kXcds * kXcds;
+}
+
+}  // namespace onebit

@@ -4,6 +4,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "onebit_grid.h"
+
 namespace onebit {
 
 // A unit of work: up to kTileElems consecutive elements of one segment,
@@ -15,12 +17,6 @@ struct Tile {
     int32_t seg;    // segment q = k*n + j
 };
 
-constexpr int kWave = 64;
-constexpr int kWavesPerBlock = 4;
-constexpr int kBlock = kWave * kWavesPerBlock;
-// The worker pass runs smaller workgroups (measured ~2% faster than 4 waves).
-constexpr int kWorkerWavesPerBlock = 2;
-constexpr int kWorkerBlock = kWave * kWorkerWavesPerBlock;
 constexpr int kSubBlocks = 4;                       // float4 loads per lane per array
 constexpr int kTileElems = kWave * 4 * kSubBlocks;  // 1024 elements = 16 sign words
 constexpr int kTileWords = kTileElems / 64;

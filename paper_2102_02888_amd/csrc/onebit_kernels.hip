@@ -169,17 +169,9 @@ __device__ __forceinline__ double wave_sum_dpp(double a)
     return __hiloint2double(hi, lo);
 }
 
-// Workgroups are dispatched to the chip's 8 XCDs round-robin (block b runs on
-// XCD (b + c) % 8 for a fixed c), and each XCD has its own L2.  Grids are
-// launched as multiples of 8 blocks and renumbered so that each XCD takes one
-// contiguous eighth of the logical blocks: every XCD then streams its own
-// address range instead of all eight interleaving 128-byte pieces of one.
-constexpr int kXcds = 8;
-__device__ __forceinline__ int64_t xcd_block()
-{
-    const int64_t per = gridDim.x / kXcds;
-    return (int64_t)(blockIdx.x % kXcds) * per + blockIdx.x / kXcds;
-}
+// This block's logical number in a grid launched by xcd_grid (one contiguous
+// eighth of the logical blocks per XCD).
+__device__ __forceinline__ int64_t xcd_block() { return xcd_block_of(blockIdx.x, gridDim.x); }
 
 // Error from the compensated form: z - C[z] given z and its segment scale s.
 __device__ __forceinline__ float error_of(float z, float s) { return z >= 0.f ? z - s : z + s; }
@@ -525,15 +517,10 @@ __global__ __launch_bounds__(kWorkerBlock) void k_worker_pass(
     float beta1, float omb1)
 {
     const int lane = threadIdx.x & (kWave - 1);
-    // each XCD walks one contiguous eighth of the items (a grid smaller than
-    // the item count strides within that eighth)
-    const int64_t per_xcd = (num_items + kXcds - 1) / kXcds;
-    const int64_t begin = (int64_t)(blockIdx.x % kXcds) * per_xcd;
-    const int64_t end = min(num_items, begin + per_xcd);
-    const int64_t stride = (int64_t)(gridDim.x / kXcds) * kWorkerWavesPerBlock;
-    for (int64_t item = begin + (int64_t)(blockIdx.x / kXcds) * kWorkerWavesPerBlock +
-                        (threadIdx.x >> 6);
-         item < end; item += stride) {
+    // each XCD walks one contiguous eighth of the items
+    const ItemWalk walk = xcd_item_walk(blockIdx.x, gridDim.x, threadIdx.x >> 6,
+                                        kWorkerWavesPerBlock, num_items);
+    for (int64_t item = walk.first; item < walk.end; item += walk.stride) {
         const int64_t grp = item / num_tiles;
         const int64_t t = item - grp * num_tiles;
         const int i0 = (int)grp * group;
@@ -1124,18 +1111,8 @@ __global__ __launch_bounds__(kBlock) void k_l1_final(const double *__restrict__ 
     if (threadIdx.x == 0) out[0] = ((red[0] + red[1]) + red[2]) + red[3];
 }
 
-// Workgroups for one wave per item.  Plans keep the tile count below 2^25, so
-// a grid of one wave per tile stays far below the 2^32 work-item limit;
-// kernels over larger item counts cap their grid and stride.
-inline int64_t blocks_for(int64_t waves)
-{
-    return ((waves + kWavesPerBlock - 1) / kWavesPerBlock + kXcds - 1) / kXcds * kXcds;
-}
-
-constexpr int64_t kMaxGridBlocks = 1 << 22;
-// The worker grid (128-thread blocks) may reach 2^24 blocks, 2^31 threads,
-// so that a BERT-Large-sized pass (n = 32) runs one item per wave.
-constexpr int64_t kMaxWorkerGridBlocks = 1 << 24;
+// Workgroups (of kWavesPerBlock waves) for one wave per item.
+inline int64_t blocks_for(int64_t waves) { return xcd_grid(waves, kWavesPerBlock); }
 
 }  // namespace
 
@@ -1180,9 +1157,7 @@ static void launch_worker_t(const DeviceTables &tb, int64_t num_tiles, const flo
     const float omb1 = 1.0f - beta1;
     const int64_t groups = (n_local + group - 1) / group;
     const int64_t items = groups * num_tiles;
-    const int64_t blocks =
-        (std::min((items + kWorkerWavesPerBlock - 1) / kWorkerWavesPerBlock, kMaxWorkerGridBlocks) +
-         kXcds - 1) / kXcds * kXcds;
+    const int64_t blocks = worker_grid(items, kWorkerWavesPerBlock, kMaxWorkerGridBlocks);
     hipLaunchKernelGGL((k_worker_pass<PACKED, G>), dim3((unsigned)blocks), dim3(kWorkerBlock), 0, s,
                        tb.tiles, num_tiles, m, m_bits, m_scales, (const typename G::T *)g, g_ld,
                        err, err_ld, scales, scales_ld, bits, bits_ld, partial, n_local, group,

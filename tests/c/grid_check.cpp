@@ -1,0 +1,90 @@
+// Enumerates launches of the tile kernels on the host, with the same grid
+// functions the kernels and their launchers use, and checks that every tile
+// (one wave per tile) or worker item (XCD-contiguous walk, possibly strided)
+// is taken by exactly one wave.  Exit status 0 when every case passes.
+#include "onebit_grid.h"
+
+#include <cstdio>
+#include <vector>
+
+using namespace onebit;
+
+static int failures = 0;
+static long cases = 0;
+
+static void fail(const char *what, long long a, long long b)
+{
+    if (failures < 20) std::printf("FAIL %s (%lld, %lld)\n", what, a, b);
+    ++failures;
+}
+
+// One wave per tile, kWavesPerBlock waves per block, logical block order.
+static void check_tiles(int64_t tiles)
+{
+    ++cases;
+    const int64_t grid = xcd_grid(tiles, kWavesPerBlock);
+    if (grid % kXcds) fail("tile grid not a multiple of the XCD count", tiles, grid);
+    if (grid * kWavesPerBlock < tiles) fail("tile grid too small", tiles, grid);
+    std::vector<unsigned char> seen((size_t)tiles, 0);
+    std::vector<unsigned char> lseen((size_t)grid, 0);
+    for (int64_t b = 0; b < grid; ++b) {
+        const int64_t lb = xcd_block_of(b, grid);
+        if (lb < 0 || lb >= grid) { fail("logical block out of range", b, grid); continue; }
+        if (lseen[(size_t)lb]++) fail("logical block taken twice", lb, grid);
+        for (int w = 0; w < kWavesPerBlock; ++w) {
+            const int64_t t = lb * kWavesPerBlock + w;
+            if (t < tiles && seen[(size_t)t]++) fail("tile taken twice", t, tiles);
+        }
+    }
+    for (int64_t t = 0; t < tiles; ++t)
+        if (!seen[(size_t)t]) fail("tile not taken", t, tiles);
+}
+
+// The worker pass: items walked per XCD with a grid capped at max_blocks.
+static void check_worker(int64_t items, int64_t max_blocks)
+{
+    ++cases;
+    const int64_t grid = worker_grid(items, kWorkerWavesPerBlock, max_blocks);
+    if (grid % kXcds) fail("worker grid not a multiple of the XCD count", items, grid);
+    if (grid > max_blocks + kXcds - 1) fail("worker grid above its cap", items, grid);
+    std::vector<unsigned char> seen((size_t)items, 0);
+    for (int64_t b = 0; b < grid; ++b) {
+        for (int w = 0; w < kWorkerWavesPerBlock; ++w) {
+            const ItemWalk walk = xcd_item_walk(b, grid, w, kWorkerWavesPerBlock, items);
+            if (walk.stride <= 0) { fail("non-positive stride", items, grid); return; }
+            for (int64_t i = walk.first; i < walk.end; i += walk.stride) {
+                if (i < 0 || i >= items) { fail("item out of range", i, items); break; }
+                if (seen[(size_t)i]++) fail("item taken twice", i, items);
+            }
+        }
+    }
+    for (int64_t i = 0; i < items; ++i)
+        if (!seen[(size_t)i]) { fail("item not taken", i, items); break; }
+}
+
+int main()
+{
+    for (int64_t t = 1; t <= 600; ++t) check_tiles(t);
+    // BERT-Large (326,288 tiles) and the stress workload's tile counts
+    for (int64_t t : {326288LL, 542089LL, 106344LL, 1275LL}) check_tiles(t);
+
+    for (int64_t items = 1; items <= 700; ++items)
+        for (int64_t cap : {1LL, 3LL, 8LL, 9LL, 24LL, 64LL, (long long)kMaxWorkerGridBlocks})
+            check_worker(items, cap);
+    // BERT-Large, n = 32: one item per wave under the real cap, and strided
+    // walks under smaller caps (including the former 2^22-block cap)
+    const int64_t bert = 32LL * 326288;
+    for (int64_t cap : {(long long)kMaxWorkerGridBlocks, (long long)kMaxGridBlocks, 1000003LL, 4096LL})
+        check_worker(bert, cap);
+    // item counts whose eighths are ragged
+    for (int64_t items : {8LL * 1000 + 7, 8LL * 1000 + 1, 123457LL})
+        for (int64_t cap : {5LL, 40LL, 1000LL})
+            check_worker(items, cap);
+
+    if (failures) {
+        std::printf("grid_check: %d failure(s) in %ld cases\n", failures, cases);
+        return 1;
+    }
+    std::printf("grid_check: ok (%ld cases)\n", cases);
+    return 0;
+}

@@ -21,10 +21,10 @@ def test_measured_traffic_requires_matching_kernel_source(tmp_path, monkeypatch)
     prof.mkdir()
     src = tmp_path / "paper_2102_02888_amd" / "csrc"
     src.mkdir(parents=True)
-    (src / "onebit_kernels.hip").write_text("// kernels v1\n")
-    (src / "onebit_abi.hip").write_text("// plans v1\n")
+    for f in bench.KERNEL_SOURCES:
+        (src / f).write_text("// %s v1\n" % f)
     import hashlib
-    sha = hashlib.sha256(b"// kernels v1\n// plans v1\n").hexdigest()
+    sha = hashlib.sha256("".join("// %s v1\n" % f for f in bench.KERNEL_SOURCES).encode()).hexdigest()
     info = {"kernels_source_sha256": sha,
             "kernels": {"k_update": {"traffic_bytes": 123.0}}}
     (prof / "pmc_traffic_w.md").write_text("x\n```json\n%s\n```\n" % json.dumps(info))
@@ -32,7 +32,7 @@ def test_measured_traffic_requires_matching_kernel_source(tmp_path, monkeypatch)
     assert bench.measured_traffic("w", "k_update") == 123.0
     assert bench.measured_traffic("w", "k_other") is None
     assert bench.measured_traffic("missing", "k_update") is None
-    (src / "onebit_abi.hip").write_text("// plans v2\n")
+    (src / "onebit_grid.h").write_text("// launch shapes v2\n")
     assert bench.measured_traffic("w", "k_update") is None
 
 
