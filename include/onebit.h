@@ -94,8 +94,9 @@ typedef struct {
 /* Creates a plan for K = num_tensors tensors (tensor_numel[k] >= 0, host
  * array) and n = n_workers >= 1 workers on the current HIP device.  The plan
  * owns small device tables (tiles, segments); *out receives the handle.
- * Errors: EINVAL (null, K < 1, n < 1, negative numel, D >= 2^40, 2^25 or
- * more tiles, more than 2^31 - 1 segments), ENOMEM, EHIP. */
+ * Errors: EINVAL (null, K < 1, n < 1, a numel below 0 or above 2^40,
+ * D >= 2^40, 2^25 or more tiles, more than 2^31 - 1 segments), ENOMEM,
+ * EHIP. */
 int onebit_plan_create(const int64_t *tensor_numel, int32_t num_tensors,
                        int32_t n_workers, onebit_plan *out);
 

@@ -293,8 +293,12 @@ int onebit_plan_create(const int64_t *tensor_numel, int32_t num_tensors, int32_t
     if (!tensor_numel) return fail(ONEBIT_EINVAL, "tensor_numel is NULL");
     if (num_tensors < 1) return fail(ONEBIT_EINVAL, "num_tensors < 1");
     if (n_workers < 1) return fail(ONEBIT_EINVAL, "n_workers < 1");
-    for (int32_t k = 0; k < num_tensors; ++k)
+    for (int32_t k = 0; k < num_tensors; ++k) {
         if (tensor_numel[k] < 0) return fail(ONEBIT_EINVAL, "tensor_numel[%d] < 0", k);
+        // bounds the layout arithmetic (the padded total is limited to 2^40 below)
+        if (tensor_numel[k] > ((int64_t)1 << 40))
+            return fail(ONEBIT_EINVAL, "tensor_numel[%d] exceeds 2^40", k);
+    }
     if ((int64_t)num_tensors * n_workers > INT32_MAX)
         return fail(ONEBIT_EINVAL, "num_tensors * n_workers = %lld segments exceeds 2^31 - 1",
                     (long long)num_tensors * n_workers);

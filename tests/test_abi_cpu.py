@@ -70,6 +70,10 @@ def test_argument_errors_before_device(native):
     bad = (ctypes.c_int64 * 2)(10, -1)
     assert lib.onebit_plan_create(bad, 2, 4, ctypes.byref(out)) == -1
     assert b"tensor_numel[1]" in lib.onebit_last_error()
+    # sizes that would overflow the layout arithmetic are refused up front
+    huge = (ctypes.c_int64 * 2)(10, (1 << 63) - 1)
+    assert lib.onebit_plan_create(huge, 2, 4, ctypes.byref(out)) == -1
+    assert b"tensor_numel[1] exceeds" in lib.onebit_last_error()
     # K * n segments must fit in int32; refused before any device call
     many = (ctypes.c_int64 * (1 << 20))()
     assert lib.onebit_plan_create(many, 1 << 20, 1 << 12, ctypes.byref(out)) == -1
