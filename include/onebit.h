@@ -3,7 +3,7 @@
  *
  * Method: Tang et al., "1-bit Adam: Communication Efficient Large-Scale
  * Training with Adam's Convergence Speed" (arXiv 2102.02888).  Warm-up runs
- * original Adam (eq. (alg:v), Section 3.2); the compression stage freezes the
+ * original Adam (eq. (alg:v), Section 3.3); the compression stage freezes the
  * variance and runs error-compensated 1-bit compressed momentum SGD
  * (Algorithm 1, Section 4.3) whose averaging is the three-phase "compressed
  * allreduce" of Section 6 / Figure "allreduce" (all-to-all of chunks, average
@@ -120,7 +120,7 @@ int onebit_plan_info(onebit_plan plan, int64_t *padded_len, int64_t *words,
                      size_t *workspace_bytes);
 
 /* Warm-up step: original Adam on the data-parallel average gradient
- * (eq. (alg:v), Section 3.2; Algorithm 1's warm-up stage):
+ * (eq. (alg:v), Section 3.3; Algorithm 1's warm-up stage):
  *   g = (1/n_grads) sum_i grads[i]      (fp64 sum in row order, one rounding)
  *   m = beta1 m + (1-beta1) g ;  v = beta2 v + (1-beta2) g*g
  *   x = x - lr * m_hat / (sqrt(v_hat) + eps)

@@ -138,7 +138,7 @@ void orc_decode_range(int64_t b, int64_t e, const uint64_t *bits, float scale, f
 }
 
 /* ------------------------------------------------------------------------ */
-/* Warm-up: original Adam, eq. (alg:v) of Section 3.2, on the averaged      */
+/* Warm-up: original Adam, eq. (alg:v) of Section 3.3, on the averaged      */
 /* data-parallel gradient (problem statement (main)).  The paper disables   */
 /* bias correction; bias_correction != 0 gives the textbook Kingma-Ba form. */
 /* Works on elements [b, e).  g has n rows of stride g_ld.                   */
