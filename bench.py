@@ -471,6 +471,9 @@ def main():
         "gpu_step_ms": {"median": per_step[len(per_step) // 2], "min": per_step[0],
                         "max": per_step[-1]},
         "warmup_adam_step_ms": warm_avg,
+        "warmup_step_ms": ({"median": sorted(warm_ms[1:])[(len(warm_ms) - 1) // 2],
+                            "min": min(warm_ms[1:]), "max": max(warm_ms[1:])}
+                           if len(warm_ms) > 1 else None),
         "roofline": {"bound": "hbm",
                      "kernel": "worker_compress (k_worker_pass<true, %s>: packed momentum, %s "
                                "gradients)" % (gname, args.grad_dtype),
