@@ -352,6 +352,8 @@ def main():
                          "'1-bit Adam (32-bits)' (uncompressed) or 'Adam(1-bit Naive)'")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-probe", action="store_true")
+    ap.add_argument("--graph", action="store_true",
+                    help="also time the step replayed from a captured HIP graph")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures one GPU: the compressed exchange is simulated in one GPU's "
@@ -435,6 +437,24 @@ def main():
                for j in range(3)]
     gpu_step_ms = sum(part_ms)
     per_step = sorted(ev[0].elapsed_time(ev[3]) for ev in events)
+    graph_ms = None
+    if args.graph:
+        # the same packed-momentum step captured once and replayed: one launch
+        # per step instead of five (worker, scales, owners, scales, update)
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            one_step()
+        for _ in range(args.warmup):
+            graph.replay()
+        gev = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(args.steps)]
+        torch.cuda.synchronize()
+        for k in range(args.steps):
+            gev[k][0].record()
+            graph.replay()
+            gev[k][1].record()
+        torch.cuda.synchronize()
+        gt = sorted(a.elapsed_time(b) for a, b in gev)
+        graph_ms = {"median": gt[len(gt) // 2], "min": gt[0], "max": gt[-1]}
 
     bw, bs, bu = algorithmic_bytes_per_param(n, gbytes)
     gname = {"f32": "GradF32", "bf16": "GradBF16", "f16": "GradF16"}[args.grad_dtype]
@@ -471,6 +491,7 @@ def main():
         "gpu_step_ms": {"median": per_step[len(per_step) // 2], "min": per_step[0],
                         "max": per_step[-1]},
         "warmup_adam_step_ms": warm_avg,
+        "graph_step_ms": graph_ms,
         "warmup_step_ms": ({"median": sorted(warm_ms[1:])[(len(warm_ms) - 1) // 2],
                             "min": min(warm_ms[1:]), "max": max(warm_ms[1:])}
                            if len(warm_ms) > 1 else None),

@@ -95,3 +95,40 @@ def test_auto_freeze_driver(dev):
                 break
     assert ref_freeze is not None and opt.frozen_at == ref_freeze > 40
     plan.close()
+
+
+@pytest.mark.gpu
+def test_graph_replay_matches_eager(dev):
+    """graph=True replays a captured compressed step; after every step its
+    state equals the eager driver's bit for bit, through an lr change (a new
+    capture), with eager work and a host synchronisation between replays."""
+    import paper_2102_02888_amd as ob
+    wl = synth.Workload(name="graph", numel=[50_000, 900, 64], n=4, warmup_steps=2, steps=6)
+    plan = ob.Plan(wl.numel, wl.n)
+    eager = ob.OnebitAdam(plan, dev, wl.lr, wl.beta1, wl.beta2, wl.eps,
+                          warmup_steps=wl.warmup_steps)
+    graphed = ob.OnebitAdam(plan, dev, wl.lr, wl.beta1, wl.beta2, wl.eps,
+                            warmup_steps=wl.warmup_steps, graph=True)
+    x0 = torch.from_numpy(synth.host_params(wl, plan.D)).to(dev)
+    eager.x.copy_(x0)
+    graphed.x.copy_(x0)
+    names = ("x", "worker_err", "worker_bits", "worker_scales", "server_err", "server_bits",
+             "server_scales")
+    captured = []
+    for t in range(1, wl.warmup_steps + wl.steps + 1):
+        g = torch.from_numpy(synth.host_grads(wl, plan.D, plan.tensor_off, t)).to(dev)
+        lr = wl.lr if t < 6 else wl.lr * 0.5
+        for opt in (eager, graphed):
+            opt.grads.copy_(g)
+            opt.step(lr=lr)
+        captured.append(graphed._graph)
+        torch.cuda.synchronize()
+        for name in names:
+            a, b = host(getattr(eager.state, name)), host(getattr(graphed.state, name))
+            assert a.tobytes() == b.tobytes(), (t, name)
+    # warm-up and the first compression step run eagerly; steps 4-5 replay one
+    # graph, and the lr change at step 6 captures another
+    assert captured[:3] == [None, None, None]
+    assert captured[3] is not None and captured[4] is captured[3]
+    assert captured[5] is not captured[4] and captured[7] is captured[5]
+    plan.close()
