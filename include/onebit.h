@@ -49,10 +49,11 @@
  *   buffer of that call except where "in/out" says so.
  * Streams.  Every call is asynchronous on `stream` (0 = the null stream).  A
  *   plan may be used from several streams if each has its own workspace.
- * Graphs.  A call issues only kernel launches on `stream` (no memset, copy,
- *   allocation or host synchronisation), so a call or a sequence of calls
- *   may be captured into a HIP graph and replayed; the graph keeps the
- *   pointers and scalar arguments given at capture.
+ * Graphs.  Every call that takes a stream issues only kernel launches on it
+ *   (no memset, copy, allocation or host synchronisation), so such a call or
+ *   a sequence of them may be captured into a HIP graph and replayed; the
+ *   graph keeps the pointers and scalar arguments given at capture.  Plan
+ *   creation and destruction allocate and copy, and are not captured.
  * Errors.  Every function returns ONEBIT_OK (0) or a negative status; on an
  *   error nothing is launched and no buffer is written.  onebit_status_str()
  *   names a status and onebit_last_error() describes the last failure of the
