@@ -21,6 +21,11 @@ constexpr int kBlock = kWave * kWavesPerBlock;
 constexpr int kWorkerWavesPerBlock = 2;
 constexpr int kWorkerBlock = kWave * kWorkerWavesPerBlock;
 
+// The kernels that sum the n gradient rows of each tile (warm-up, the 32-bit
+// comparison step) run 16-wave workgroups over 16 consecutive tiles.
+constexpr int kRowWaves = 16;
+constexpr int kRowBlock = kWave * kRowWaves;
+
 // Workgroups are dispatched to the chip's 8 XCDs round-robin (block b runs on
 // XCD (b + c) % 8 for a fixed c), and each XCD has its own L2.  Grids are
 // launched as multiples of 8 blocks and renumbered so that each XCD takes one

@@ -178,32 +178,36 @@ __device__ __forceinline__ float error_of(float z, float s) { return z >= 0.f ? 
 
 // ---------------------------------------------------------------------------
 // Warm-up Adam (eq. (alg:v)) on the average of n_grads gradient rows.
+//
+// The row-summing kernels (this one and the 32-bit comparison step) give the
+// 16 waves of a workgroup 16 consecutive tiles and read each gradient row
+// together, with a workgroup barrier after every row: each row is then
+// streamed in 64 KB runs rather than in 16 independent 4 KB pieces.  Waves
+// without a tile keep the pace.  Every wave of a workgroup runs the same row
+// loop, so every wave reaches every barrier.
 // ---------------------------------------------------------------------------
+// sum += one gradient row of the tile (fp64, in row order)
 template <bool FULL, class G>
-__device__ __forceinline__ void warmup_tile(const Tile &tile, int lane, float *__restrict__ x,
-                                            float *__restrict__ m, float *__restrict__ v,
-                                            const typename G::T *__restrict__ g, int64_t g_ld,
-                                            int n_grads, float lr, float beta1, float omb1,
-                                            float beta2, float omb2, float eps, int use_bc,
-                                            float bc1, float bc2)
+__device__ __forceinline__ void add_row(double (&sum)[kSubBlocks][4],
+                                        const typename G::T *__restrict__ row, int lane, int len)
 {
-    const int len = tile.len;
-    const int64_t base = tile.start;
-    const double dn = (double)n_grads;
-    // every load of the tile precedes the first store (see update_tile)
-    double sum[kSubBlocks][4];
 #pragma unroll
-    for (int b = 0; b < kSubBlocks; ++b)
+    for (int b = 0; b < kSubBlocks; ++b) {
+        const v4f gv = ldg4<FULL, G>(row, b * (kWave * 4) + 4 * lane, len);
 #pragma unroll
-        for (int c = 0; c < 4; ++c) sum[b][c] = 0.0;
-    for (int i = 0; i < n_grads; ++i) {
-#pragma unroll
-        for (int b = 0; b < kSubBlocks; ++b) {
-            const v4f gv = ldg4<FULL, G>(g + (int64_t)i * g_ld + base, b * (kWave * 4) + 4 * lane, len);
-#pragma unroll
-            for (int c = 0; c < 4; ++c) sum[b][c] += (double)gv[c];
-        }
+        for (int c = 0; c < 4; ++c) sum[b][c] += (double)gv[c];
     }
+}
+
+// Adam on the averaged gradient sum / n; loads of x, m, v precede the stores.
+template <bool FULL>
+__device__ __forceinline__ void warmup_update(const double (&sum)[kSubBlocks][4], int64_t base,
+                                              int len, int lane, float *__restrict__ x,
+                                              float *__restrict__ m, float *__restrict__ v,
+                                              double dn, float lr, float beta1, float omb1,
+                                              float beta2, float omb2, float eps, int use_bc,
+                                              float bc1, float bc2)
+{
     v4f xv[kSubBlocks], mv[kSubBlocks], vv[kSubBlocks];
 #pragma unroll
     for (int b = 0; b < kSubBlocks; ++b) {
@@ -321,17 +325,14 @@ __global__ __launch_bounds__(kBlock) void k_adam_message(
 // uncompressed.  m_i = beta1 m + (1-beta1) g_i per worker, m = mean_i m_i
 // (fp64 sum in worker order, one rounding), x -= lr m / sqrt(v + eps).
 // ---------------------------------------------------------------------------
-template <bool FULL, class G>
-__device__ __forceinline__ void uncompressed_tile(const Tile &tile, int lane,
-                                                  float *__restrict__ x, float *__restrict__ m,
-                                                  const float *__restrict__ v,
-                                                  const typename G::T *__restrict__ g,
-                                                  int64_t g_ld, int n, float lr, float beta1,
-                                                  float omb1, float eps)
+template <bool FULL>
+__device__ __forceinline__ void uncompressed_load(int64_t base, int len, int lane,
+                                                  const float *__restrict__ x,
+                                                  const float *__restrict__ m,
+                                                  const float *__restrict__ v, float beta1,
+                                                  v4f (&bm)[kSubBlocks], v4f (&xv)[kSubBlocks],
+                                                  v4f (&vv)[kSubBlocks])
 {
-    const int len = tile.len;
-    const int64_t base = tile.start;
-    v4f bm[kSubBlocks], xv[kSubBlocks], vv[kSubBlocks];
 #pragma unroll
     for (int b = 0; b < kSubBlocks; ++b) {
         const int li = b * (kWave * 4) + 4 * lane;
@@ -339,24 +340,34 @@ __device__ __forceinline__ void uncompressed_tile(const Tile &tile, int lane,
         xv[b] = ld4<FULL>(x + base, li, len);
         vv[b] = ld4<FULL>(v + base, li, len);
     }
-    double sum[kSubBlocks][4];
+}
+
+// sum += worker i's momentum beta1 m + (1 - beta1) g_i (fp32, then fp64 sum)
+template <bool FULL, class G>
+__device__ __forceinline__ void add_momentum_row(double (&sum)[kSubBlocks][4],
+                                                 const v4f (&bm)[kSubBlocks],
+                                                 const typename G::T *__restrict__ row, int lane,
+                                                 int len, float omb1)
+{
 #pragma unroll
-    for (int b = 0; b < kSubBlocks; ++b)
+    for (int b = 0; b < kSubBlocks; ++b) {
+        const v4f gv = ldg4<FULL, G>(row, b * (kWave * 4) + 4 * lane, len);
 #pragma unroll
-        for (int c = 0; c < 4; ++c) sum[b][c] = 0.0;
-    for (int i = 0; i < n; ++i) {
-#pragma unroll
-        for (int b = 0; b < kSubBlocks; ++b) {
-            const v4f gv = ldg4<FULL, G>(g + (int64_t)i * g_ld + base, b * (kWave * 4) + 4 * lane, len);
-#pragma unroll
-            for (int c = 0; c < 4; ++c) {
-                float mi = omb1 * gv[c];
-                mi = bm[b][c] + mi;
-                sum[b][c] += (double)mi;
-            }
+        for (int c = 0; c < 4; ++c) {
+            float mi = omb1 * gv[c];
+            mi = bm[b][c] + mi;
+            sum[b][c] += (double)mi;
         }
     }
-    const double dn = (double)n;
+}
+
+template <bool FULL>
+__device__ __forceinline__ void uncompressed_store(const double (&sum)[kSubBlocks][4], int64_t base,
+                                                   int len, int lane, v4f (&xv)[kSubBlocks],
+                                                   const v4f (&vv)[kSubBlocks],
+                                                   float *__restrict__ x, float *__restrict__ m,
+                                                   double dn, float lr, float eps)
+{
 #pragma unroll
     for (int b = 0; b < kSubBlocks; ++b) {
         const int li = b * (kWave * 4) + 4 * lane;
@@ -376,38 +387,77 @@ __device__ __forceinline__ void uncompressed_tile(const Tile &tile, int lane,
 }
 
 template <class G>
-__global__ __launch_bounds__(kBlock) void k_uncompressed(
+__global__ __launch_bounds__(kRowBlock) void k_uncompressed(
     const Tile *__restrict__ tiles, int64_t num_tiles, float *__restrict__ x,
     float *__restrict__ m, const float *__restrict__ v, const typename G::T *__restrict__ g,
     int64_t g_ld, int n, float lr, float beta1, float omb1, float eps)
 {
     const int lane = threadIdx.x & (kWave - 1);
-    const int64_t t = xcd_block() * kWavesPerBlock + (threadIdx.x >> 6);
-    if (t >= num_tiles) return;
-    const Tile tile = tiles[t];
-    if (tile.len == kTileElems)
-        uncompressed_tile<true, G>(tile, lane, x, m, v, g, g_ld, n, lr, beta1, omb1, eps);
+    const int64_t t = xcd_block() * kRowWaves + (threadIdx.x >> 6);
+    const bool active = t < num_tiles;
+    Tile tile{0, 0, 0};
+    if (active) tile = tiles[t];
+    const bool full = tile.len == kTileElems;
+    v4f bm[kSubBlocks], xv[kSubBlocks], vv[kSubBlocks];
+    if (full)
+        uncompressed_load<true>(tile.start, tile.len, lane, x, m, v, beta1, bm, xv, vv);
     else
-        uncompressed_tile<false, G>(tile, lane, x, m, v, g, g_ld, n, lr, beta1, omb1, eps);
+        uncompressed_load<false>(tile.start, tile.len, lane, x, m, v, beta1, bm, xv, vv);
+    double sum[kSubBlocks][4];
+#pragma unroll
+    for (int b = 0; b < kSubBlocks; ++b)
+#pragma unroll
+        for (int c = 0; c < 4; ++c) sum[b][c] = 0.0;
+    for (int i = 0; i < n; ++i) {
+        const typename G::T *row = g + (int64_t)i * g_ld + tile.start;
+        if (full)
+            add_momentum_row<true, G>(sum, bm, row, lane, tile.len, omb1);
+        else if (active)
+            add_momentum_row<false, G>(sum, bm, row, lane, tile.len, omb1);
+        __builtin_amdgcn_s_barrier();  // the workgroup reads each row together
+    }
+    if (!active) return;
+    const double dn = (double)n;
+    if (full)
+        uncompressed_store<true>(sum, tile.start, tile.len, lane, xv, vv, x, m, dn, lr, eps);
+    else
+        uncompressed_store<false>(sum, tile.start, tile.len, lane, xv, vv, x, m, dn, lr, eps);
 }
 
 template <class G>
-__global__ __launch_bounds__(kBlock) void k_warmup(
+__global__ __launch_bounds__(kRowBlock) void k_warmup(
     const Tile *__restrict__ tiles, int64_t num_tiles, float *__restrict__ x,
     float *__restrict__ m, float *__restrict__ v, const typename G::T *__restrict__ g, int64_t g_ld,
     int n_grads, float lr, float beta1, float omb1, float beta2, float omb2, float eps,
     int use_bc, float bc1, float bc2)
 {
     const int lane = threadIdx.x & (kWave - 1);
-    const int64_t t = xcd_block() * kWavesPerBlock + (threadIdx.x >> 6);
-    if (t >= num_tiles) return;
-    const Tile tile = tiles[t];
-    if (tile.len == kTileElems)
-        warmup_tile<true, G>(tile, lane, x, m, v, g, g_ld, n_grads, lr, beta1, omb1, beta2, omb2,
-                          eps, use_bc, bc1, bc2);
+    const int64_t t = xcd_block() * kRowWaves + (threadIdx.x >> 6);
+    const bool active = t < num_tiles;
+    Tile tile{0, 0, 0};
+    if (active) tile = tiles[t];
+    const bool full = tile.len == kTileElems;
+    double sum[kSubBlocks][4];
+#pragma unroll
+    for (int b = 0; b < kSubBlocks; ++b)
+#pragma unroll
+        for (int c = 0; c < 4; ++c) sum[b][c] = 0.0;
+    for (int i = 0; i < n_grads; ++i) {
+        const typename G::T *row = g + (int64_t)i * g_ld + tile.start;
+        if (full)
+            add_row<true, G>(sum, row, lane, tile.len);
+        else if (active)
+            add_row<false, G>(sum, row, lane, tile.len);
+        __builtin_amdgcn_s_barrier();  // the workgroup reads each row together
+    }
+    if (!active) return;
+    const double dn = (double)n_grads;
+    if (full)
+        warmup_update<true>(sum, tile.start, tile.len, lane, x, m, v, dn, lr, beta1, omb1,
+                            beta2, omb2, eps, use_bc, bc1, bc2);
     else
-        warmup_tile<false, G>(tile, lane, x, m, v, g, g_ld, n_grads, lr, beta1, omb1, beta2, omb2,
-                           eps, use_bc, bc1, bc2);
+        warmup_update<false>(sum, tile.start, tile.len, lane, x, m, v, dn, lr, beta1, omb1,
+                             beta2, omb2, eps, use_bc, bc1, bc2);
 }
 
 // ---------------------------------------------------------------------------
@@ -1123,7 +1173,8 @@ static hipError_t launch_warmup_t(const DeviceTables &tb, int64_t num_tiles, flo
                                   float bc2, hipStream_t s)
 {
     const float omb1 = 1.0f - beta1, omb2 = 1.0f - beta2;
-    hipLaunchKernelGGL(k_warmup<G>, dim3((unsigned)blocks_for(num_tiles)), dim3(kBlock), 0, s, tb.tiles,
+    hipLaunchKernelGGL(k_warmup<G>, dim3((unsigned)xcd_grid(num_tiles, kRowWaves)), dim3(kRowBlock), 0, s,
+                       tb.tiles,
                        num_tiles, x, m, v, (const typename G::T *)g, g_ld, n_grads, lr, beta1,
                        omb1, beta2, omb2, eps, use_bc, bc1, bc2);
     return hipGetLastError();
@@ -1226,7 +1277,8 @@ static void launch_uncompressed_t(const DeviceTables &tb, int64_t num_tiles, flo
                                   float beta1, float eps, hipStream_t s)
 {
     const float omb1 = 1.0f - beta1;
-    hipLaunchKernelGGL(k_uncompressed<G>, dim3((unsigned)blocks_for(num_tiles)), dim3(kBlock), 0, s,
+    hipLaunchKernelGGL(k_uncompressed<G>, dim3((unsigned)xcd_grid(num_tiles, kRowWaves)),
+                       dim3(kRowBlock), 0, s,
                        tb.tiles, num_tiles, x, m, v, (const typename G::T *)g, g_ld, n, lr, beta1,
                        omb1, eps);
 }

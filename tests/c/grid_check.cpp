@@ -18,21 +18,21 @@ static void fail(const char *what, long long a, long long b)
     ++failures;
 }
 
-// One wave per tile, kWavesPerBlock waves per block, logical block order.
-static void check_tiles(int64_t tiles)
+// One wave per tile, waves_per_block waves per block, logical block order.
+static void check_tiles(int64_t tiles, int waves_per_block)
 {
     ++cases;
-    const int64_t grid = xcd_grid(tiles, kWavesPerBlock);
+    const int64_t grid = xcd_grid(tiles, waves_per_block);
     if (grid % kXcds) fail("tile grid not a multiple of the XCD count", tiles, grid);
-    if (grid * kWavesPerBlock < tiles) fail("tile grid too small", tiles, grid);
+    if (grid * waves_per_block < tiles) fail("tile grid too small", tiles, grid);
     std::vector<unsigned char> seen((size_t)tiles, 0);
     std::vector<unsigned char> lseen((size_t)grid, 0);
     for (int64_t b = 0; b < grid; ++b) {
         const int64_t lb = xcd_block_of(b, grid);
         if (lb < 0 || lb >= grid) { fail("logical block out of range", b, grid); continue; }
         if (lseen[(size_t)lb]++) fail("logical block taken twice", lb, grid);
-        for (int w = 0; w < kWavesPerBlock; ++w) {
-            const int64_t t = lb * kWavesPerBlock + w;
+        for (int w = 0; w < waves_per_block; ++w) {
+            const int64_t t = lb * waves_per_block + w;
             if (t < tiles && seen[(size_t)t]++) fail("tile taken twice", t, tiles);
         }
     }
@@ -64,9 +64,12 @@ static void check_worker(int64_t items, int64_t max_blocks)
 
 int main()
 {
-    for (int64_t t = 1; t <= 600; ++t) check_tiles(t);
-    // BERT-Large (326,288 tiles) and the stress workload's tile counts
-    for (int64_t t : {326288LL, 542089LL, 106344LL, 1275LL}) check_tiles(t);
+    // the streaming kernels (kWavesPerBlock) and the row-summing ones (kRowWaves)
+    for (int wpb : {kWavesPerBlock, kRowWaves}) {
+        for (int64_t t = 1; t <= 600; ++t) check_tiles(t, wpb);
+        // BERT-Large (326,288 tiles) and the stress workload's tile counts
+        for (int64_t t : {326288LL, 542089LL, 106344LL, 1275LL}) check_tiles(t, wpb);
+    }
 
     for (int64_t items = 1; items <= 700; ++items)
         for (int64_t cap : {1LL, 3LL, 8LL, 9LL, 24LL, 64LL, (long long)kMaxWorkerGridBlocks})
