@@ -465,13 +465,15 @@ __global__ __launch_bounds__(kRowBlock) void k_warmup(
 // sign words of z_i, per-tile partial sum of z_i^2, and z_i written back as the
 // new compensated error state.
 //
-// A wave handles one tile for a group of consecutive workers, and the items
-// run group-major, split into one contiguous eighth per XCD: the waves in
-// flight on an XCD work on the same few worker rows, so each XCD streams
-// through 2 x group rows of (g, error state) at a time instead of all 2n.
-// With one worker per group the momentum of a tile is re-derived by every
-// worker; in packed form that is 1/8 byte per element per worker from a sign
-// array small enough to stay in the last-level cache.
+// Packed momentum (every step after the first): a wave handles one tile for
+// a group of consecutive workers (one worker in practice), and the items run
+// group-major, split into one contiguous eighth per XCD: the waves in flight
+// on an XCD work on the same few worker rows, so each XCD streams through
+// 2 x group rows of (g, error state) at a time instead of all 2n.  The
+// momentum of a tile is re-derived by every worker, 1/8 byte per element per
+// worker from a sign array small enough to stay in the last-level cache.
+// An fp32 momentum (the first compression step) is read once per tile for
+// all local workers instead, by k_worker_rows.
 // ---------------------------------------------------------------------------
 // The shared momentum m_{t-1} of the tile times beta1.  PACKED: m_{t-1} is
 // the previous step's gathered server message, decoded from its sign words
@@ -502,22 +504,20 @@ __device__ __forceinline__ void beta1_momentum(v4f (&bm)[kSubBlocks], const Tile
     }
 }
 
-template <bool FULL, bool PACKED, class G>
-__device__ __forceinline__ void worker_tile(
-    const Tile &tile, int64_t t, int lane, int64_t num_tiles, const float *__restrict__ m,
-    const uint64_t *__restrict__ m_bits, const float *__restrict__ m_scales,
+// Worker i's row of the tile: z_i from the momentum term bm = beta1 m, the
+// gradient row and the previous compensated value; its sign words, tile sum
+// of squares and new compensated value.
+template <bool FULL, class G>
+__device__ __forceinline__ void worker_row(
+    const Tile &tile, int64_t t, int lane, int64_t num_tiles, const v4f (&bm)[kSubBlocks], int i,
     const typename G::T *__restrict__ g, int64_t g_ld, float *__restrict__ err, int64_t err_ld,
     const float *__restrict__ scales, int64_t scales_ld, uint64_t *__restrict__ bits,
-    int64_t bits_ld, double *__restrict__ partial, int i0, int i1, float beta1, float omb1)
+    int64_t bits_ld, double *__restrict__ partial, float omb1)
 {
     const int len = tile.len;
     const int64_t base = tile.start;
     const int nwords = (len + 63) >> 6;
-
-    v4f bm[kSubBlocks];
-    beta1_momentum<FULL, PACKED>(bm, tile, lane, m, m_bits, m_scales, beta1);
-
-    for (int i = i0; i < i1; ++i) {
+    {
         const float sp = scales[(int64_t)i * scales_ld + tile.seg];
         const typename G::T *gi = g + (int64_t)i * g_ld + base;
         float *ei = err + (int64_t)i * err_ld + base;
@@ -557,6 +557,22 @@ __device__ __forceinline__ void worker_tile(
     }
 }
 
+// The tile for workers [i0, i1), the momentum term loaded or decoded once.
+template <bool FULL, bool PACKED, class G>
+__device__ __forceinline__ void worker_tile(
+    const Tile &tile, int64_t t, int lane, int64_t num_tiles, const float *__restrict__ m,
+    const uint64_t *__restrict__ m_bits, const float *__restrict__ m_scales,
+    const typename G::T *__restrict__ g, int64_t g_ld, float *__restrict__ err, int64_t err_ld,
+    const float *__restrict__ scales, int64_t scales_ld, uint64_t *__restrict__ bits,
+    int64_t bits_ld, double *__restrict__ partial, int i0, int i1, float beta1, float omb1)
+{
+    v4f bm[kSubBlocks];
+    beta1_momentum<FULL, PACKED>(bm, tile, lane, m, m_bits, m_scales, beta1);
+    for (int i = i0; i < i1; ++i)
+        worker_row<FULL, G>(tile, t, lane, num_tiles, bm, i, g, g_ld, err, err_ld, scales,
+                            scales_ld, bits, bits_ld, partial, omb1);
+}
+
 template <bool PACKED, class G>
 __global__ __launch_bounds__(kWorkerBlock) void k_worker_pass(
     const Tile *__restrict__ tiles, int64_t num_tiles, const float *__restrict__ m,
@@ -584,6 +600,39 @@ __global__ __launch_bounds__(kWorkerBlock) void k_worker_pass(
             worker_tile<false, PACKED, G>(tile, t, lane, num_tiles, m, m_bits, m_scales, g, g_ld,
                                           err, err_ld, scales, scales_ld, bits, bits_ld, partial,
                                           i0, i1, beta1, omb1);
+    }
+}
+
+// ---------------------------------------------------------------------------
+// The worker pass with an fp32 momentum (the first compression step): m is
+// read once per tile for all local workers, and the 16 waves of a workgroup
+// walk the worker rows together (one barrier per row), as in the warm-up.
+template <class G>
+__global__ __launch_bounds__(kRowBlock) void k_worker_rows(
+    const Tile *__restrict__ tiles, int64_t num_tiles, const float *__restrict__ m,
+    const typename G::T *__restrict__ g, int64_t g_ld, float *__restrict__ err, int64_t err_ld,
+    const float *__restrict__ scales, int64_t scales_ld, uint64_t *__restrict__ bits,
+    int64_t bits_ld, double *__restrict__ partial, int n_local, float beta1, float omb1)
+{
+    const int lane = threadIdx.x & (kWave - 1);
+    const int64_t t = xcd_block() * kRowWaves + (threadIdx.x >> 6);
+    const bool active = t < num_tiles;
+    Tile tile{0, 0, 0};
+    if (active) tile = tiles[t];
+    const bool full = tile.len == kTileElems;
+    v4f bm[kSubBlocks];
+    if (full)
+        beta1_momentum<true, false>(bm, tile, lane, m, nullptr, nullptr, beta1);
+    else
+        beta1_momentum<false, false>(bm, tile, lane, m, nullptr, nullptr, beta1);
+    for (int i = 0; i < n_local; ++i) {
+        if (full)
+            worker_row<true, G>(tile, t, lane, num_tiles, bm, i, g, g_ld, err, err_ld, scales,
+                                scales_ld, bits, bits_ld, partial, omb1);
+        else if (active)
+            worker_row<false, G>(tile, t, lane, num_tiles, bm, i, g, g_ld, err, err_ld, scales,
+                                 scales_ld, bits, bits_ld, partial, omb1);
+        __builtin_amdgcn_s_barrier();  // the workgroup reads each worker row together
     }
 }
 
@@ -1206,13 +1255,23 @@ static void launch_worker_t(const DeviceTables &tb, int64_t num_tiles, const flo
                             int n_local, int group, float beta1, hipStream_t s)
 {
     const float omb1 = 1.0f - beta1;
-    const int64_t groups = (n_local + group - 1) / group;
-    const int64_t items = groups * num_tiles;
-    const int64_t blocks = worker_grid(items, kWorkerWavesPerBlock, kMaxWorkerGridBlocks);
-    hipLaunchKernelGGL((k_worker_pass<PACKED, G>), dim3((unsigned)blocks), dim3(kWorkerBlock), 0, s,
-                       tb.tiles, num_tiles, m, m_bits, m_scales, (const typename G::T *)g, g_ld,
-                       err, err_ld, scales, scales_ld, bits, bits_ld, partial, n_local, group,
-                       items, beta1, omb1);
+    if constexpr (PACKED) {
+        const int64_t groups = (n_local + group - 1) / group;
+        const int64_t items = groups * num_tiles;
+        const int64_t blocks = worker_grid(items, kWorkerWavesPerBlock, kMaxWorkerGridBlocks);
+        hipLaunchKernelGGL((k_worker_pass<PACKED, G>), dim3((unsigned)blocks), dim3(kWorkerBlock),
+                           0, s, tb.tiles, num_tiles, m, m_bits, m_scales,
+                           (const typename G::T *)g, g_ld, err, err_ld, scales, scales_ld, bits,
+                           bits_ld, partial, n_local, group, items, beta1, omb1);
+    } else {
+        (void)m_bits;
+        (void)m_scales;
+        (void)group;
+        hipLaunchKernelGGL(k_worker_rows<G>, dim3((unsigned)xcd_grid(num_tiles, kRowWaves)),
+                           dim3(kRowBlock), 0, s, tb.tiles, num_tiles, m,
+                           (const typename G::T *)g, g_ld, err, err_ld, scales, scales_ld, bits,
+                           bits_ld, partial, n_local, beta1, omb1);
+    }
 }
 
 template <class G>
