@@ -10,7 +10,8 @@ namespace onebit {
 
 // A unit of work: up to kTileElems consecutive elements of one segment,
 // starting on a 64-element (one sign word) boundary.  One wavefront owns one
-// tile; a 256-thread workgroup runs four consecutive tiles.
+// tile (one tile of one worker row, in the packed worker pass); the launch
+// shapes are in onebit_grid.h.
 struct Tile {
     int64_t start;  // first flat element (multiple of 64)
     int32_t len;    // elements in the tile, 1..kTileElems

@@ -517,44 +517,42 @@ __device__ __forceinline__ void worker_row(
     const int len = tile.len;
     const int64_t base = tile.start;
     const int nwords = (len + 63) >> 6;
-    {
-        const float sp = scales[(int64_t)i * scales_ld + tile.seg];
-        const typename G::T *gi = g + (int64_t)i * g_ld + base;
-        float *ei = err + (int64_t)i * err_ld + base;
-        uint64_t *bi = bits + (int64_t)i * bits_ld + (base >> 6);
-        v4f gv[kSubBlocks], cv[kSubBlocks];
+    const float sp = scales[(int64_t)i * scales_ld + tile.seg];
+    const typename G::T *gi = g + (int64_t)i * g_ld + base;
+    float *ei = err + (int64_t)i * err_ld + base;
+    uint64_t *bi = bits + (int64_t)i * bits_ld + (base >> 6);
+    v4f gv[kSubBlocks], cv[kSubBlocks];
 #pragma unroll
-        for (int b = 0; b < kSubBlocks; ++b) {
-            const int li = b * (kWave * 4) + 4 * lane;
-            gv[b] = ldg4<FULL, G>(gi, li, len);
-            cv[b] = ld4<FULL>(ei, li, len);
-        }
-        double acc = 0.0;
-#pragma unroll
-        for (int b = 0; b < kSubBlocks; ++b) {
-            const int li = b * (kWave * 4) + 4 * lane;
-            v4f zv;
-            uint32_t nib = 0;
-#pragma unroll
-            for (int c = 0; c < 4; ++c) {
-                const float d = error_of(cv[b][c], sp);
-                float mi = omb1 * gv[b][c];
-                mi = bm[b][c] + mi;
-                const float z = mi + d;
-                zv[c] = z;
-                const bool valid = FULL || li + c < len;
-                const double zd = valid ? (double)z : 0.0;
-                acc += zd * zd;
-                nib |= (valid && z >= 0.f) ? (1u << c) : 0u;
-            }
-            st4<FULL>(ei, li, len, zv);
-            const uint64_t word = row_sign_word(nib, lane);
-            const int w = 4 * b + (lane >> 4);
-            if ((lane & 15) == 0 && (FULL || w < nwords)) bi[w] = word;
-        }
-        acc = wave_sum(acc);
-        if (lane == 0) partial[(int64_t)i * num_tiles + t] = acc;
+    for (int b = 0; b < kSubBlocks; ++b) {
+        const int li = b * (kWave * 4) + 4 * lane;
+        gv[b] = ldg4<FULL, G>(gi, li, len);
+        cv[b] = ld4<FULL>(ei, li, len);
     }
+    double acc = 0.0;
+#pragma unroll
+    for (int b = 0; b < kSubBlocks; ++b) {
+        const int li = b * (kWave * 4) + 4 * lane;
+        v4f zv;
+        uint32_t nib = 0;
+#pragma unroll
+        for (int c = 0; c < 4; ++c) {
+            const float d = error_of(cv[b][c], sp);
+            float mi = omb1 * gv[b][c];
+            mi = bm[b][c] + mi;
+            const float z = mi + d;
+            zv[c] = z;
+            const bool valid = FULL || li + c < len;
+            const double zd = valid ? (double)z : 0.0;
+            acc += zd * zd;
+            nib |= (valid && z >= 0.f) ? (1u << c) : 0u;
+        }
+        st4<FULL>(ei, li, len, zv);
+        const uint64_t word = row_sign_word(nib, lane);
+        const int w = 4 * b + (lane >> 4);
+        if ((lane & 15) == 0 && (FULL || w < nwords)) bi[w] = word;
+    }
+    acc = wave_sum(acc);
+    if (lane == 0) partial[(int64_t)i * num_tiles + t] = acc;
 }
 
 // The tile for workers [i0, i1), the momentum term loaded or decoded once.
