@@ -394,42 +394,25 @@ def main():
     synth.device_grads(wl, plan.D, plan.tensor_off, wl.warmup_steps + 1, st.grads, scale_vec)
     torch.cuda.synchronize()
 
-    def one_step(ev=None, first=False):
-        # the first compression step starts from the warm-up's fp32 m; later
-        # steps take m from the previous step's server message
-        if ev:
-            ev[0].record()
-        if first:
-            ob.onebit_worker_compress(plan, st.m, st.grads, st.worker_err, st.worker_bits,
-                                      st.worker_scales, wl.beta1, st.workspace)
-        else:
-            ob.onebit_worker_compress(plan, None, st.grads, st.worker_err, st.worker_bits,
-                                      st.worker_scales, wl.beta1, st.workspace,
-                                      m_bits=st.server_bits, m_scales=st.server_scales)
-        if ev:
-            ev[1].record()
-        ob.onebit_server_reduce_compress(plan, 0, n, st.worker_bits, st.worker_scales,
-                                         st.server_err, st.server_bits, st.server_scales,
-                                         st.workspace)
-        if ev:
-            ev[2].record()
-        ob.onebit_decompress_update(plan, st.server_bits, st.server_scales, st.x, None, st.v,
-                                    wl.lr, wl.eps)
-        if ev:
-            ev[3].record()
-
     if args.variant != "onebit":
         return bench_variant(args, wl, plan, st, gbytes)
 
-    one_step(first=True)  # untimed: the step that leaves the warm-up's fp32 momentum
+    # The timed step is State.step: the fused onebit_step (worker pass, its
+    # scale finalize, the chunk owners' pass, its finalize, the update), in
+    # its events form, which also marks the launch stream before the worker
+    # pass, before the owners' pass, before the update and after it.
+    st.step(wl.lr, wl.beta1, wl.eps)  # untimed: the step that leaves the warm-up's fp32 m
+    assert st.momentum_is_packed()
     for _ in range(args.warmup):
-        one_step()
-    torch.cuda.synchronize()
+        st.step(wl.lr, wl.beta1, wl.eps)
     events = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
+    for ev in events:  # creates each HIP event; the step re-records them on its stream
+        for e in ev:
+            e.record()
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for k in range(args.steps):
-        one_step(events[k])
+        st.step(wl.lr, wl.beta1, wl.eps, events=events[k])
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     ms_step = wall * 1e3 / args.steps
@@ -443,7 +426,7 @@ def main():
         # per step instead of five (worker, scales, owners, scales, update)
         graph = torch.cuda.CUDAGraph()
         with torch.cuda.graph(graph):
-            one_step()
+            st.step(wl.lr, wl.beta1, wl.eps)
         for _ in range(args.warmup):
             graph.replay()
         gev = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(args.steps)]
@@ -464,6 +447,8 @@ def main():
     step_bytes = d * (bw + bs + bu)
     worker_bytes = d * bw
     achieved = worker_bytes / (part_ms[0] * 1e-3) / 1e9
+    # the same pass counted with m read as an fp32 value (4 B) instead of a bit
+    bw_fp32_m = 4 + n * (gbytes + 4 + 4 + 1 / 8)
     result = {
         "metric": ("compression-phase step params/sec and achieved HBM GB/s vs peak, BERT-Large"
                    if wl.name == "bert_large" else
@@ -486,6 +471,8 @@ def main():
         "step_hbm_gbps_algorithmic": step_bytes / (ms_step * 1e-3) / 1e9,
         "step_frac_of_peak": step_bytes / (ms_step * 1e-3) / 1e9 / HBM_PEAK_GBPS,
         "bytes_per_param": {"worker": bw, "server": bs, "update": bu},
+        "timed_call": "State.step -> onebit_step (onebit_step_events: the same launches "
+                      "with four event marks)",
         "kernel_ms": {"worker_compress": part_ms[0], "server_reduce_compress": part_ms[1],
                       "decompress_update": part_ms[2], "sum": gpu_step_ms},
         "gpu_step_ms": {"median": per_step[len(per_step) // 2], "min": per_step[0],
@@ -501,7 +488,18 @@ def main():
                      "achieved": achieved, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
                      "frac": achieved / HBM_PEAK_GBPS,
                      "traffic": measured_traffic(wl.name, "k_worker_pass<true, %s>" % gname),
-                     "algorithmic_bytes_per_launch": worker_bytes},
+                     "algorithmic_bytes_per_launch": worker_bytes,
+                     "bytes_per_param": bw,
+                     "bytes_per_param_rule": "m read as its sign bit (packed momentum): "
+                                             "1/8 + n*(%d g + 4 err in + 4 err out + 1/8 bit)"
+                                             % gbytes,
+                     "bytes_per_param_fp32_m": bw_fp32_m,
+                     "frac_fp32_m": (bw_fp32_m * d / (part_ms[0] * 1e-3) / 1e9
+                                     / HBM_PEAK_GBPS),
+                     "ms": part_ms[0],
+                     "timed": "HIP events on the launch stream before and after the worker "
+                              "pass (k_worker_pass and its scale finalize) of each timed "
+                              "onebit_step, averaged over the timed steps"},
         "kernels": {name: {"ms": ms, "algorithmic_bytes": nbytes,
                            "gbps": nbytes / (ms * 1e-3) / 1e9,
                            "frac": nbytes / (ms * 1e-3) / 1e9 / HBM_PEAK_GBPS,

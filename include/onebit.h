@@ -234,6 +234,22 @@ int onebit_step(onebit_plan plan, float *x, float *m, const float *v_frozen,
                 float lr, float beta1, float eps, void *workspace,
                 onebit_stream stream);
 
+/* onebit_step with timing marks, to profile the fused step phase by phase:
+ * the same launches, and in addition hipEventRecord(events[k], stream)
+ * before the worker pass (k = 0), before the chunk owners' pass (k = 1),
+ * before the update (k = 2) and after it (k = 3).  events: a host array of
+ * four hipEvent_t (void *) created by the caller, with timing enabled to read
+ * elapsed times; a NULL entry skips that mark.  The marks add no host
+ * synchronisation; a call with events is not meant for graph capture.
+ * Errors: those of onebit_step (all checked before the first launch or
+ * mark), EINVAL if events is NULL, EHIP if a record fails. */
+int onebit_step_events(onebit_plan plan, float *x, float *m, const float *v_frozen,
+                       const void *grads, int32_t grad_dtype, int64_t grad_ld,
+                       float *worker_err, int64_t err_ld, float *server_err,
+                       uint64_t *worker_bits, float *worker_scales, uint64_t *server_bits,
+                       float *server_scales, float lr, float beta1, float eps,
+                       void *workspace, void *const *events, onebit_stream stream);
+
 /* Comparison variants of Section 7.2 (not part of 1-bit Adam itself). */
 
 /* "1-bit Adam (32-bits)": the compression stage with the identity compressor

@@ -388,14 +388,19 @@ int onebit_warmup_adam_step(onebit_plan p, float *x, float *m, float *v, const v
     return ONEBIT_OK;
 }
 
-int onebit_worker_compress(onebit_plan p, const float *m, const uint64_t *m_bits,
-                           const float *m_scales, const void *grads, int32_t grad_dtype,
-                           int64_t grad_ld, int32_t n_local, float *worker_err, int64_t err_ld,
-                           uint64_t *worker_bits, int64_t bits_ld, float *worker_scales,
-                           int64_t scales_ld, float beta1, void *workspace,
-                           onebit_stream stream)
+}  // extern "C"
+
+namespace {
+
+// The three calls of a compression step, each split into its argument
+// checks and its launches, so that the fused step checks everything before
+// its first launch.
+int check_worker(const onebit_plan_s *p, const float *m, const uint64_t *m_bits,
+                 const float *m_scales, const void *grads, int32_t grad_dtype, int64_t grad_ld,
+                 int32_t n_local, const float *worker_err, int64_t err_ld,
+                 const uint64_t *worker_bits, int64_t bits_ld, const float *worker_scales,
+                 int64_t scales_ld, const void *workspace)
 {
-    TRY(check_plan(p));
     if (m) {
         TRY(check_f32(p, m, "m"));
     } else {
@@ -416,31 +421,37 @@ int onebit_worker_compress(onebit_plan p, const float *m, const uint64_t *m_bits
     TRY(check_ld(err_ld, p->D, n_local > 1, "err_ld"));
     TRY(check_ld(bits_ld, p->W, false, "bits_ld"));
     TRY(check_ld(scales_ld, p->S, false, "scales_ld"));
+    return ONEBIT_OK;
+}
+
+int run_worker(const onebit_plan_s *p, const float *m, const uint64_t *m_bits,
+               const float *m_scales, const void *grads, int32_t grad_dtype, int64_t grad_ld,
+               int32_t n_local, float *worker_err, int64_t err_ld, uint64_t *worker_bits,
+               int64_t bits_ld, float *worker_scales, int64_t scales_ld, float beta1,
+               void *workspace, hipStream_t s)
+{
     double *part = (double *)((char *)workspace + worker_partial_offset(p));
-    hipStream_t s = (hipStream_t)stream;
     // Packed momentum costs 1/8 byte per element to re-derive, so each wave
     // takes one worker and the grid streams two rows at a time; an fp32
     // momentum is read once per tile for all local workers instead.
     const int group = m ? n_local : 1;
     if (p->T > 0)
         TRY_HIP(onebit::launch_worker_pass(p->tb, p->T, m, m_bits, m_scales, grads, grad_dtype,
-                                       grad_ld, worker_err, err_ld, worker_scales, scales_ld,
-                                       worker_bits, bits_ld, part, n_local, group, beta1, s),
-            "worker kernel launch");
+                                           grad_ld, worker_err, err_ld, worker_scales, scales_ld,
+                                           worker_bits, bits_ld, part, n_local, group, beta1, s),
+                "worker kernel launch");
     TRY_HIP(onebit::launch_finalize(p->tb, p->max_seg_tiles, (int64_t)n_local * p->S, p->S, 0,
                                     p->n, 0, 0, part, p->T, worker_scales, scales_ld, s),
             "worker scale kernel launch");
     return ONEBIT_OK;
 }
 
-int onebit_server_reduce_compress(onebit_plan p, int32_t server_begin, int32_t server_end,
-                                  const uint64_t *worker_bits, int64_t bits_ld,
-                                  int64_t bits_word_base, const float *worker_scales,
-                                  int64_t scales_ld, int64_t scales_seg_base, float *server_err,
-                                  uint64_t *server_bits, float *server_scales, void *workspace,
-                                  onebit_stream stream)
+int check_server(const onebit_plan_s *p, int32_t server_begin, int32_t server_end,
+                 const uint64_t *worker_bits, int64_t bits_ld, int64_t bits_word_base,
+                 const float *worker_scales, int64_t scales_ld, int64_t scales_seg_base,
+                 const float *server_err, const uint64_t *server_bits,
+                 const float *server_scales, const void *workspace)
 {
-    TRY(check_plan(p));
     TRY(check_u64(p, worker_bits, "worker_bits"));
     if (!worker_scales) return fail(ONEBIT_EINVAL, "worker_scales is NULL");
     if (!aligned(worker_scales, 4)) return fail(ONEBIT_EALIGN, "worker_scales misaligned");
@@ -471,10 +482,18 @@ int onebit_server_reduce_compress(onebit_plan p, int32_t server_begin, int32_t s
         return fail(ONEBIT_EINVAL, "scales_seg_base %lld is not in [0, %lld]",
                     (long long)scales_seg_base, (long long)qlo);
     TRY(check_ld(scales_ld, qhi + 1 - scales_seg_base, false, "scales_ld"));
+    return ONEBIT_OK;
+}
+
+int run_server(const onebit_plan_s *p, int32_t server_begin, int32_t server_end,
+               const uint64_t *worker_bits, int64_t bits_ld, int64_t bits_word_base,
+               const float *worker_scales, int64_t scales_ld, int64_t scales_seg_base,
+               float *server_err, uint64_t *server_bits, float *server_scales, void *workspace,
+               hipStream_t s)
+{
     const int64_t tb = p->chunk_tile_begin[server_begin];
     const int64_t tc = p->chunk_tile_begin[server_end] - tb;
     double *part = (double *)((char *)workspace + server_partial_offset(p));
-    hipStream_t s = (hipStream_t)stream;
     if (tc > 0)
         TRY_HIP(onebit::launch_server_pass(p->tb, tb, tc, p->n, worker_bits, bits_ld,
                                            bits_word_base, worker_scales, scales_ld,
@@ -488,22 +507,106 @@ int onebit_server_reduce_compress(onebit_plan p, int32_t server_begin, int32_t s
     return ONEBIT_OK;
 }
 
-int onebit_decompress_update(onebit_plan p, const uint64_t *server_bits,
-                             const float *server_scales, float *x, float *m_out,
-                             const float *v_frozen, float lr, float eps, onebit_stream stream)
+int check_update(const onebit_plan_s *p, const uint64_t *server_bits,
+                 const float *server_scales, const float *x, const float *m_out,
+                 const float *v_frozen)
 {
-    TRY(check_plan(p));
     TRY(check_u64(p, server_bits, "server_bits"));
     if (!server_scales) return fail(ONEBIT_EINVAL, "server_scales is NULL");
     if (!aligned(server_scales, 4)) return fail(ONEBIT_EALIGN, "server_scales misaligned");
     TRY(check_f32(p, x, "x"));
     if (m_out) TRY(check_f32(p, m_out, "m_out"));
     TRY(check_f32(p, v_frozen, "v_frozen"));
+    return ONEBIT_OK;
+}
+
+int run_update(const onebit_plan_s *p, const uint64_t *server_bits, const float *server_scales,
+               float *x, float *m_out, const float *v_frozen, float lr, float eps, hipStream_t s)
+{
     if (p->T == 0) return ONEBIT_OK;
     TRY_HIP(onebit::launch_update(p->tb, p->T, server_bits, server_scales, x, m_out, v_frozen,
-                                  lr, eps, (hipStream_t)stream),
+                                  lr, eps, s),
             "update kernel launch");
     return ONEBIT_OK;
+}
+
+int record(void *const *events, int k, hipStream_t s)
+{
+    if (events && events[k])
+        TRY_HIP(hipEventRecord((hipEvent_t)events[k], s), "hipEventRecord");
+    return ONEBIT_OK;
+}
+
+// The fused step: all n workers (rows of W words and S scales), all n chunk
+// owners reading those rows in place, the update writing m when m is given.
+int step_impl(onebit_plan_s *p, float *x, float *m, const float *v_frozen, const void *grads,
+              int32_t grad_dtype, int64_t grad_ld, float *worker_err, int64_t err_ld,
+              float *server_err, uint64_t *worker_bits, float *worker_scales,
+              uint64_t *server_bits, float *server_scales, float lr, float beta1, float eps,
+              void *workspace, void *const *events, hipStream_t s)
+{
+    TRY(check_plan(p));
+    // Every argument is checked before the first launch, so an error writes nothing.
+    TRY(check_worker(p, m, server_bits, server_scales, grads, grad_dtype, grad_ld, p->n,
+                     worker_err, err_ld, worker_bits, p->W, worker_scales, p->S, workspace));
+    TRY(check_server(p, 0, p->n, worker_bits, p->W, 0, worker_scales, p->S, 0, server_err,
+                     server_bits, server_scales, workspace));
+    TRY(check_update(p, server_bits, server_scales, x, m, v_frozen));
+    TRY(record(events, 0, s));
+    TRY(run_worker(p, m, server_bits, server_scales, grads, grad_dtype, grad_ld, p->n,
+                   worker_err, err_ld, worker_bits, p->W, worker_scales, p->S, beta1, workspace,
+                   s));
+    TRY(record(events, 1, s));
+    TRY(run_server(p, 0, p->n, worker_bits, p->W, 0, worker_scales, p->S, 0, server_err,
+                   server_bits, server_scales, workspace, s));
+    TRY(record(events, 2, s));
+    TRY(run_update(p, server_bits, server_scales, x, m, v_frozen, lr, eps, s));
+    return record(events, 3, s);
+}
+
+}  // namespace
+
+extern "C" {
+
+int onebit_worker_compress(onebit_plan p, const float *m, const uint64_t *m_bits,
+                           const float *m_scales, const void *grads, int32_t grad_dtype,
+                           int64_t grad_ld, int32_t n_local, float *worker_err, int64_t err_ld,
+                           uint64_t *worker_bits, int64_t bits_ld, float *worker_scales,
+                           int64_t scales_ld, float beta1, void *workspace,
+                           onebit_stream stream)
+{
+    TRY(check_plan(p));
+    TRY(check_worker(p, m, m_bits, m_scales, grads, grad_dtype, grad_ld, n_local, worker_err,
+                     err_ld, worker_bits, bits_ld, worker_scales, scales_ld, workspace));
+    return run_worker(p, m, m_bits, m_scales, grads, grad_dtype, grad_ld, n_local, worker_err,
+                      err_ld, worker_bits, bits_ld, worker_scales, scales_ld, beta1, workspace,
+                      (hipStream_t)stream);
+}
+
+int onebit_server_reduce_compress(onebit_plan p, int32_t server_begin, int32_t server_end,
+                                  const uint64_t *worker_bits, int64_t bits_ld,
+                                  int64_t bits_word_base, const float *worker_scales,
+                                  int64_t scales_ld, int64_t scales_seg_base, float *server_err,
+                                  uint64_t *server_bits, float *server_scales, void *workspace,
+                                  onebit_stream stream)
+{
+    TRY(check_plan(p));
+    TRY(check_server(p, server_begin, server_end, worker_bits, bits_ld, bits_word_base,
+                     worker_scales, scales_ld, scales_seg_base, server_err, server_bits,
+                     server_scales, workspace));
+    return run_server(p, server_begin, server_end, worker_bits, bits_ld, bits_word_base,
+                      worker_scales, scales_ld, scales_seg_base, server_err, server_bits,
+                      server_scales, workspace, (hipStream_t)stream);
+}
+
+int onebit_decompress_update(onebit_plan p, const uint64_t *server_bits,
+                             const float *server_scales, float *x, float *m_out,
+                             const float *v_frozen, float lr, float eps, onebit_stream stream)
+{
+    TRY(check_plan(p));
+    TRY(check_update(p, server_bits, server_scales, x, m_out, v_frozen));
+    return run_update(p, server_bits, server_scales, x, m_out, v_frozen, lr, eps,
+                      (hipStream_t)stream);
 }
 
 int onebit_step(onebit_plan p, float *x, float *m, const float *v_frozen, const void *grads,
@@ -512,23 +615,22 @@ int onebit_step(onebit_plan p, float *x, float *m, const float *v_frozen, const 
                 float *server_scales, float lr, float beta1, float eps, void *workspace,
                 onebit_stream stream)
 {
-    TRY(check_plan(p));
-    // Validate everything before the first launch so that an error writes nothing.
-    TRY(check_f32(p, x, "x"));
-    if (m) TRY(check_f32(p, m, "m"));
-    TRY(check_f32(p, v_frozen, "v_frozen"));
-    TRY(check_f32(p, server_err, "server_err"));
-    TRY(check_u64(p, server_bits, "server_bits"));
-    if (!server_scales) return fail(ONEBIT_EINVAL, "server_scales is NULL");
-    if (!aligned(server_scales, 4)) return fail(ONEBIT_EALIGN, "server_scales misaligned");
-    TRY(onebit_worker_compress(p, m, server_bits, server_scales, grads, grad_dtype, grad_ld, p->n,
-                               worker_err, err_ld, worker_bits, p->W, worker_scales, p->S,
-                               beta1, workspace, stream));
-    TRY(onebit_server_reduce_compress(p, 0, p->n, worker_bits, p->W, 0, worker_scales, p->S, 0,
-                                      server_err, server_bits, server_scales, workspace,
-                                      stream));
-    return onebit_decompress_update(p, server_bits, server_scales, x, m, v_frozen, lr, eps,
-                                    stream);
+    return step_impl(p, x, m, v_frozen, grads, grad_dtype, grad_ld, worker_err, err_ld,
+                     server_err, worker_bits, worker_scales, server_bits, server_scales, lr,
+                     beta1, eps, workspace, nullptr, (hipStream_t)stream);
+}
+
+int onebit_step_events(onebit_plan p, float *x, float *m, const float *v_frozen,
+                       const void *grads, int32_t grad_dtype, int64_t grad_ld, float *worker_err,
+                       int64_t err_ld, float *server_err, uint64_t *worker_bits,
+                       float *worker_scales, uint64_t *server_bits, float *server_scales,
+                       float lr, float beta1, float eps, void *workspace, void *const *events,
+                       onebit_stream stream)
+{
+    if (!events) return fail(ONEBIT_EINVAL, "events is NULL");
+    return step_impl(p, x, m, v_frozen, grads, grad_dtype, grad_ld, worker_err, err_ld,
+                     server_err, worker_bits, worker_scales, server_bits, server_scales, lr,
+                     beta1, eps, workspace, events, (hipStream_t)stream);
 }
 
 int onebit_adam_message_step(onebit_plan p, float *x, float *m, float *v, const uint64_t *bits,

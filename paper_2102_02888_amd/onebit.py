@@ -78,6 +78,34 @@ def _rows(t):
     return t.shape[0] if t.dim() == 2 else 1
 
 
+def chunk_word_ranges(seg_begin, seg_end, K, n):
+    """Per chunk j, the lowest and highest sign word of its segments (k, j)
+    over all K tensors (segment q = k*n + j covers elements
+    [seg_begin[q], seg_end[q])); -1, -1 for a chunk whose segments are all
+    empty.  Computed once per plan, so that a chunk owners' call costs O(n)
+    on the host instead of O(K*n)."""
+    b = np.asarray(seg_begin, np.int64).reshape(K, n)
+    e = np.asarray(seg_end, np.int64).reshape(K, n)
+    full = e > b
+    big = np.iinfo(np.int64).max
+    lo = np.where(full, b // 64, big).min(axis=0)
+    hi = np.where(full, (e - 1) // 64, -1).max(axis=0)
+    lo[hi < 0] = -1
+    return lo, hi
+
+
+def chunk_extent(chunk_word_lo, chunk_word_hi, K, n, server_begin, server_end):
+    """(lowest word, highest word, highest segment) touched by the chunk
+    owners [server_begin, server_end), from chunk_word_ranges(); the words are
+    -1 if every owned segment is empty."""
+    hi = chunk_word_hi[server_begin:server_end]
+    lo = chunk_word_lo[server_begin:server_end]
+    owned = hi >= 0
+    if not owned.any():
+        return -1, -1, (K - 1) * n + server_end - 1
+    return int(lo[owned].min()), int(hi.max()), (K - 1) * n + server_end - 1
+
+
 class Plan:
     """Layout of K tensors cut into n chunks, with its device tile tables."""
 
@@ -108,6 +136,8 @@ class Plan:
         call("onebit_plan_info", h, None, None, None,
              self.chunk_len.ctypes.data_as(ctypes.c_void_p), None)
         self.numel = numel
+        self.chunk_word_lo, self.chunk_word_hi = chunk_word_ranges(
+            self.seg_begin, self.seg_end, self.K, self.n)
 
     @property
     def workspace_words(self):
@@ -116,15 +146,8 @@ class Plan:
     def chunk_extent(self, server_begin, server_end):
         """(lowest word, highest word, highest segment) touched by the chunk
         owners [server_begin, server_end); words are -1 if all are empty."""
-        wlo, whi = -1, -1
-        for k in range(self.K):
-            for j in range(server_begin, server_end):
-                q = k * self.n + j
-                b, e = int(self.seg_begin[q]), int(self.seg_end[q])
-                if e > b:
-                    wlo = b // 64 if wlo < 0 else min(wlo, b // 64)
-                    whi = max(whi, (e - 1) // 64)
-        return wlo, whi, (self.K - 1) * self.n + server_end - 1
+        return chunk_extent(self.chunk_word_lo, self.chunk_word_hi, self.K, self.n,
+                            server_begin, server_end)
 
     @property
     def handle(self):
@@ -223,22 +246,38 @@ def onebit_decompress_update(plan, server_bits, server_scales, x, m_out, v_froze
 
 def onebit_step(plan, x, m, v_frozen, grads, worker_err, server_err, worker_bits,
                 worker_scales, server_bits, server_scales, lr, beta1, eps, workspace,
-                stream=None):
+                stream=None, events=None):
+    """The fused step.  events: optional four torch.cuda.Event objects
+    (already recorded once, so that their HIP events exist) marked on the
+    stream before the worker pass, the chunk owners' pass and the update, and
+    after the update (onebit_step_events)."""
     n, D, W, S = plan.n, plan.D, plan.W, plan.S
     # the step addresses worker_bits / worker_scales with row strides W and S
     for t, name, cols in ((worker_bits, "worker_bits", W), (worker_scales, "worker_scales", S)):
         if t is not None and t.dim() == 2 and cols > 0 and t.stride(0) != cols:
             raise ValueError("%s must be contiguous [n, %d] for onebit_step" % (name, cols))
-    call("onebit_step", plan.handle, _ptr(x, torch.float32, "x", D),
-         _ptr(m, torch.float32, "m", D), _ptr(v_frozen, torch.float32, "v_frozen", D),
-         *_grads(grads, D, n), _ld(grads),
-         _ptr(worker_err, torch.float32, "worker_err", D, n), _ld(worker_err),
-         _ptr(server_err, torch.float32, "server_err", D),
-         _ptr(worker_bits, torch.int64, "worker_bits", W, n),
-         _ptr(worker_scales, torch.float32, "worker_scales", S, n),
-         _ptr(server_bits, torch.int64, "server_bits", W),
-         _ptr(server_scales, torch.float32, "server_scales", S), lr, beta1, eps,
-         _ptr(workspace, torch.float64, "workspace", plan.workspace_words), _stream(stream))
+    args = [plan.handle, _ptr(x, torch.float32, "x", D),
+            _ptr(m, torch.float32, "m", D), _ptr(v_frozen, torch.float32, "v_frozen", D),
+            *_grads(grads, D, n), _ld(grads),
+            _ptr(worker_err, torch.float32, "worker_err", D, n), _ld(worker_err),
+            _ptr(server_err, torch.float32, "server_err", D),
+            _ptr(worker_bits, torch.int64, "worker_bits", W, n),
+            _ptr(worker_scales, torch.float32, "worker_scales", S, n),
+            _ptr(server_bits, torch.int64, "server_bits", W),
+            _ptr(server_scales, torch.float32, "server_scales", S), lr, beta1, eps,
+            _ptr(workspace, torch.float64, "workspace", plan.workspace_words)]
+    if events is None:
+        call("onebit_step", *args, _stream(stream))
+        return
+    if len(events) != 4:
+        raise ValueError("events must hold four torch.cuda.Event objects")
+    handles = (ctypes.c_void_p * 4)()
+    for k, ev in enumerate(events):
+        if ev is not None:
+            if not ev.cuda_event:
+                raise ValueError("events[%d] has no HIP event yet: record it once first" % k)
+            handles[k] = ev.cuda_event
+    call("onebit_step_events", *args, handles, _stream(stream))
 
 
 def onebit_decode(plan, bits, scales, out, stream=None):
@@ -293,7 +332,9 @@ class State:
     current value either way."""
 
     def __init__(self, plan, device, n_local=None, grad_rows=None, packed_momentum=True,
-                 grad_dtype=torch.float32):
+                 grad_dtype=torch.float32, grads=None):
+        """grads: an existing [rows, >= D] gradient tensor to read (shared,
+        not copied) instead of a new zero one."""
         n = plan.n if n_local is None else n_local
         D, W, S = plan.D, plan.W, plan.S
         f = dict(dtype=torch.float32, device=device)
@@ -302,8 +343,10 @@ class State:
         self.x = torch.zeros(D, **f)
         self.m = torch.zeros(D, **f)
         self.v = torch.zeros(D, **f)
-        self.grads = torch.zeros((n if grad_rows is None else grad_rows, D), dtype=grad_dtype,
-                                 device=device)
+        if grads is None:
+            grads = torch.zeros((n if grad_rows is None else grad_rows, D), dtype=grad_dtype,
+                                device=device)
+        self.grads = grads
         self.worker_err = torch.zeros((n, D), **f)
         self.worker_bits = torch.zeros((n, W), dtype=torch.int64, device=device)
         self.worker_scales = torch.zeros((n, S), **f)
@@ -347,11 +390,13 @@ class State:
     def momentum_is_packed(self):
         return self.packed_momentum and self.compression_steps > 0
 
-    def step(self, lr, beta1, eps, stream=None):
+    def step(self, lr, beta1, eps, stream=None, events=None):
+        """One compression step (onebit_step); events: see onebit_step."""
         m = None if self.momentum_is_packed() else self.m
         onebit_step(self.plan, self.x, m, self.v, self.grads, self.worker_err,
                     self.server_err, self.worker_bits, self.worker_scales, self.server_bits,
-                    self.server_scales, lr, beta1, eps, self.workspace, stream=stream)
+                    self.server_scales, lr, beta1, eps, self.workspace, stream=stream,
+                    events=events)
         self.compression_steps += 1
 
     def step_uncompressed(self, lr, beta1, eps, stream=None):

@@ -13,7 +13,7 @@ import torch
 
 import oracle
 import synth
-from parity_util import check_bits, check_fp, check_scales, host
+from parity_util import SegmentOracle, check_bits, check_fp, check_scales, host
 
 pytestmark = pytest.mark.gpu
 
@@ -30,7 +30,32 @@ def _np(t):
     return np.ascontiguousarray(t.detach().cpu().numpy())
 
 
+def _check_segments(st, so, mom=None, wdelta=None, sdelta=None, final=True):
+    """Device state against the oracle on every sampled segment: sign words
+    bit for bit, scales within 1 ulp, fp32 state within the tolerance."""
+    for sg in so.segs:
+        q, b, e = sg["q"], sg["b"], sg["e"]
+        w0, w1 = b // 64, (e + 63) // 64
+        check_bits("worker bits seg %d" % q, host(st.worker_bits[:so.n, w0:w1]), sg["wbits"])
+        check_bits("server bits seg %d" % q, host(st.server_bits[w0:w1]), sg["sbits"])
+        check_scales("worker scales seg %d" % q, host(st.worker_scales[:so.n, q]), sg["wscales"])
+        check_scales("server scale seg %d" % q, host(st.server_scales[q:q + 1]),
+                     np.array([sg["sscale"]], np.float32))
+        if not final:
+            continue
+        check_fp("x seg %d" % q, _np(st.x[b:e]), sg["x"])
+        check_fp("m seg %d" % q, _np(mom[b:e]), sg["m"])
+        check_fp("worker delta seg %d" % q, _np(wdelta[:so.n, b:e]), sg["delta"])
+        if sdelta is not None:
+            check_fp("server delta seg %d" % q, _np(sdelta[b:e]), sg["dbar"])
+
+
 def _free_run_sampled(ob, dev, wl, warm, steps, sample_segs, grad_dtype=torch.float32):
+    """`warm` Adam warm-up steps, then `steps` compression steps through
+    State.step (the fused onebit_step, packed momentum from the second
+    compression step on: the launch configuration bench.py times), checked
+    against the oracle on whole sampled segments after the warm-up, after
+    every step (sign words and scales) and at the end (all fp32 state)."""
     n = wl.n
     plan = ob.Plan(wl.numel, n)
     L = oracle.Layout(wl.numel, n)
@@ -40,67 +65,45 @@ def _free_run_sampled(ob, dev, wl, warm, steps, sample_segs, grad_dtype=torch.fl
     st = ob.State(plan, dev, grad_dtype=grad_dtype)
     scale_vec = torch.from_numpy(synth.grad_scale_per_element(wl, plan.D, plan.tensor_off)).to(dev)
     st.x.copy_(synth.device_params(wl, plan.D, dev))
-    segs = []
-    for q in sample_segs:
-        b, e = int(L.seg_begin[q]), int(L.seg_end[q])
-        assert e > b
-        segs.append(dict(q=q, b=b, e=e, ln=e - b, x=_np(st.x[b:e]),
-                         m=np.zeros(e - b, np.float32), v=np.zeros(e - b, np.float32)))
-    for t in range(1, warm + 1):
-        synth.device_grads(wl, plan.D, plan.tensor_off, t, st.grads, scale_vec)
-        for sg in segs:
-            g = _np(st.grads[:, sg["b"]:sg["e"]])
-            oracle.warmup_range(0, sg["ln"], sg["x"], sg["m"], sg["v"], g, sg["ln"], n,
-                                wl.lr, wl.beta1, wl.beta2, wl.eps, 0, t)
-        st.warmup(wl.lr, wl.beta1, wl.beta2, wl.eps, t)
-    torch.cuda.synchronize()
-    for sg in segs:
-        b, e = sg["b"], sg["e"]
-        check_fp("warm-up x seg %d" % sg["q"], _np(st.x[b:e]), sg["x"])
-        check_fp("warm-up v seg %d" % sg["q"], _np(st.v[b:e]), sg["v"])
-        nw = (sg["ln"] + 63) // 64
-        sg.update(delta=np.zeros((n, sg["ln"]), np.float32), dbar=np.zeros(sg["ln"], np.float32),
-                  wbits=np.zeros((n, nw), np.uint64), wscales=np.zeros(n, np.float32),
-                  sbits=np.zeros(nw, np.uint64), z=np.zeros(sg["ln"], np.float32))
-    for t in range(warm + 1, warm + steps + 1):
-        synth.device_grads(wl, plan.D, plan.tensor_off, t, st.grads, scale_vec)
-        for sg in segs:
-            g = _np(st.grads[:, sg["b"]:sg["e"]])
-            for i in range(n):
-                sg["wscales"][i] = oracle.worker_segment(0, sg["ln"], wl.beta1, sg["m"], g[i],
-                                                         sg["delta"][i], sg["wbits"][i], sg["z"])
-            del g
-            sg["sscale"] = oracle.server_segment(0, sg["ln"], n, sg["wbits"].reshape(-1),
-                                                 sg["wbits"].shape[1], sg["wscales"], 1,
-                                                 sg["dbar"], sg["sbits"], sg["z"])
-            oracle.update_segment(0, sg["ln"], sg["sbits"], sg["sscale"], wl.lr, wl.eps,
-                                  sg["x"], sg["m"], sg["v"])
-        st.step(wl.lr, wl.beta1, wl.eps)
-    torch.cuda.synchronize()
-    wdelta = st.worker_delta()
-    sdelta = st.server_delta()
-    mom = st.momentum()
-    torch.cuda.synchronize()
-    for sg in segs:
-        q, b, e = sg["q"], sg["b"], sg["e"]
-        w0, w1 = b // 64, (e + 63) // 64
-        check_bits("worker bits seg %d" % q, host(st.worker_bits[:, w0:w1]), sg["wbits"])
-        check_bits("server bits seg %d" % q, host(st.server_bits[w0:w1]), sg["sbits"])
-        check_scales("worker scales seg %d" % q, host(st.worker_scales[:, q]), sg["wscales"])
-        check_scales("server scale seg %d" % q, host(st.server_scales[q:q + 1]),
-                     np.array([sg["sscale"]], np.float32))
-        check_fp("x seg %d" % q, _np(st.x[b:e]), sg["x"])
-        check_fp("m seg %d" % q, _np(mom[b:e]), sg["m"])
-        check_fp("worker delta seg %d" % q, _np(wdelta[:, b:e]), sg["delta"])
-        check_fp("server delta seg %d" % q, _np(sdelta[b:e]), sg["dbar"])
-    del wdelta, sdelta, mom, st
-    plan.close()
-    torch.cuda.empty_cache()
+    so = SegmentOracle(L, sample_segs, lambda b, e: _np(st.x[b:e]), n)
+    grads = lambda b, e: _np(st.grads[:, b:e])
+    try:
+        for t in range(1, warm + 1):
+            synth.device_grads(wl, plan.D, plan.tensor_off, t, st.grads, scale_vec)
+            so.warmup(grads, t, wl.lr, wl.beta1, wl.beta2, wl.eps)
+            st.warmup(wl.lr, wl.beta1, wl.beta2, wl.eps, t)
+        torch.cuda.synchronize()
+        for sg in so.segs:
+            b, e = sg["b"], sg["e"]
+            check_fp("warm-up x seg %d" % sg["q"], _np(st.x[b:e]), sg["x"])
+            check_fp("warm-up m seg %d" % sg["q"], _np(st.m[b:e]), sg["m"])
+            check_fp("warm-up v seg %d" % sg["q"], _np(st.v[b:e]), sg["v"])
+        for t in range(warm + 1, warm + steps + 1):
+            synth.device_grads(wl, plan.D, plan.tensor_off, t, st.grads, scale_vec)
+            so.step(grads, wl.lr, wl.beta1, wl.eps)
+            st.step(wl.lr, wl.beta1, wl.eps)
+            torch.cuda.synchronize()
+            _check_segments(st, so, final=False)
+            print("%s step %d ok" % (wl.name, t), flush=True)
+        assert st.momentum_is_packed() == (steps > 1)
+        wdelta = st.worker_delta()
+        sdelta = st.server_delta()
+        mom = st.momentum()
+        torch.cuda.synchronize()
+        _check_segments(st, so, mom, wdelta, sdelta)
+        del wdelta, sdelta, mom
+    finally:
+        so.close()
+        del st
+        plan.close()
+        torch.cuda.empty_cache()
 
 
 def test_bert_large_full_size(ob, dev):
-    """d = 334,088,192, n = 32: first and last of the 32 chunks."""
-    _free_run_sampled(ob, dev, synth.get("bert_large"), warm=2, steps=2, sample_segs=[0, 31])
+    """d = 334,088,192, n = 32, 5 warm-up + 10 compression steps: the first,
+    a middle and the last of the 32 chunks."""
+    wl = synth.get("bert_large")
+    _free_run_sampled(ob, dev, wl, warm=wl.warmup_steps, steps=10, sample_segs=[0, 15, 31])
 
 
 def test_bert_large_full_size_bf16_grads(ob, dev):
@@ -118,13 +121,16 @@ def test_bert_base_full_size_fp16_grads(ob, dev):
 
 
 def test_bert_base_full_size(ob, dev):
-    """d = 108,888,576, n = 16: the last chunk is the short one."""
-    _free_run_sampled(ob, dev, synth.get("bert_base"), warm=2, steps=3, sample_segs=[0, 15])
+    """d = 108,888,576, n = 16, 5 warm-up + 10 compression steps: the first,
+    a middle and the last (short) chunk."""
+    wl = synth.get("bert_base")
+    _free_run_sampled(ob, dev, wl, warm=wl.warmup_steps, steps=10, sample_segs=[0, 7, 15])
 
 
 def test_stress_full_size(ob, dev):
-    """All 5,000 tensors (per-tensor chunking, n = 8): a few segments of
-    small, medium and large tensors, including a tensor's short last chunk."""
+    """All 5,000 tensors (per-tensor chunking, n = 8), 5 warm-up + 10
+    compression steps: segments of the smallest, a median, the largest and
+    the last tensor, each tensor's first and last non-empty chunk."""
     wl = synth.get("stress")
     L = oracle.Layout(wl.numel, wl.n)
     order = np.argsort(wl.numel)
@@ -137,97 +143,123 @@ def test_stress_full_size(ob, dev):
                 if j == 0:
                     picks.append(q)
         picks.append(last)
-    _free_run_sampled(ob, dev, wl, warm=2, steps=3, sample_segs=sorted(set(picks)))
+    _free_run_sampled(ob, dev, wl, warm=wl.warmup_steps, steps=10,
+                      sample_segs=sorted(set(picks)))
 
 
 def test_share256_full_size(ob, dev):
-    """One GPU's share of a 256-worker BERT-Large step at its real shape: the
+    """One GPU's share of a 256-worker BERT-Large run at its real shape, in
+    bench.py's calls: 5 warm-up steps of the local worker, then 10
+    compression steps (fp32 momentum first, then packed), each with the
     local worker over all d, the owner of chunk 0 reducing 256 incoming
-    packed chunks (synthetic, seeded), and the update over all d with the
-    other 255 gathered chunks synthetic as well."""
+    packed chunks (synthetic, seeded per step), and the update over all d
+    with the other 255 gathered chunks synthetic as well."""
     wl = synth.get("share256")
     n, j = wl.n, wl.server_chunk
     plan = ob.Plan(wl.numel, n)
     L = oracle.Layout(wl.numel, n)
-    D, W = plan.D, plan.W
+    D, W, S = plan.D, plan.W, plan.S
     st = ob.State(plan, dev, n_local=1)
     scale_vec = torch.from_numpy(synth.grad_scale_per_element(wl, D, plan.tensor_off)).to(dev)
     st.x.copy_(synth.device_params(wl, D, dev))
-    sample = [0, 77, 255]
-    segs = {q: dict(b=int(L.seg_begin[q]), e=int(L.seg_end[q])) for q in sample}
-    for q, sg in segs.items():
-        sg["ln"] = sg["e"] - sg["b"]
-        sg["x"] = _np(st.x[sg["b"]:sg["e"]])
-        sg["m"] = np.zeros(sg["ln"], np.float32)
-        sg["v"] = np.zeros(sg["ln"], np.float32)
-    warm = 2
-    for t in range(1, warm + 1):
-        synth.device_grads(wl, D, plan.tensor_off, t, st.grads, scale_vec)
-        for sg in segs.values():
-            g = _np(st.grads[:, sg["b"]:sg["e"]])
-            oracle.warmup_range(0, sg["ln"], sg["x"], sg["m"], sg["v"], g, sg["ln"], 1,
-                                wl.lr, wl.beta1, wl.beta2, wl.eps, 0, t)
-        st.warmup(wl.lr, wl.beta1, wl.beta2, wl.eps, t)
-    # one compression step
-    synth.device_grads(wl, D, plan.tensor_off, warm + 1, st.grads, scale_vec)
-    ob.onebit_worker_compress(plan, st.m, st.grads, st.worker_err, st.worker_bits,
-                              st.worker_scales, wl.beta1, st.workspace)  # first step: fp32 m
+    so = SegmentOracle(L, [0, 77, 255], lambda b, e: _np(st.x[b:e]), 1)
+    grads = lambda b, e: _np(st.grads[:, b:e])
     b0, e0 = int(L.seg_begin[j]), int(L.seg_end[j])
     cw0, cw1 = b0 // 64, (e0 + 63) // 64
-    recv_bits, recv_scales = synth.device_bits_and_scales(n, cw1 - cw0, wl.seed_incoming, dev)
-    # what the all-gather would bring for the other chunks
-    gath_bits, gath_scales = synth.device_bits_and_scales(1, W, wl.seed_incoming + 1, dev)
-    st.server_bits.copy_(gath_bits[0])
-    st.server_scales.copy_(gath_scales.expand(plan.S) * torch.linspace(0.5, 1.5, plan.S, device=dev))
-    # the owned chunk's scale is part of the server error state: zero at the
-    # first compression step, like the zero server error buffer
-    st.server_scales[j] = 0.0
-    ob.onebit_server_reduce_compress(plan, j, j + 1, recv_bits, recv_scales, st.server_err,
-                                     st.server_bits, st.server_scales, st.workspace,
-                                     bits_word_base=cw0, scales_seg_base=j, scales_ld=1)
-    x_before_update = {q: _np(st.x[sg["b"]:sg["e"]]) for q, sg in segs.items()}
-    ob.onebit_decompress_update(plan, st.server_bits, st.server_scales, st.x, st.m, st.v,
-                                wl.lr, wl.eps)
-    torch.cuda.synchronize()
-    # oracle: the local worker on the sampled segments
-    gh = {q: _np(st.grads[0, sg["b"]:sg["e"]]) for q, sg in segs.items()}
-    for q, sg in segs.items():
-        nw = (sg["ln"] + 63) // 64
-        delta = np.zeros(sg["ln"], np.float32)
-        bits = np.zeros(nw, np.uint64)
-        z = np.zeros(sg["ln"], np.float32)
-        s = oracle.worker_segment(0, sg["ln"], wl.beta1, sg["m"], gh[q], delta, bits, z)
-        w0, w1 = sg["b"] // 64, (sg["e"] + 63) // 64
-        check_bits("worker bits seg %d" % q, host(st.worker_bits[0, w0:w1]), bits)
-        check_scales("worker scale seg %d" % q, host(st.worker_scales[0, q:q + 1]),
-                     np.array([s], np.float32))
-        sg["delta"] = delta
-        check_fp("warm-up x seg %d" % q, x_before_update[q], sg["x"])
-        check_fp("v seg %d" % q, _np(st.v[sg["b"]:sg["e"]]), sg["v"])
-    # oracle: the owner of chunk j from the received rows
-    rb = host(recv_bits).copy()
-    rs = _np(recv_scales)
-    ln0 = e0 - b0
-    dbar = np.zeros(ln0, np.float32)
-    sb = np.zeros(cw1 - cw0, np.uint64)
-    z = np.zeros(ln0, np.float32)
-    s_bar = oracle.server_segment(0, ln0, n, rb.reshape(-1), cw1 - cw0, rs, 1, dbar, sb, z)
-    check_bits("server bits chunk %d" % j, host(st.server_bits[cw0:cw1]), sb)
-    check_scales("server scale chunk %d" % j, host(st.server_scales[j:j + 1]),
-                 np.array([s_bar], np.float32))
-    check_fp("server delta chunk %d" % j, _np(st.server_delta()[b0:e0]), dbar)
-    # oracle: the update on the sampled segments with the gathered words
-    sbits_all = host(st.server_bits)
-    sscales_all = _np(st.server_scales)
-    for q, sg in segs.items():
-        w0, w1 = sg["b"] // 64, (sg["e"] + 63) // 64
-        x = x_before_update[q].copy()
-        m = np.zeros(sg["ln"], np.float32)
-        oracle.update_segment(0, sg["ln"], np.ascontiguousarray(sbits_all[w0:w1]),
-                              sscales_all[q], wl.lr, wl.eps, x, m, sg["v"])
-        check_fp("x seg %d" % q, _np(st.x[sg["b"]:sg["e"]]), x)
-        check_fp("m seg %d" % q, _np(st.m[sg["b"]:sg["e"]]), m)
-    del st
+    assert cw0 == 0 and S == n  # one flat tensor: segment q is chunk q
+    try:
+        for t in range(1, wl.warmup_steps + 1):
+            synth.device_grads(wl, D, plan.tensor_off, t, st.grads, scale_vec)
+            so.warmup(grads, t, wl.lr, wl.beta1, wl.beta2, wl.eps)
+            st.warmup(wl.lr, wl.beta1, wl.beta2, wl.eps, t)
+        torch.cuda.synchronize()
+        for sg in so.segs:
+            check_fp("warm-up x seg %d" % sg["q"], _np(st.x[sg["b"]:sg["e"]]), sg["x"])
+            check_fp("warm-up v seg %d" % sg["q"], _np(st.v[sg["b"]:sg["e"]]), sg["v"])
+        for k in range(10):
+            t = wl.warmup_steps + 1 + k
+            synth.device_grads(wl, D, plan.tensor_off, t, st.grads, scale_vec)
+            so.workers(grads, wl.beta1)
+            if k == 0:
+                ob.onebit_worker_compress(plan, st.m, st.grads, st.worker_err, st.worker_bits,
+                                          st.worker_scales, wl.beta1, st.workspace)
+            else:
+                ob.onebit_worker_compress(plan, None, st.grads, st.worker_err, st.worker_bits,
+                                          st.worker_scales, wl.beta1, st.workspace,
+                                          m_bits=st.server_bits, m_scales=st.server_scales)
+            recv_bits, recv_scales = synth.device_bits_and_scales(n, cw1 - cw0,
+                                                                  wl.seed_incoming + 2 * t, dev)
+            ob.onebit_server_reduce_compress(plan, j, j + 1, recv_bits, recv_scales,
+                                             st.server_err, st.server_bits, st.server_scales,
+                                             st.workspace, bits_word_base=cw0,
+                                             scales_seg_base=j, scales_ld=1)
+            # what the all-gather brings for the other 255 chunks this step
+            gbits, _ = synth.device_bits_and_scales(1, W - cw1, wl.seed_incoming + 2 * t + 1, dev)
+            _, gscales = synth.device_bits_and_scales(S - 1, 1, wl.seed_incoming + 2 * t + 1, dev)
+            st.server_bits[cw1:] = gbits[0]
+            st.server_scales[j + 1:] = gscales
+            ob.onebit_decompress_update(plan, st.server_bits, st.server_scales, st.x, None, st.v,
+                                        wl.lr, wl.eps)
+            sbits_h, sscales_h = host(st.server_bits), _np(st.server_scales)
+            gathered = {sg["q"]: (sbits_h[sg["b"] // 64:(sg["e"] + 63) // 64], sscales_h[sg["q"]])
+                        for sg in so.segs if sg["q"] != j}
+            so.owners_and_updates(wl.lr, wl.eps, received={j: (host(recv_bits), _np(recv_scales))},
+                                  gathered=gathered)
+            torch.cuda.synchronize()
+            _check_segments(st, so, final=False)
+            print("share256 step %d ok" % t, flush=True)
+        wdelta = st.worker_delta()
+        sdelta = st.server_delta()
+        mom = torch.zeros_like(st.m)
+        ob.onebit_decode(plan, st.server_bits, st.server_scales, mom)
+        torch.cuda.synchronize()
+        # the server error exists only for the owned chunk
+        _check_segments(st, so, mom, wdelta, None)
+        sg0 = so.segs[0]
+        assert sg0["q"] == j
+        check_fp("server delta chunk %d" % j, _np(sdelta[b0:e0]), sg0["dbar"])
+        del wdelta, sdelta, mom
+    finally:
+        so.close()
+        del st
+        plan.close()
+        torch.cuda.empty_cache()
+
+
+def test_bert_large_two_states_bitwise(ob, dev):
+    """Two States fed identical BERT-Large inputs (one shared gradient
+    tensor) run 3 compression steps, the first with the fp32 momentum
+    (k_worker_rows at its full grid) and two packed: every sign word, scale
+    and element of x and both error states agree bit for bit over all of d
+    and all 32 rows.  A regression test of run-to-run determinism at the
+    benchmark's grid size."""
+    wl = synth.get("bert_large")
+    plan = ob.Plan(wl.numel, wl.n)
+    a = ob.State(plan, dev)
+    b = ob.State(plan, dev, grads=a.grads)
+    scale_vec = torch.from_numpy(synth.grad_scale_per_element(wl, plan.D, plan.tensor_off)).to(dev)
+    a.x.copy_(synth.device_params(wl, plan.D, dev))
+    synth.device_grads(wl, plan.D, plan.tensor_off, 1, a.grads, scale_vec)
+    a.warmup(wl.lr, wl.beta1, wl.beta2, wl.eps, 1)
+    for name in ("x", "m", "v"):
+        getattr(b, name).copy_(getattr(a, name))
+    names = ("x", "worker_err", "worker_bits", "worker_scales", "server_err", "server_bits",
+             "server_scales")
+    for t in (2, 3, 4):
+        synth.device_grads(wl, plan.D, plan.tensor_off, t, a.grads, scale_vec)
+        a.step(wl.lr, wl.beta1, wl.eps)
+        b.step(wl.lr, wl.beta1, wl.eps)
+        torch.cuda.synchronize()
+        for name in names:
+            u, w = getattr(a, name), getattr(b, name)
+            if u.dtype == torch.float32:
+                u, w = u.view(torch.int32), w.view(torch.int32)
+            same = torch.equal(u, w)
+            if not same:
+                diff = int((u != w).sum())
+                raise AssertionError("step %d: %s differs in %d of %d elements"
+                                     % (t, name, diff, u.numel()))
+    del a, b
     plan.close()
     torch.cuda.empty_cache()
 

@@ -37,12 +37,18 @@ def test_step_replays_from_a_hip_graph(dev):
     x0 = torch.from_numpy(synth.host_params(wl, plan.D)).to(dev)
     for st in states:
         st.x.copy_(x0)
+    # Algorithm 1's order: both warm-up steps, then (v frozen) the first
+    # compression step eagerly, with the warm-up's fp32 momentum
     for t in (1, 2):
         g = torch.from_numpy(synth.host_grads(wl, plan.D, plan.tensor_off, t)).to(dev)
         for st in states:
             st.grads.copy_(g)
             st.warmup(wl.lr, wl.beta1, wl.beta2, wl.eps, t)
-            st.step(wl.lr, wl.beta1, wl.eps)  # first compression step, eager (fp32 momentum)
+    g = torch.from_numpy(synth.host_grads(wl, plan.D, plan.tensor_off, 3)).to(dev)
+    for st in states:
+        st.grads.copy_(g)
+        st.step(wl.lr, wl.beta1, wl.eps)
+        assert st.momentum_is_packed()  # the next step decodes m from the message
     torch.cuda.synchronize()
     eager, graphed = states
     graph = torch.cuda.CUDAGraph()
@@ -269,4 +275,53 @@ def test_plan_without_elements(dev):
     torch.cuda.synchronize()
     assert not host(st.worker_scales).any() and not host(st.server_scales).any()
     assert st.momentum().numel() == 0 and st.worker_delta().numel() == 0
+    plan.close()
+
+
+def test_step_events_form_matches_plain_step(dev):
+    """onebit_step_events runs the launches of onebit_step bit for bit and
+    marks the stream in order around the three phases."""
+    import paper_2102_02888_amd as ob
+    from paper_2102_02888_amd import _native
+    numel, n = [300_000, 5000, 64], 4
+    plan = ob.Plan(numel, n)
+    wl = synth.Workload(name="events", numel=numel, n=n, warmup_steps=1, steps=0)
+    states = [ob.State(plan, dev), ob.State(plan, dev)]
+    x0 = torch.from_numpy(synth.host_params(wl, plan.D)).to(dev)
+    g = torch.from_numpy(synth.host_grads(wl, plan.D, plan.tensor_off, 1)).to(dev)
+    for st in states:
+        st.x.copy_(x0)
+        st.grads.copy_(g)
+        st.warmup(wl.lr, wl.beta1, wl.beta2, wl.eps, 1)
+    events = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
+    for e in events:
+        e.record()
+    for t in (2, 3, 4):
+        g = torch.from_numpy(synth.host_grads(wl, plan.D, plan.tensor_off, t)).to(dev)
+        for st in states:
+            st.grads.copy_(g)
+        states[0].step(wl.lr, wl.beta1, wl.eps)
+        states[1].step(wl.lr, wl.beta1, wl.eps, events=events)
+        torch.cuda.synchronize()
+        for name in ("x", "m", "worker_err", "worker_bits", "worker_scales", "server_err",
+                     "server_bits", "server_scales"):
+            a, b = host(getattr(states[0], name)), host(getattr(states[1], name))
+            assert a.tobytes() == b.tobytes(), (t, name)
+        spans = [events[k].elapsed_time(events[k + 1]) for k in range(3)]
+        assert all(s >= 0 for s in spans) and spans[0] > 0, spans
+    # a NULL event array is refused before any launch
+    st = states[1]
+    before = host(st.x).copy()
+    vp = ctypes.c_void_p
+    L = _native.lib()
+    rc = L.onebit_step_events(plan.handle, vp(st.x.data_ptr()), None, vp(st.v.data_ptr()),
+                              vp(st.grads.data_ptr()), 0, plan.D, vp(st.worker_err.data_ptr()),
+                              plan.D, vp(st.server_err.data_ptr()),
+                              vp(st.worker_bits.data_ptr()), vp(st.worker_scales.data_ptr()),
+                              vp(st.server_bits.data_ptr()), vp(st.server_scales.data_ptr()),
+                              1e-3, 0.9, 1e-8, vp(st.workspace.data_ptr()), None,
+                              vp(torch.cuda.current_stream().cuda_stream))
+    torch.cuda.synchronize()
+    assert rc == -1 and b"events" in L.onebit_last_error()
+    assert host(st.x).tobytes() == before.tobytes()
     plan.close()

@@ -487,6 +487,55 @@ def test_hand_worked_example_on_gpu(ob, dev):
     plan.close()
 
 
+def test_eps_placement_on_gpu(ob, dev):
+    """tests/golden/eps_placement.json through the ABI: the warm-up divides by
+    sqrt(v) + eps, the compression update by sqrt(v_frozen + eps), exactly."""
+    import json
+    import os
+    gd = json.load(open(os.path.join(os.path.dirname(__file__), "golden", "eps_placement.json")))
+    su = gd["warmup"]
+    k = su["tensor_numel"][0]
+    plan = ob.Plan(su["tensor_numel"], su["n_workers"])
+    st = ob.State(plan, dev)
+    st.x[:k] = torch.tensor(su["x"])
+    for t, sd in enumerate(su["steps"], start=1):
+        st.grads.zero_()
+        st.grads[:, :k] = torch.tensor(sd["grads"])
+        st.warmup(su["lr"], su["beta1"], su["beta2"], su["eps"], t,
+                  bias_correction=su["bias_correction"])
+        torch.cuda.synchronize()
+        assert host(st.m)[:k].tolist() == sd["m"]
+        assert host(st.v)[:k].tolist() == sd["v"]
+        assert host(st.x)[:k].tolist() == sd["x"]
+    plan.close()
+    su = gd["compression"]
+    plan = ob.Plan(su["tensor_numel"], su["n_workers"])
+    st = ob.State(plan, dev)
+    st.x[:2] = torch.tensor(su["x"])
+    st.m[:2] = torch.tensor(su["m"])
+    st.v[:2] = torch.tensor(su["v_frozen"])
+    for sd in su["steps"]:
+        st.grads.zero_()
+        st.grads[:, :2] = torch.tensor(sd["grads"])
+        st.step(su["lr"], su["beta1"], su["eps"])
+        torch.cuda.synchronize()
+        assert float(host(st.server_scales)[0]) == sd["server_scale_chunk0"]
+        assert int(host(st.server_bits)[0]) == sd["server_bits_word0"]
+        assert host(st.x)[:2].tolist() == sd["x"]
+        assert host(st.momentum())[:2].tolist() == sd["m"]
+    # the update call alone, from the first step's message
+    x = torch.zeros(plan.D, dtype=torch.float32, device=dev)
+    x[:2] = torch.tensor(su["x"])
+    bits = torch.zeros(plan.W, dtype=torch.int64, device=dev)
+    bits[0] = su["steps"][0]["server_bits_word0"]
+    scales = torch.zeros(plan.S, dtype=torch.float32, device=dev)
+    scales[0] = su["steps"][0]["server_scale_chunk0"]
+    ob.onebit_decompress_update(plan, bits, scales, x, None, st.v, su["lr"], su["eps"])
+    torch.cuda.synchronize()
+    assert host(x)[:2].tolist() == su["steps"][0]["x"]
+    plan.close()
+
+
 def _random_config(seed):
     rng = np.random.default_rng(1000 + seed)
     k = int(rng.integers(1, 21))

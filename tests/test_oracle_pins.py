@@ -167,6 +167,51 @@ def test_hand_worked_two_steps():
     assert not st.x[2:].any() and not st.delta[:, 2:].any()
 
 
+def test_eps_placement_warmup():
+    """tests/golden/eps_placement.json, warm-up part: eq. (alg:v) divides by
+    sqrt(v) + eps; the hand-worked values differ from sqrt(v + eps)'s."""
+    su = _golden("eps_placement.json")["warmup"]
+    L = oracle.Layout(su["tensor_numel"], su["n_workers"])
+    k = su["tensor_numel"][0]
+    x = np.zeros(L.D, np.float32); x[:k] = su["x"]
+    m = np.zeros(L.D, np.float32); m[:k] = su["m"]
+    v = np.zeros(L.D, np.float32); v[:k] = su["v"]
+    g = np.zeros((su["n_workers"], L.D), np.float32)
+    for t, sd in enumerate(su["steps"], start=1):
+        g[:, :k] = sd["grads"]
+        oracle.warmup_step(L, x, m, v, g, su["n_workers"], su["lr"], su["beta1"], su["beta2"],
+                           su["eps"], su["bias_correction"], t)
+        np.testing.assert_array_equal(m[:k], sd["m"])
+        np.testing.assert_array_equal(v[:k], sd["v"])
+        np.testing.assert_array_equal(x[:k], sd["x"])
+    # the other placement of eps would move x[0] to 1 - 0.5/sqrt(2) at step 1
+    assert su["steps"][0]["x"][0] != np.float32(1 - 0.5 / np.sqrt(2.0))
+
+
+def test_eps_placement_compression_update():
+    """tests/golden/eps_placement.json, compression part: Algorithm 1's final
+    step divides the decoded momentum by sqrt(v_frozen + eps)."""
+    su = _golden("eps_placement.json")["compression"]
+    L = oracle.Layout(su["tensor_numel"], su["n_workers"])
+    x = np.zeros(L.D, np.float32); x[:2] = su["x"]
+    m = np.zeros(L.D, np.float32); m[:2] = su["m"]
+    v = np.zeros(L.D, np.float32); v[:2] = su["v_frozen"]
+    st = oracle.State(L, x, m, v)
+    g = np.zeros((su["n_workers"], L.D), np.float32)
+    for sd in su["steps"]:
+        g[:, :2] = sd["grads"]
+        st.step(g, lr=su["lr"], beta1=su["beta1"], eps=su["eps"])
+        assert st.sscales[0] == sd["server_scale_chunk0"]
+        assert int(st.sbits[0]) == sd["server_bits_word0"]
+        np.testing.assert_array_equal(st.x[:2], sd["x"])
+        np.testing.assert_array_equal(st.m[:2], sd["m"])
+    # and the update alone, from the first step's message: sqrt(v + eps) = [2, 4]
+    x1 = np.array(su["x"], np.float32)
+    oracle.update_segment(0, 2, np.array([3], np.uint64), 13.0, su["lr"], su["eps"], x1,
+                          None, np.array(su["v_frozen"], np.float32))
+    np.testing.assert_array_equal(x1, su["steps"][0]["x"])
+
+
 # ---------------------------------------------------------------------------
 # Error-feedback identity and telescoping (appendix "Proof to the updating form")
 # ---------------------------------------------------------------------------
