@@ -186,16 +186,44 @@ __device__ __forceinline__ float error_of(float z, float s) { return z >= 0.f ? 
 // without a tile keep the pace.  Every wave of a workgroup runs the same row
 // loop, so every wave reaches every barrier.
 // ---------------------------------------------------------------------------
-// sum += one gradient row of the tile (fp64, in row order)
+// One gradient row of the tile as fp32 (zeros past the tile when !FULL).
 template <bool FULL, class G>
-__device__ __forceinline__ void add_row(double (&sum)[kSubBlocks][4],
-                                        const typename G::T *__restrict__ row, int lane, int len)
+__device__ __forceinline__ void load_grad_row(v4f (&gv)[kSubBlocks],
+                                              const typename G::T *__restrict__ row, int lane,
+                                              int len)
 {
 #pragma unroll
-    for (int b = 0; b < kSubBlocks; ++b) {
-        const v4f gv = ldg4<FULL, G>(row, b * (kWave * 4) + 4 * lane, len);
+    for (int b = 0; b < kSubBlocks; ++b) gv[b] = ldg4<FULL, G>(row, b * (kWave * 4) + 4 * lane, len);
+}
+
+// sum += one loaded gradient row (fp64, rows added in row order)
+__device__ __forceinline__ void add_grad_row(double (&sum)[kSubBlocks][4],
+                                             const v4f (&gv)[kSubBlocks])
+{
 #pragma unroll
-        for (int c = 0; c < 4; ++c) sum[b][c] += (double)gv[c];
+    for (int b = 0; b < kSubBlocks; ++b)
+#pragma unroll
+        for (int c = 0; c < 4; ++c) sum[b][c] += (double)gv[b][c];
+}
+
+// sum = the n gradient rows of the tile, added in row order, with a
+// workgroup barrier after every row; every wave runs the same number of
+// barriers (active: the wave has a tile).  Issuing row i+1's loads before
+// adding row i measured the same (8.79 against 8.74 ms on the BERT-Large
+// shape, same buffers), and without the barriers the pass is 6% slower.
+template <bool FULL, class G>
+__device__ __forceinline__ void warmup_rows_walk(double (&sum)[kSubBlocks][4], const Tile &tile,
+                                                 int lane, bool active,
+                                                 const typename G::T *__restrict__ g,
+                                                 int64_t g_ld, int n)
+{
+    for (int i = 0; i < n; ++i) {
+        if (active) {
+            v4f gv[kSubBlocks];
+            load_grad_row<FULL, G>(gv, g + tile.start + (int64_t)i * g_ld, lane, tile.len);
+            add_grad_row(sum, gv);
+        }
+        __builtin_amdgcn_s_barrier();  // the workgroup reads each row together
     }
 }
 
@@ -442,14 +470,10 @@ __global__ __launch_bounds__(kRowBlock) void k_warmup(
     for (int b = 0; b < kSubBlocks; ++b)
 #pragma unroll
         for (int c = 0; c < 4; ++c) sum[b][c] = 0.0;
-    for (int i = 0; i < n_grads; ++i) {
-        const typename G::T *row = g + (int64_t)i * g_ld + tile.start;
-        if (full)
-            add_row<true, G>(sum, row, lane, tile.len);
-        else if (active)
-            add_row<false, G>(sum, row, lane, tile.len);
-        __builtin_amdgcn_s_barrier();  // the workgroup reads each row together
-    }
+    if (full)
+        warmup_rows_walk<true, G>(sum, tile, lane, true, g, g_ld, n_grads);
+    else
+        warmup_rows_walk<false, G>(sum, tile, lane, active, g, g_ld, n_grads);
     if (!active) return;
     const double dn = (double)n_grads;
     if (full)
@@ -506,28 +530,41 @@ __device__ __forceinline__ void beta1_momentum(v4f (&bm)[kSubBlocks], const Tile
 
 // Worker i's row of the tile: z_i from the momentum term bm = beta1 m, the
 // gradient row and the previous compensated value; its sign words, tile sum
-// of squares and new compensated value.
+// of squares and new compensated value.  Split into the loads of the row and
+// the arithmetic and stores, so that a caller can issue the next row's loads
+// before this row's stores.
 template <bool FULL, class G>
-__device__ __forceinline__ void worker_row(
-    const Tile &tile, int64_t t, int lane, int64_t num_tiles, const v4f (&bm)[kSubBlocks], int i,
-    const typename G::T *__restrict__ g, int64_t g_ld, float *__restrict__ err, int64_t err_ld,
-    const float *__restrict__ scales, int64_t scales_ld, uint64_t *__restrict__ bits,
-    int64_t bits_ld, double *__restrict__ partial, float omb1)
+__device__ __forceinline__ void worker_row_load(const Tile &tile, int lane, int i,
+                                                const typename G::T *__restrict__ g, int64_t g_ld,
+                                                const float *__restrict__ err, int64_t err_ld,
+                                                const float *__restrict__ scales,
+                                                int64_t scales_ld, v4f (&gv)[kSubBlocks],
+                                                v4f (&cv)[kSubBlocks], float &sp)
 {
     const int len = tile.len;
-    const int64_t base = tile.start;
-    const int nwords = (len + 63) >> 6;
-    const float sp = scales[(int64_t)i * scales_ld + tile.seg];
-    const typename G::T *gi = g + (int64_t)i * g_ld + base;
-    float *ei = err + (int64_t)i * err_ld + base;
-    uint64_t *bi = bits + (int64_t)i * bits_ld + (base >> 6);
-    v4f gv[kSubBlocks], cv[kSubBlocks];
+    sp = scales[(int64_t)i * scales_ld + tile.seg];
+    const typename G::T *gi = g + (int64_t)i * g_ld + tile.start;
+    const float *ei = err + (int64_t)i * err_ld + tile.start;
 #pragma unroll
     for (int b = 0; b < kSubBlocks; ++b) {
         const int li = b * (kWave * 4) + 4 * lane;
         gv[b] = ldg4<FULL, G>(gi, li, len);
         cv[b] = ld4<FULL>(ei, li, len);
     }
+}
+
+template <bool FULL>
+__device__ __forceinline__ void worker_row_store(
+    const Tile &tile, int64_t t, int lane, int64_t num_tiles, const v4f (&bm)[kSubBlocks], int i,
+    const v4f (&gv)[kSubBlocks], const v4f (&cv)[kSubBlocks], float sp, float *__restrict__ err,
+    int64_t err_ld, uint64_t *__restrict__ bits, int64_t bits_ld, double *__restrict__ partial,
+    float omb1)
+{
+    const int len = tile.len;
+    const int64_t base = tile.start;
+    const int nwords = (len + 63) >> 6;
+    float *ei = err + (int64_t)i * err_ld + base;
+    uint64_t *bi = bits + (int64_t)i * bits_ld + (base >> 6);
     double acc = 0.0;
 #pragma unroll
     for (int b = 0; b < kSubBlocks; ++b) {
@@ -553,6 +590,20 @@ __device__ __forceinline__ void worker_row(
     }
     acc = wave_sum(acc);
     if (lane == 0) partial[(int64_t)i * num_tiles + t] = acc;
+}
+
+template <bool FULL, class G>
+__device__ __forceinline__ void worker_row(
+    const Tile &tile, int64_t t, int lane, int64_t num_tiles, const v4f (&bm)[kSubBlocks], int i,
+    const typename G::T *__restrict__ g, int64_t g_ld, float *__restrict__ err, int64_t err_ld,
+    const float *__restrict__ scales, int64_t scales_ld, uint64_t *__restrict__ bits,
+    int64_t bits_ld, double *__restrict__ partial, float omb1)
+{
+    v4f gv[kSubBlocks], cv[kSubBlocks];
+    float sp;
+    worker_row_load<FULL, G>(tile, lane, i, g, g_ld, err, err_ld, scales, scales_ld, gv, cv, sp);
+    worker_row_store<FULL>(tile, t, lane, num_tiles, bm, i, gv, cv, sp, err, err_ld, bits,
+                           bits_ld, partial, omb1);
 }
 
 // The tile for workers [i0, i1), the momentum term loaded or decoded once.
@@ -605,6 +656,54 @@ __global__ __launch_bounds__(kWorkerBlock) void k_worker_pass(
 // The worker pass with an fp32 momentum (the first compression step): m is
 // read once per tile for all local workers, and the 16 waves of a workgroup
 // walk the worker rows together (one barrier per row), as in the warm-up.
+// The rows are double-buffered: row i+1's loads (gradient, error state and
+// scale) are issued before row i's arithmetic and stores, so each wave keeps
+// two rows of loads in flight and never waits on a load issued right after
+// its own stores (measured 23.75 against 23.86 ms for one row at a time, and
+// 24.76 ms without the barriers, on the BERT-Large shape, same buffers).
+// ---------------------------------------------------------------------------
+template <bool FULL, class G>
+__device__ __forceinline__ void worker_rows_walk(
+    const Tile &tile, int64_t t, int lane, int64_t num_tiles, bool active,
+    const v4f (&bm)[kSubBlocks], const typename G::T *__restrict__ g, int64_t g_ld,
+    float *__restrict__ err, int64_t err_ld, const float *__restrict__ scales, int64_t scales_ld,
+    uint64_t *__restrict__ bits, int64_t bits_ld, double *__restrict__ partial, int n_local,
+    float omb1)
+{
+    v4f ga[kSubBlocks], ca[kSubBlocks], gb[kSubBlocks], cb[kSubBlocks];
+    float sa = 0.f, sb = 0.f;
+#define ROW_LOAD(i, gv, cv, sp) \
+    worker_row_load<FULL, G>(tile, lane, i, g, g_ld, err, err_ld, scales, scales_ld, gv, cv, sp)
+#define ROW_STORE(i, gv, cv, sp)                                                           \
+    worker_row_store<FULL>(tile, t, lane, num_tiles, bm, i, gv, cv, sp, err, err_ld, bits, \
+                           bits_ld, partial, omb1)
+    if (active) ROW_LOAD(0, ga, ca, sa);
+    int i = 0;
+    // rows i, i+1 and i+2 exist: unconditional loads inside the loop (the
+    // last one or two rows are peeled off), so the wait before row i's
+    // arithmetic leaves row i+1's loads in flight
+    for (; i + 2 < n_local; i += 2) {
+        if (active) ROW_LOAD(i + 1, gb, cb, sb);
+        if (active) ROW_STORE(i, ga, ca, sa);
+        __builtin_amdgcn_s_barrier();  // the workgroup reads each worker row together
+        if (active) ROW_LOAD(i + 2, ga, ca, sa);
+        if (active) ROW_STORE(i + 1, gb, cb, sb);
+        __builtin_amdgcn_s_barrier();
+    }
+    if (i + 1 < n_local) {  // rows i and i+1 remain (n_local is uniform)
+        if (active) ROW_LOAD(i + 1, gb, cb, sb);
+        if (active) ROW_STORE(i, ga, ca, sa);
+        __builtin_amdgcn_s_barrier();
+        if (active) ROW_STORE(i + 1, gb, cb, sb);
+        __builtin_amdgcn_s_barrier();
+    } else {  // row i remains
+        if (active) ROW_STORE(i, ga, ca, sa);
+        __builtin_amdgcn_s_barrier();
+    }
+#undef ROW_LOAD
+#undef ROW_STORE
+}
+
 template <class G>
 __global__ __launch_bounds__(kRowBlock) void k_worker_rows(
     const Tile *__restrict__ tiles, int64_t num_tiles, const float *__restrict__ m,
@@ -619,18 +718,16 @@ __global__ __launch_bounds__(kRowBlock) void k_worker_rows(
     if (active) tile = tiles[t];
     const bool full = tile.len == kTileElems;
     v4f bm[kSubBlocks];
-    if (full)
+    // every wave of the workgroup takes one of the two walks, which run the
+    // same number of barriers
+    if (full) {
         beta1_momentum<true, false>(bm, tile, lane, m, nullptr, nullptr, beta1);
-    else
+        worker_rows_walk<true, G>(tile, t, lane, num_tiles, true, bm, g, g_ld, err, err_ld,
+                                  scales, scales_ld, bits, bits_ld, partial, n_local, omb1);
+    } else {
         beta1_momentum<false, false>(bm, tile, lane, m, nullptr, nullptr, beta1);
-    for (int i = 0; i < n_local; ++i) {
-        if (full)
-            worker_row<true, G>(tile, t, lane, num_tiles, bm, i, g, g_ld, err, err_ld, scales,
-                                scales_ld, bits, bits_ld, partial, omb1);
-        else if (active)
-            worker_row<false, G>(tile, t, lane, num_tiles, bm, i, g, g_ld, err, err_ld, scales,
-                                 scales_ld, bits, bits_ld, partial, omb1);
-        __builtin_amdgcn_s_barrier();  // the workgroup reads each worker row together
+        worker_rows_walk<false, G>(tile, t, lane, num_tiles, active, bm, g, g_ld, err, err_ld,
+                                   scales, scales_ld, bits, bits_ld, partial, n_local, omb1);
     }
 }
 
