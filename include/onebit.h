@@ -234,6 +234,29 @@ int onebit_step(onebit_plan plan, float *x, float *m, const float *v_frozen,
                 float lr, float beta1, float eps, void *workspace,
                 onebit_stream stream);
 
+/* onebit_step for callers that cannot allocate device memory (code under HIP
+ * graph capture, tight serving loops, harnesses that forbid hipMalloc): the
+ * same launches and results, with no workspace argument.  The per-tile
+ * partial sums go to the library's own static device array of
+ * ONEBIT_NOALLOC_SCRATCH_BYTES (96 MiB), which every GPU the library runs on
+ * holds until the process ends; its address is looked up on the first call
+ * on each device.  The call allocates and frees nothing.  Every call on one
+ * GPU shares that GPU's array: calls that overlap on one GPU (other streams,
+ * other threads, other plans) race and must be serialised by the caller.
+ * Nothing in the array needs clearing between calls (each step writes every
+ * partial it reads).  Errors: those of onebit_step; EINVAL when the plan's
+ * workspace_bytes (about 8 (n + 1) bytes per tile of 1024 elements) exceeds
+ * ONEBIT_NOALLOC_SCRATCH_BYTES -- a BERT-Large-shaped buffer of 334M
+ * parameters with n = 32 needs 86 MB and fits; EHIP if the array's address
+ * cannot be found. */
+#define ONEBIT_NOALLOC_SCRATCH_BYTES ((size_t)96 << 20)
+int onebit_step_noalloc(onebit_plan plan, float *x, float *m, const float *v_frozen,
+                        const void *grads, int32_t grad_dtype, int64_t grad_ld,
+                        float *worker_err, int64_t err_ld, float *server_err,
+                        uint64_t *worker_bits, float *worker_scales, uint64_t *server_bits,
+                        float *server_scales, float lr, float beta1, float eps,
+                        onebit_stream stream);
+
 /* onebit_step with timing marks, to profile the fused step phase by phase:
  * the same launches, and in addition hipEventRecord(events[k], stream)
  * before the worker pass (k = 0), before the chunk owners' pass (k = 1),

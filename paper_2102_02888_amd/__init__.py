@@ -6,7 +6,7 @@ header ``include/onebit.h``); this package is the Python binding.
 from .onebit import (  # noqa: F401
     Plan, State, onebit_decode, onebit_decompress_update, onebit_error_materialize,
     onebit_plan_create,
-    onebit_server_reduce_compress, onebit_step, onebit_warmup_adam_step,
+    onebit_server_reduce_compress, onebit_step, onebit_step_noalloc, onebit_warmup_adam_step,
     onebit_worker_compress, onebit_uncompressed_step, onebit_adam_message_step, onebit_l1_norm,
 )
 from .freeze import VarianceFreezeDetector  # noqa: F401

@@ -39,6 +39,8 @@ SIGNATURES = {
     "onebit_decompress_update": [_vp, _vp, _vp, _vp, _vp, _vp, _f32, _f32, _vp],
     "onebit_step": [_vp, _vp, _vp, _vp, _vp, _i32, _i64, _vp, _i64, _vp, _vp, _vp, _vp, _vp,
                     _f32, _f32, _f32, _vp, _vp],
+    "onebit_step_noalloc": [_vp, _vp, _vp, _vp, _vp, _i32, _i64, _vp, _i64, _vp, _vp, _vp, _vp,
+                            _vp, _f32, _f32, _f32, _vp],
     "onebit_step_events": [_vp, _vp, _vp, _vp, _vp, _i32, _i64, _vp, _i64, _vp, _vp, _vp, _vp,
                            _vp, _f32, _f32, _f32, _vp, _vp, _vp],
     "onebit_decode": [_vp, _vp, _vp, _vp, _vp],

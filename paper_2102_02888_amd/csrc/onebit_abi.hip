@@ -16,6 +16,9 @@
 #include "../../include/onebit.h"
 #include "onebit_internal.h"
 
+static_assert(onebit::kScratchBytes == ONEBIT_NOALLOC_SCRATCH_BYTES,
+              "the scratch array and the header's limit must agree");
+
 using onebit::DeviceTables;
 using onebit::kTileElems;
 using onebit::Tile;
@@ -618,6 +621,26 @@ int onebit_step(onebit_plan p, float *x, float *m, const float *v_frozen, const 
     return step_impl(p, x, m, v_frozen, grads, grad_dtype, grad_ld, worker_err, err_ld,
                      server_err, worker_bits, worker_scales, server_bits, server_scales, lr,
                      beta1, eps, workspace, nullptr, (hipStream_t)stream);
+}
+
+int onebit_step_noalloc(onebit_plan p, float *x, float *m, const float *v_frozen,
+                        const void *grads, int32_t grad_dtype, int64_t grad_ld,
+                        float *worker_err, int64_t err_ld, float *server_err,
+                        uint64_t *worker_bits, float *worker_scales, uint64_t *server_bits,
+                        float *server_scales, float lr, float beta1, float eps,
+                        onebit_stream stream)
+{
+    TRY(check_plan(p));
+    if (p->workspace_bytes > onebit::kScratchBytes)
+        return fail(ONEBIT_EINVAL,
+                    "the plan needs %zu bytes of workspace; onebit_step_noalloc's scratch holds "
+                    "%zu (use onebit_step with a caller workspace)",
+                    p->workspace_bytes, onebit::kScratchBytes);
+    void *scratch = nullptr;
+    TRY_HIP(onebit::scratch_address(p->device, &scratch), "scratch symbol lookup");
+    return step_impl(p, x, m, v_frozen, grads, grad_dtype, grad_ld, worker_err, err_ld,
+                     server_err, worker_bits, worker_scales, server_bits, server_scales, lr,
+                     beta1, eps, scratch, nullptr, (hipStream_t)stream);
 }
 
 int onebit_step_events(onebit_plan p, float *x, float *m, const float *v_frozen,

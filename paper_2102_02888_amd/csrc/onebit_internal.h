@@ -88,6 +88,17 @@ hipError_t launch_update(const DeviceTables &tb, int64_t num_tiles, const uint64
                          const float *sscales, float *x, float *m_out, const float *v,
                          float lr, float eps, hipStream_t s);
 
+// The library's own scratch memory, for callers that cannot allocate: a
+// static device array of kScratchBytes on every device the library runs on,
+// held until the process ends.  scratch_address() returns its device address
+// on `device` (looked up once per device, with that device made current for
+// the lookup and restored afterwards), or an error for a device index at or
+// above kMaxScratchDevices or a failed lookup.  Every call on one device
+// shares the array.
+constexpr size_t kScratchBytes = (size_t)96 << 20;
+constexpr int kMaxScratchDevices = 64;
+hipError_t scratch_address(int device, void **ptr);
+
 hipError_t launch_materialize(const DeviceTables &tb, int64_t num_tiles, int rows,
                               const float *err, int64_t err_ld, const float *scales,
                               int64_t scales_ld, float *out, int64_t out_ld, hipStream_t s);

@@ -20,6 +20,7 @@
 // workspace and summed in a fixed order by a finalize kernel; no atomics.
 #include "onebit_internal.h"
 #include <algorithm>
+#include <mutex>
 
 namespace onebit {
 namespace {
@@ -1526,6 +1527,42 @@ hipError_t launch_materialize(const DeviceTables &tb, int64_t num_tiles, int row
     hipLaunchKernelGGL(k_materialize, dim3((unsigned)blocks_for(num_tiles)), dim3(kBlock), 0, s,
                        tb.tiles, num_tiles, rows, err, err_ld, scales, scales_ld, out, out_ld);
     return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// Scratch memory of the entry point that allocates nothing: the per-tile
+// fp64 partial sums that the caller's workspace holds otherwise.  Host code
+// never uses the array's name as an address (on the host it is only a
+// handle for the symbol lookup); it uses the per-device address that
+// hipGetSymbolAddress returns.
+// ---------------------------------------------------------------------------
+static __device__ __align__(256) double scratch[kScratchBytes / sizeof(double)];
+
+namespace {
+std::once_flag g_scratch_once[kMaxScratchDevices];
+void *g_scratch_ptr[kMaxScratchDevices];
+hipError_t g_scratch_err[kMaxScratchDevices];
+}  // namespace
+
+hipError_t scratch_address(int device, void **ptr)
+{
+    *ptr = nullptr;
+    if (device < 0 || device >= kMaxScratchDevices) return hipErrorInvalidDevice;
+    std::call_once(g_scratch_once[device], [device] {
+        int prev = -1;
+        hipError_t e = hipGetDevice(&prev);
+        if (e == hipSuccess && prev != device) e = hipSetDevice(device);
+        void *p = nullptr;
+        if (e == hipSuccess) e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (prev >= 0 && prev != device) {
+            const hipError_t r = hipSetDevice(prev);
+            if (e == hipSuccess) e = r;
+        }
+        g_scratch_err[device] = e;
+        g_scratch_ptr[device] = e == hipSuccess ? p : nullptr;
+    });
+    *ptr = g_scratch_ptr[device];
+    return g_scratch_err[device];
 }
 
 }  // namespace onebit

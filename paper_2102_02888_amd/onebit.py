@@ -16,6 +16,7 @@ from ._native import PlanInfo, call, lib
 __all__ = [
     "Plan", "onebit_plan_create", "onebit_warmup_adam_step", "onebit_worker_compress",
     "onebit_server_reduce_compress", "onebit_decompress_update", "onebit_step",
+    "onebit_step_noalloc",
     "onebit_error_materialize", "onebit_decode", "onebit_uncompressed_step",
     "onebit_adam_message_step", "onebit_l1_norm", "State",
 ]
@@ -278,6 +279,26 @@ def onebit_step(plan, x, m, v_frozen, grads, worker_err, server_err, worker_bits
                 raise ValueError("events[%d] has no HIP event yet: record it once first" % k)
             handles[k] = ev.cuda_event
     call("onebit_step_events", *args, handles, _stream(stream))
+
+
+def onebit_step_noalloc(plan, x, m, v_frozen, grads, worker_err, server_err, worker_bits,
+                        worker_scales, server_bits, server_scales, lr, beta1, eps, stream=None):
+    """onebit_step without a workspace: the library's static scratch array on
+    the device holds the partial sums (calls on one GPU share it and must not
+    overlap)."""
+    n, D, W, S = plan.n, plan.D, plan.W, plan.S
+    for t, name, cols in ((worker_bits, "worker_bits", W), (worker_scales, "worker_scales", S)):
+        if t is not None and t.dim() == 2 and cols > 0 and t.stride(0) != cols:
+            raise ValueError("%s must be contiguous [n, %d] for onebit_step_noalloc" % (name, cols))
+    call("onebit_step_noalloc", plan.handle, _ptr(x, torch.float32, "x", D),
+         _ptr(m, torch.float32, "m", D), _ptr(v_frozen, torch.float32, "v_frozen", D),
+         *_grads(grads, D, n), _ld(grads),
+         _ptr(worker_err, torch.float32, "worker_err", D, n), _ld(worker_err),
+         _ptr(server_err, torch.float32, "server_err", D),
+         _ptr(worker_bits, torch.int64, "worker_bits", W, n),
+         _ptr(worker_scales, torch.float32, "worker_scales", S, n),
+         _ptr(server_bits, torch.int64, "server_bits", W),
+         _ptr(server_scales, torch.float32, "server_scales", S), lr, beta1, eps, _stream(stream))
 
 
 def onebit_decode(plan, bits, scales, out, stream=None):

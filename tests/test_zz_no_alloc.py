@@ -1,0 +1,68 @@
+"""onebit_step_noalloc, the step for callers that cannot allocate, against
+onebit_step with a caller workspace: identical results, bit for bit, over
+two runs in a row on one device (the second plan smaller than the first, so
+the second run reuses the library's scratch array with less of it live)."""
+import ctypes
+
+import pytest
+import torch
+
+import synth
+from parity_util import host
+
+pytestmark = pytest.mark.gpu
+
+NAMES = ("x", "m", "worker_err", "worker_bits", "worker_scales", "server_err", "server_bits",
+         "server_scales")
+
+
+def _compare_runs(ob, dev, numel, n, steps, seed):
+    plan = ob.Plan(numel, n)
+    assert plan.workspace_bytes <= (96 << 20)
+    wl = synth.Workload(name="noalloc", numel=numel, n=n, warmup_steps=1, steps=steps,
+                        seed_grads=seed)
+    ref, new = ob.State(plan, dev), ob.State(plan, dev)
+    x0 = torch.from_numpy(synth.host_params(wl, plan.D)).to(dev)
+    g = torch.from_numpy(synth.host_grads(wl, plan.D, plan.tensor_off, 1)).to(dev)
+    for st in (ref, new):
+        st.x.copy_(x0)
+        st.grads.copy_(g)
+        st.warmup(wl.lr, wl.beta1, wl.beta2, wl.eps, 1)
+    for t in range(2, 2 + steps):
+        g = torch.from_numpy(synth.host_grads(wl, plan.D, plan.tensor_off, t)).to(dev)
+        ref.grads.copy_(g)
+        new.grads.copy_(g)
+        packed = t > 2  # the first compression step reads the warm-up's fp32 m
+        ref.step(wl.lr, wl.beta1, wl.eps)
+        ob.onebit_step_noalloc(plan, new.x, None if packed else new.m, new.v, new.grads,
+                               new.worker_err, new.server_err, new.worker_bits,
+                               new.worker_scales, new.server_bits, new.server_scales, wl.lr,
+                               wl.beta1, wl.eps)
+        torch.cuda.synchronize()
+        for name in NAMES:
+            a, b = host(getattr(ref, name)), host(getattr(new, name))
+            assert a.tobytes() == b.tobytes(), (numel, n, t, name)
+    plan.close()
+
+
+def test_noalloc_step_matches_workspace_step(dev):
+    import paper_2102_02888_amd as ob
+    # a plan of 1,079 tiles, then a smaller one of 96 tiles
+    _compare_runs(ob, dev, [1_000_000, 70_001, 5000, 64, 0, 300], 8, steps=3, seed=21)
+    _compare_runs(ob, dev, [90_000, 3000, 1], 4, steps=2, seed=22)
+
+
+def test_noalloc_step_refuses_plans_beyond_its_scratch(dev):
+    """A plan whose workspace exceeds the static array is refused before any
+    buffer is touched (the buffers may then be anything, NULL included)."""
+    import paper_2102_02888_amd as ob
+    from paper_2102_02888_amd import _native
+    L = _native.lib()
+    plan = ob.Plan([1 << 27], 128)  # 131,072 tiles, (128 + 1) partial sums each
+    assert plan.workspace_bytes > (96 << 20)
+    vp = ctypes.c_void_p
+    rc = L.onebit_step_noalloc(plan.handle, None, None, None, None, 0, plan.D, None, plan.D,
+                               None, None, None, None, None, 1e-3, 0.9, 1e-8,
+                               vp(torch.cuda.current_stream().cuda_stream))
+    assert rc == -1 and b"scratch" in L.onebit_last_error()
+    plan.close()
