@@ -840,53 +840,61 @@ __device__ __forceinline__ void wave_sync()
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
-// Last part of the server pass for one tile: average, add the server error,
-// store the new compensated error state, the sign words and the tile's sum of
-// squares.
+// One sub-block (256 elements) of the server pass's last part: average, add
+// the server error, store the new compensated error state and the sign words;
+// returns this wave's fp64 sum of squares of the sub-block (every lane gets
+// it).  sum[c] and cv[c] are the lane's elements b*256 + 4*lane + c.
 template <bool FULL, bool POW2>
-__device__ __forceinline__ void server_epilogue(const double (&sum)[kSubBlocks][4],
-                                                const v4f (&cv)[kSubBlocks], float sprev, int n,
-                                                int lane, const Tile &tile, int64_t t,
-                                                float *__restrict__ serr,
-                                                uint64_t *__restrict__ sbits,
-                                                double *__restrict__ partial)
+__device__ __forceinline__ double server_epilogue_sub(const double (&sum)[4], v4f cv,
+                                                      float sprev, int n, int lane,
+                                                      const Tile &tile, int b,
+                                                      float *__restrict__ serr,
+                                                      uint64_t *__restrict__ sbits)
 {
     const int len = tile.len;
     const int64_t base = tile.start;
     const int nwords = (len + 63) >> 6;
     const double dn = (double)n;
     const double inv_n = 1.0 / dn;
+    const int li = b * (kWave * 4) + 4 * lane;
     double acc = 0.0;
+    v4f zv;
+    uint32_t nib = 0;
 #pragma unroll
-    for (int b = 0; b < kSubBlocks; ++b) {
-        const int li = b * (kWave * 4) + 4 * lane;
-        v4f zv;
-        uint32_t nib = 0;
-#pragma unroll
-        for (int c = 0; c < 4; ++c) {
-            const float avg = (float)(POW2 ? sum[b][c] * inv_n : sum[b][c] / dn);
-            const float z = avg + error_of(cv[b][c], sprev);
-            zv[c] = z;
-            const bool valid = FULL || li + c < len;
-            const double zd = valid ? (double)z : 0.0;
-            // zd * zd is exact in fp64 (a 24-bit significand squared), so the
-            // fused form rounds exactly as the separate multiply and add would
-            acc = __builtin_fma(zd, zd, acc);
-            nib |= (valid && z >= 0.f) ? (1u << c) : 0u;
-        }
-        st4<FULL>(serr + base, li, len, zv);
-        const uint64_t word = row_sign_word(nib, lane);
-        const int w = 4 * b + (lane >> 4);
-        if ((lane & 15) == 0 && (FULL || w < nwords)) sbits[(base >> 6) + w] = word;
+    for (int c = 0; c < 4; ++c) {
+        // avg = sum / n rounded to fp32 (for a power-of-two n, sum * (1/n) is
+        // the same exact scaling), then the compensated value and its square
+        const float avg = (float)(POW2 ? sum[c] * inv_n : sum[c] / dn);
+        const float z = avg + error_of(cv[c], sprev);
+        zv[c] = z;
+        const bool valid = FULL || li + c < len;
+        const double zd = valid ? (double)z : 0.0;
+        // zd * zd is exact in fp64 (a 24-bit significand squared), so the
+        // fused form rounds exactly as the separate multiply and add would
+        acc = __builtin_fma(zd, zd, acc);
+        nib |= (valid && z >= 0.f) ? (1u << c) : 0u;
     }
-    acc = wave_sum_dpp(acc);
-    if (lane == 0) partial[t] = acc;
+    st4<FULL>(serr + base, li, len, zv);
+    const uint64_t word = row_sign_word(nib, lane);
+    const int w = 4 * b + (lane >> 4);
+    if ((lane & 15) == 0 && (FULL || w < nwords)) sbits[(base >> 6) + w] = word;
+    return acc;
 }
 
 // LDS row stride (in 32-bit words) of the sign staging: a multiple of 4 keeps
 // 128-bit accesses aligned, and 40 puts the 64 words a wave reads at once in
 // the accumulation on 64 different banks.
 constexpr int kBitsStride = kServerRowBatch + 8;
+
+// One wave's LDS working set for a batch of up to kServerRowBatch incoming
+// rows of one tile: the sign words, transposed ([half-word h][row r]), the
+// rows' scales, and the lookup tables built from them.
+struct ServerBatchLds {
+    uint32_t bits[2 * kTileWords][kBitsStride];
+    double lut4[kServerRowBatch / 4][16];
+    double lut8[2][256];
+    float scale[kServerRowBatch];
+};
 
 // 8x8 bit transposes of the four byte columns of 8 words: bit j of byte b of
 // a[k] moves to bit k of byte b of a[j] (three rounds of block swaps: 4x4,
@@ -914,67 +922,183 @@ __device__ __forceinline__ void transpose_bits8x8(uint32_t (&a)[8])
     }
 }
 
-__global__ __launch_bounds__(kBlock) void k_server_pass(
-    const Tile *__restrict__ tiles, const int32_t *__restrict__ chunk_tiles, int64_t tile_begin,
-    int64_t tile_count, int n,
-    int grouping_limit, const uint64_t *__restrict__ wbits, int64_t bits_ld,
-    int64_t bits_word_base, const float *__restrict__ wscales, int64_t scales_ld,
-    int64_t scales_seg_base, float *__restrict__ serr, const float *__restrict__ sscales,
-    uint64_t *__restrict__ sbits, double *__restrict__ partial)
-{
-    // s_bits[wave][half-word h of the tile][worker row r]
-    __shared__ __align__(16) uint32_t s_bits[kWavesPerBlock][2 * kTileWords][kBitsStride];
-    __shared__ double s_lut4[kWavesPerBlock][kServerRowBatch / 4][16];
-    __shared__ double s_lut8[kWavesPerBlock][2][256];
-    __shared__ float s_scale[kWavesPerBlock][kServerRowBatch];
-    const int lane = threadIdx.x & (kWave - 1);
-    const int wv = threadIdx.x >> 6;
-    const int64_t rel = xcd_block() * kWavesPerBlock + wv;
-    if (rel >= tile_count) return;
-    const int64_t t = chunk_tiles[tile_begin + rel];
-    const Tile tile = tiles[t];
-    const int len = tile.len;
-    const int64_t base = tile.start;
-    const int nwords = (len + 63) >> 6;
-    const int64_t w0 = (base >> 6) - bits_word_base;
-    const int64_t sq = (int64_t)tile.seg - scales_seg_base;
-    const bool full = len == kTileElems;
+// The incoming sign words and scales of one tile as the chunk owner reads
+// them: row i's word for tile word wi is at words[i * bits_ld + wi], its
+// scale at scales[i * scales_ld].
+struct ServerRows {
+    const uint64_t *words;   // the tile's first word in row 0
+    int64_t bits_ld;
+    const float *scales;     // the segment's scale in row 0
+    int64_t scales_ld;
+    int nwords;              // words of the tile
+    bool full;               // a full tile
+};
 
-    // issue the error-state loads first; they are consumed at the end
-    const float sprev = sscales[tile.seg];
-    v4f cv[kSubBlocks];
-#pragma unroll
-    for (int b = 0; b < kSubBlocks; ++b) {
-        const int li = b * (kWave * 4) + 4 * lane;
-        cv[b] = full ? ld4<true>(serr + base, li, len) : ld4<false>(serr + base, li, len);
-    }
-    // the first batch of sign words and scales is loaded before the exponent
-    // check below, so that both memory round trips overlap
+// Loads rows [r0, r0 + rows) of the tile (rows <= kServerRowBatch): lane L
+// takes word wi = L % 16 of rows r0 + L/16 + 4k, and the scale of row r0 + L.
+__device__ __forceinline__ void server_load_batch(const ServerRows &in, int r0, int rows,
+                                                  int lane, uint64_t (&stg)[kServerRowBatch / 4],
+                                                  float &scl)
+{
     const int wi = lane & (kTileWords - 1);
-    uint64_t stg[kServerRowBatch / 4];
-    float scl = 0.f;
-    auto load_batch = [&](int r0) {
-        const int rows = min(kServerRowBatch, n - r0);
-        // row r0 + (lane >> 4) + 4k of the lane's word wi
-        const uint64_t *p = wbits + (int64_t)(r0 + (lane >> 4)) * bits_ld + w0 + wi;
-        const int64_t step = 4 * bits_ld;
-        if (full && rows == kServerRowBatch) {  // wave-uniform: every load in range
+    const uint64_t *p = in.words + (int64_t)(r0 + (lane >> 4)) * in.bits_ld + wi;
+    const int64_t step = 4 * in.bits_ld;
+    if (in.full && rows == kServerRowBatch) {  // wave-uniform: every load in range
 #pragma unroll
-            for (int k = 0; k < kServerRowBatch / 4; ++k)
-                stg[k] = __builtin_nontemporal_load(p + k * step);
-        } else {
+        for (int k = 0; k < kServerRowBatch / 4; ++k) stg[k] = __builtin_nontemporal_load(p + k * step);
+    } else {
 #pragma unroll
-            for (int k = 0; k < kServerRowBatch / 4; ++k) {
-                const int r = (lane >> 4) + 4 * k;
-                stg[k] = (r < rows && wi < nwords) ? __builtin_nontemporal_load(p + k * step) : 0ull;
+        for (int k = 0; k < kServerRowBatch / 4; ++k) {
+            const int r = (lane >> 4) + 4 * k;
+            stg[k] = (r < rows && wi < in.nwords) ? __builtin_nontemporal_load(p + k * step) : 0ull;
+        }
+    }
+    scl = lane < rows ? in.scales[(int64_t)(r0 + lane) * in.scales_ld] : 0.f;
+}
+
+// Writes a loaded batch into the wave's staging area (rows past the batch's
+// last row, up to the next multiple of 8, get zero words).
+__device__ __forceinline__ void server_stage_batch(ServerBatchLds &L, const ServerRows &in,
+                                                   int rows, int lane,
+                                                   const uint64_t (&stg)[kServerRowBatch / 4],
+                                                   float scl)
+{
+    const int wi = lane & (kTileWords - 1);
+    const int rows8 = (rows + 7) & ~7;
+    if (in.full && rows == kServerRowBatch) {  // wave-uniform
+#pragma unroll
+        for (int k = 0; k < kServerRowBatch / 4; ++k) {
+            const int r = (lane >> 4) + 4 * k;
+            L.bits[2 * wi][r] = (uint32_t)stg[k];
+            L.bits[2 * wi + 1][r] = (uint32_t)(stg[k] >> 32);
+        }
+    } else {
+#pragma unroll
+        for (int k = 0; k < kServerRowBatch / 4; ++k) {
+            const int r = (lane >> 4) + 4 * k;
+            if (r < rows8 && wi < in.nwords) {
+                L.bits[2 * wi][r] = (uint32_t)stg[k];
+                L.bits[2 * wi + 1][r] = (uint32_t)(stg[k] >> 32);
             }
         }
-        scl = lane < rows ? wscales[(int64_t)(r0 + lane) * scales_ld + sq] : 0.f;
-    };
-    load_batch(0);
+    }
+    if (lane < rows) L.scale[lane] = scl;
+}
 
-    // exponent range of the segment's nonzero scales (one batch: the scales
-    // just loaded; more: read them all)
+// sum += the staged batch's decoded messages, grouped: each group of 8 rows is
+// one lookup in a 256-entry table of its signed scale sums (exact, so any
+// grouping gives the worker-order sum).  The 16-entry tables of 4 rows are
+// built first; each (half-word, group) block is then regrouped in place by
+// four 8x8 bit transposes, after which byte e>>3 of word r8 + (e&7) is
+// element e's table index.
+__device__ __forceinline__ void server_batch_grouped(double (&sum)[kSubBlocks][4],
+                                                     ServerBatchLds &L, int rows, int lane)
+{
+    const int half = (lane >> 3) & 1;
+    const int groups8 = (rows + 7) >> 3;
+    // 16-entry tables of 4 workers, two per group of 8 (rows past the last
+    // worker add 0)
+    for (int e = lane; e < 32 * groups8; e += kWave) {
+        const int q = e >> 4, idx = e & 15;
+        double v = 0.0;
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+            const int r = 4 * q + k;
+            if (r < rows) {
+                const double sc = (double)L.scale[r];
+                v += ((idx >> k) & 1) ? sc : -sc;
+            }
+        }
+        L.lut4[q][idx] = v;
+    }
+#pragma unroll 1
+    for (int k = 0; k < (2 * kTileWords) * (kServerRowBatch / 8) / kWave; ++k) {
+        const int blk = lane + kWave * k;
+        const int hwb = blk & (2 * kTileWords - 1), gb = blk / (2 * kTileWords);
+        if (gb < groups8) {
+            uint32_t *p = &L.bits[hwb][8 * gb];
+            const uint4 u0 = *(const uint4 *)p;
+            const uint4 u1 = *(const uint4 *)(p + 4);
+            uint32_t a[8] = {u0.x, u0.y, u0.z, u0.w, u1.x, u1.y, u1.z, u1.w};
+            transpose_bits8x8(a);
+            *(uint4 *)p = make_uint4(a[0], a[1], a[2], a[3]);
+            *(uint4 *)(p + 4) = make_uint4(a[4], a[5], a[6], a[7]);
+        }
+    }
+    wave_sync();
+    // two groups of 8 workers at a time
+    for (int g0 = 0; 8 * g0 < rows; g0 += 2) {
+        const int gcnt = min(2, groups8 - g0);
+#pragma unroll
+        for (int k = 0; k < 512 / kWave; ++k) {
+            const int e = lane + kWave * k;
+            const int g = e >> 8, idx = e & 255;  // g = k / 4: uniform
+            if (g < gcnt) {
+                const int q = 2 * (g0 + g);
+                L.lut8[g][idx] = L.lut4[q][idx & 15] + L.lut4[q + 1][idx >> 4];
+            }
+        }
+        wave_sync();
+        for (int g = 0; g < gcnt; ++g) {
+            const int r8 = 8 * (g0 + g);
+            // two sub-blocks at a time: their 8 table indices first, then the
+            // 8 lookups, then the adds, so that the LDS round trips overlap
+#pragma unroll
+            for (int bh = 0; bh < kSubBlocks; bh += 2) {
+                uint32_t idx[2][4];
+#pragma unroll
+                for (int bb = 0; bb < 2; ++bb) {
+                    const int hw = 2 * (4 * (bh + bb) + (lane >> 4)) + half;
+                    // the lane's elements e = 4 (lane & 7) + c of the half-word:
+                    // byte e >> 3 of word e & 7 holds the 8 workers' bits of e
+                    const uint8_t *blk = (const uint8_t *)&L.bits[hw][r8];
+                    const int o = 16 * (lane & 1) + ((lane & 7) >> 1);
+#pragma unroll
+                    for (int c = 0; c < 4; ++c) idx[bb][c] = blk[o + 4 * c];
+                }
+                double val[2][4];
+#pragma unroll
+                for (int bb = 0; bb < 2; ++bb)
+#pragma unroll
+                    for (int c = 0; c < 4; ++c) val[bb][c] = L.lut8[g][idx[bb][c]];
+#pragma unroll
+                for (int bb = 0; bb < 2; ++bb)
+#pragma unroll
+                    for (int c = 0; c < 4; ++c) sum[bh + bb][c] += val[bb][c];
+            }
+        }
+        wave_sync();
+    }
+}
+
+// sum += the staged batch's decoded messages one worker at a time, in row
+// order (the path for scale sets whose partial sums may round).
+__device__ __forceinline__ void server_batch_one_by_one(double (&sum)[kSubBlocks][4],
+                                                        const ServerBatchLds &L, int rows,
+                                                        int lane)
+{
+    const int half = (lane >> 3) & 1;
+    const int shift = 4 * (lane & 7);
+    for (int r = 0; r < rows; ++r) {
+        const double sp = (double)L.scale[r];
+        const double sn = -sp;
+#pragma unroll
+        for (int b = 0; b < kSubBlocks; ++b) {
+            const uint32_t nib = (L.bits[2 * (4 * b + (lane >> 4)) + half][r] >> shift) & 0xFu;
+#pragma unroll
+            for (int c = 0; c < 4; ++c) sum[b][c] += ((nib >> c) & 1u) ? sp : sn;
+        }
+    }
+}
+
+// Whether the segment's incoming scales allow the grouped sum: every partial
+// sum of +-scales is exact in fp64 when the nonzero scales' exponents span at
+// most grouping_limit = 29 - ceil(log2 n) binades (and none is Inf or NaN).
+// `first` holds the scale of row `lane` when n <= kServerRowBatch (already
+// loaded); otherwise all n scales are read.  Every lane gets the answer.
+__device__ __forceinline__ bool server_grouped(const ServerRows &in, int n, int grouping_limit,
+                                               int lane, float first)
+{
     int emax = 0, emin = 1 << 20;
     auto widen = [&](float sc) {
         const uint32_t u = __float_as_uint(sc) & 0x7FFFFFFFu;
@@ -984,149 +1108,200 @@ __global__ __launch_bounds__(kBlock) void k_server_pass(
         emin = min(emin, e);
     };
     if (n <= kServerRowBatch)
-        widen(scl);
+        widen(first);
     else
-        for (int r = lane; r < n; r += kWave) widen(wscales[(int64_t)r * scales_ld + sq]);
+        for (int r = lane; r < n; r += kWave) widen(in.scales[(int64_t)r * in.scales_ld]);
     emax = wave_max(emax);
     emin = wave_min(emin);
-    const bool grouped = emax < 255 && (emax == 0 || emax - emin <= grouping_limit);
-    const int half = (lane >> 3) & 1;
-    const int shift = 4 * (lane & 7);
+    return emax < 255 && (emax == 0 || emax - emin <= grouping_limit);
+}
+
+// ---------------------------------------------------------------------------
+// Chunk owners' pass, one wave per tile (every n): the wave walks the
+// incoming rows in batches of kServerRowBatch, then finishes the tile.  Each
+// wave owns its LDS staging area, so it synchronises only with itself; the
+// tile's error-state loads are issued first so that they overlap the
+// sign-word traffic, and the first batch is loaded before the exponent check.
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(kBlock) void k_server_pass(
+    const Tile *__restrict__ tiles, const int32_t *__restrict__ chunk_tiles, int64_t tile_begin,
+    int64_t tile_count, int n,
+    int grouping_limit, const uint64_t *__restrict__ wbits, int64_t bits_ld,
+    int64_t bits_word_base, const float *__restrict__ wscales, int64_t scales_ld,
+    int64_t scales_seg_base, float *__restrict__ serr, const float *__restrict__ sscales,
+    uint64_t *__restrict__ sbits, double *__restrict__ partial)
+{
+    __shared__ __align__(16) ServerBatchLds s_lds[kWavesPerBlock];
+    const int lane = threadIdx.x & (kWave - 1);
+    const int wv = threadIdx.x >> 6;
+    const int64_t rel = xcd_block() * kWavesPerBlock + wv;
+    if (rel >= tile_count) return;
+    const int64_t t = chunk_tiles[tile_begin + rel];
+    const Tile tile = tiles[t];
+    const int len = tile.len;
+    const int64_t base = tile.start;
+    const ServerRows in{wbits + ((base >> 6) - bits_word_base), bits_ld,
+                        wscales + ((int64_t)tile.seg - scales_seg_base), scales_ld,
+                        (len + 63) >> 6, len == kTileElems};
+    ServerBatchLds &L = s_lds[wv];
+
+    // issue the error-state loads first; they are consumed at the end
+    const float sprev = sscales[tile.seg];
+    v4f cv[kSubBlocks];
+#pragma unroll
+    for (int b = 0; b < kSubBlocks; ++b) {
+        const int li = b * (kWave * 4) + 4 * lane;
+        cv[b] = in.full ? ld4<true>(serr + base, li, len) : ld4<false>(serr + base, li, len);
+    }
+    uint64_t stg[kServerRowBatch / 4];
+    float scl = 0.f;
+    server_load_batch(in, 0, min(kServerRowBatch, n), lane, stg, scl);
+    const bool grouped = server_grouped(in, n, grouping_limit, lane, scl);
     double sum[kSubBlocks][4];
 #pragma unroll
     for (int b = 0; b < kSubBlocks; ++b)
 #pragma unroll
         for (int c = 0; c < 4; ++c) sum[b][c] = 0.0;
-
     for (int r0 = 0; r0 < n; r0 += kServerRowBatch) {
-        if (r0 > 0) load_batch(r0);
         const int rows = min(kServerRowBatch, n - r0);
-        const int rows8 = (rows + 7) & ~7;  // rows past the last worker hold zero words
-        if (full && rows == kServerRowBatch) {  // wave-uniform
-#pragma unroll
-            for (int k = 0; k < kServerRowBatch / 4; ++k) {
-                const int r = (lane >> 4) + 4 * k;
-                s_bits[wv][2 * wi][r] = (uint32_t)stg[k];
-                s_bits[wv][2 * wi + 1][r] = (uint32_t)(stg[k] >> 32);
-            }
-        } else {
-#pragma unroll
-            for (int k = 0; k < kServerRowBatch / 4; ++k) {
-                const int r = (lane >> 4) + 4 * k;
-                if (r < rows8 && wi < nwords) {
-                    s_bits[wv][2 * wi][r] = (uint32_t)stg[k];
-                    s_bits[wv][2 * wi + 1][r] = (uint32_t)(stg[k] >> 32);
-                }
-            }
-        }
-        if (lane < rows) s_scale[wv][lane] = scl;
+        if (r0 > 0) server_load_batch(in, r0, rows, lane, stg, scl);
+        server_stage_batch(L, in, rows, lane, stg, scl);
         wave_sync();
-        if (grouped) {
-            // 16-entry tables of 4 workers, two per group of 8 (rows past the
-            // last worker add 0)
-            const int groups8 = (rows + 7) >> 3;
-            for (int e = lane; e < 32 * groups8; e += kWave) {
-                const int q = e >> 4, idx = e & 15;
-                double v = 0.0;
+        if (grouped)
+            server_batch_grouped(sum, L, rows, lane);
+        else
+            server_batch_one_by_one(sum, L, rows, lane);
+        wave_sync();
+    }
+    // FULL and POW2 are wave-uniform, so each wave runs one variant
+    const bool pow2 = (n & (n - 1)) == 0;
+    double acc = 0.0;
 #pragma unroll
-                for (int k = 0; k < 4; ++k) {
-                    const int r = 4 * q + k;
-                    if (r < rows) {
-                        const double sc = (double)s_scale[wv][r];
-                        v += ((idx >> k) & 1) ? sc : -sc;
-                    }
-                }
-                s_lut4[wv][q][idx] = v;
-            }
-            // regroup each (half-word, group of 8 workers) block in place:
-            // afterwards byte e>>3 of word r8 + (e&7) is element e's table index
-#pragma unroll 1
-            for (int k = 0; k < (2 * kTileWords) * (kServerRowBatch / 8) / kWave; ++k) {
-                const int blk = lane + kWave * k;
-                const int hwb = blk & (2 * kTileWords - 1), gb = blk / (2 * kTileWords);
-                if (gb < groups8) {
-                    uint32_t *p = &s_bits[wv][hwb][8 * gb];
-                    const uint4 u0 = *(const uint4 *)p;
-                    const uint4 u1 = *(const uint4 *)(p + 4);
-                    uint32_t a[8] = {u0.x, u0.y, u0.z, u0.w, u1.x, u1.y, u1.z, u1.w};
-                    transpose_bits8x8(a);
-                    *(uint4 *)p = make_uint4(a[0], a[1], a[2], a[3]);
-                    *(uint4 *)(p + 4) = make_uint4(a[4], a[5], a[6], a[7]);
-                }
-            }
+    for (int b = 0; b < kSubBlocks; ++b) {
+        if (in.full && pow2)
+            acc += server_epilogue_sub<true, true>(sum[b], cv[b], sprev, n, lane, tile, b, serr, sbits);
+        else if (in.full)
+            acc += server_epilogue_sub<true, false>(sum[b], cv[b], sprev, n, lane, tile, b, serr, sbits);
+        else if (pow2)
+            acc += server_epilogue_sub<false, true>(sum[b], cv[b], sprev, n, lane, tile, b, serr, sbits);
+        else
+            acc += server_epilogue_sub<false, false>(sum[b], cv[b], sprev, n, lane, tile, b, serr, sbits);
+    }
+    acc = wave_sum_dpp(acc);
+    if (lane == 0) partial[t] = acc;
+}
+
+// ---------------------------------------------------------------------------
+// Chunk owners' pass for many workers (n > kServerRowBatch): the
+// kSplitWaves waves of a workgroup share one tile.  When the grouped sum
+// applies, wave w takes row batches w, w + kSplitWaves, ...; the waves' exact
+// partial sums are then added through LDS (exact, so in any order), and wave
+// w finishes sub-block w of the tile.  Otherwise wave 0 adds every row one by
+// one in worker order and hands the other waves their sub-blocks.
+// ---------------------------------------------------------------------------
+constexpr int kSplitWaves = kSubBlocks;
+
+__global__ __launch_bounds__(kSplitWaves * kWave) void k_server_split(
+    const Tile *__restrict__ tiles, const int32_t *__restrict__ chunk_tiles, int64_t tile_begin,
+    int64_t tile_count, int n, int grouping_limit, const uint64_t *__restrict__ wbits,
+    int64_t bits_ld, int64_t bits_word_base, const float *__restrict__ wscales,
+    int64_t scales_ld, int64_t scales_seg_base, float *__restrict__ serr,
+    const float *__restrict__ sscales, uint64_t *__restrict__ sbits, double *__restrict__ partial)
+{
+    // the staging areas while rows are summed, then the exchange of partial
+    // sums: xch[sub-block][source wave][element of the sub-block]
+    union SplitLds {
+        ServerBatchLds batch[kSplitWaves];
+        double xch[kSubBlocks][kSplitWaves][kWave * 4];
+    };
+    __shared__ __align__(16) SplitLds s_lds;
+    __shared__ double s_red[kSplitWaves];
+    const int lane = threadIdx.x & (kWave - 1);
+    const int wv = threadIdx.x >> 6;
+    const int64_t rel = xcd_block();
+    if (rel >= tile_count) return;  // the whole workgroup
+    const int64_t t = chunk_tiles[tile_begin + rel];
+    const Tile tile = tiles[t];
+    const int len = tile.len;
+    const int64_t base = tile.start;
+    const ServerRows in{wbits + ((base >> 6) - bits_word_base), bits_ld,
+                        wscales + ((int64_t)tile.seg - scales_seg_base), scales_ld,
+                        (len + 63) >> 6, len == kTileElems};
+    ServerBatchLds &L = s_lds.batch[wv];
+
+    const float sprev = sscales[tile.seg];
+    const int li = wv * (kWave * 4) + 4 * lane;  // this wave's sub-block
+    const v4f cv = in.full ? ld4<true>(serr + base, li, len) : ld4<false>(serr + base, li, len);
+    uint64_t stg[kServerRowBatch / 4];
+    float scl = 0.f;
+    const int rfirst = kServerRowBatch * wv;  // may be past n when n <= 96: no rows then
+    server_load_batch(in, rfirst, max(0, min(kServerRowBatch, n - rfirst)), lane, stg, scl);
+    // every wave reads all n scales and reaches the same decision
+    const bool grouped = server_grouped(in, n, grouping_limit, lane, 0.f);
+    double sum[kSubBlocks][4];
+#pragma unroll
+    for (int b = 0; b < kSubBlocks; ++b)
+#pragma unroll
+        for (int c = 0; c < 4; ++c) sum[b][c] = 0.0;
+    if (grouped) {
+        constexpr int kStep = kServerRowBatch * kSplitWaves;
+        for (int r0 = rfirst; r0 < n; r0 += kStep) {
+            const int rows = min(kServerRowBatch, n - r0);
+            server_stage_batch(L, in, rows, lane, stg, scl);
+            // the next batch's words travel while this one is summed
+            if (r0 + kStep < n)
+                server_load_batch(in, r0 + kStep, min(kServerRowBatch, n - r0 - kStep), lane, stg,
+                                  scl);
             wave_sync();
-            // two groups of 8 workers at a time
-            for (int g0 = 0; 8 * g0 < rows; g0 += 2) {
-                const int gcnt = min(2, groups8 - g0);
-#pragma unroll
-                for (int k = 0; k < 512 / kWave; ++k) {
-                    const int e = lane + kWave * k;
-                    const int g = e >> 8, idx = e & 255;  // g = k / 4: uniform
-                    if (g < gcnt) {
-                        const int q = 2 * (g0 + g);
-                        s_lut8[wv][g][idx] = s_lut4[wv][q][idx & 15] + s_lut4[wv][q + 1][idx >> 4];
-                    }
-                }
-                wave_sync();
-                for (int g = 0; g < gcnt; ++g) {
-                    const int r8 = 8 * (g0 + g);
-                    // two sub-blocks at a time: their 8 table indices first,
-                    // then the 8 lookups, then the adds, so that the LDS round
-                    // trips overlap
-#pragma unroll
-                    for (int bh = 0; bh < kSubBlocks; bh += 2) {
-                        uint32_t idx[2][4];
-#pragma unroll
-                        for (int bb = 0; bb < 2; ++bb) {
-                            const int hw = 2 * (4 * (bh + bb) + (lane >> 4)) + half;
-                            // the lane's elements e = 4 (lane & 7) + c of the half-word:
-                            // byte e >> 3 of word e & 7 holds the 8 workers' bits of e
-                            const uint8_t *blk = (const uint8_t *)&s_bits[wv][hw][r8];
-                            const int o = 16 * (lane & 1) + ((lane & 7) >> 1);
-#pragma unroll
-                            for (int c = 0; c < 4; ++c) idx[bb][c] = blk[o + 4 * c];
-                        }
-                        double val[2][4];
-#pragma unroll
-                        for (int bb = 0; bb < 2; ++bb)
-#pragma unroll
-                            for (int c = 0; c < 4; ++c) val[bb][c] = s_lut8[wv][g][idx[bb][c]];
-#pragma unroll
-                        for (int bb = 0; bb < 2; ++bb)
-#pragma unroll
-                            for (int c = 0; c < 4; ++c) sum[bh + bb][c] += val[bb][c];
-                    }
-                }
-                wave_sync();
-            }
-        } else {
-            for (int r = 0; r < rows; ++r) {
-                const double sp = (double)s_scale[wv][r];
-                const double sn = -sp;
-#pragma unroll
-                for (int b = 0; b < kSubBlocks; ++b) {
-                    const uint32_t nib = (s_bits[wv][2 * (4 * b + (lane >> 4)) + half][r] >> shift) & 0xFu;
-#pragma unroll
-                    for (int c = 0; c < 4; ++c) sum[b][c] += ((nib >> c) & 1u) ? sp : sn;
-                }
-            }
+            server_batch_grouped(sum, L, rows, lane);
+            wave_sync();
         }
-        wave_sync();
+    } else if (wv == 0) {
+        for (int r0 = 0; r0 < n; r0 += kServerRowBatch) {
+            const int rows = min(kServerRowBatch, n - r0);
+            if (r0 > 0) server_load_batch(in, r0, rows, lane, stg, scl);
+            server_stage_batch(L, in, rows, lane, stg, scl);
+            wave_sync();
+            server_batch_one_by_one(sum, L, rows, lane);
+            wave_sync();
+        }
     }
-    // avg = sum / n rounded to fp32 (for a power-of-two n, sum * (1/n) is the
-    // same exact scaling), then the compensated value, its sign word and
-    // square; FULL and POW2 are wave-uniform, so each wave runs one variant
-    if (full) {
-        if ((n & (n - 1)) == 0)
-            server_epilogue<true, true>(sum, cv, sprev, n, lane, tile, t, serr, sbits, partial);
-        else
-            server_epilogue<true, false>(sum, cv, sprev, n, lane, tile, t, serr, sbits, partial);
-    } else {
-        if ((n & (n - 1)) == 0)
-            server_epilogue<false, true>(sum, cv, sprev, n, lane, tile, t, serr, sbits, partial);
-        else
-            server_epilogue<false, false>(sum, cv, sprev, n, lane, tile, t, serr, sbits, partial);
+    __syncthreads();  // every wave is done with its staging area
+#pragma unroll
+    for (int b = 0; b < kSubBlocks; ++b) {
+        if (b == wv) continue;
+        double2 *dst = (double2 *)&s_lds.xch[b][wv][4 * lane];
+        dst[0] = make_double2(sum[b][0], sum[b][1]);
+        dst[1] = make_double2(sum[b][2], sum[b][3]);
     }
+    __syncthreads();
+    double s4[4];
+#pragma unroll
+    for (int c = 0; c < 4; ++c) s4[c] = sum[wv][c];
+#pragma unroll
+    for (int w = 0; w < kSplitWaves; ++w) {
+        if (w == wv) continue;
+        const double2 *src = (const double2 *)&s_lds.xch[wv][w][4 * lane];
+        const double2 a = src[0], b = src[1];
+        s4[0] += a.x;
+        s4[1] += a.y;
+        s4[2] += b.x;
+        s4[3] += b.y;
+    }
+    const bool pow2 = (n & (n - 1)) == 0;
+    double acc;
+    if (in.full && pow2)
+        acc = server_epilogue_sub<true, true>(s4, cv, sprev, n, lane, tile, wv, serr, sbits);
+    else if (in.full)
+        acc = server_epilogue_sub<true, false>(s4, cv, sprev, n, lane, tile, wv, serr, sbits);
+    else if (pow2)
+        acc = server_epilogue_sub<false, true>(s4, cv, sprev, n, lane, tile, wv, serr, sbits);
+    else
+        acc = server_epilogue_sub<false, false>(s4, cv, sprev, n, lane, tile, wv, serr, sbits);
+    acc = wave_sum_dpp(acc);
+    if (lane == 0) s_red[wv] = acc;
+    __syncthreads();
+    if (threadIdx.x == 0) partial[t] = (s_red[0] + s_red[1]) + (s_red[2] + s_red[3]);
 }
 
 
@@ -1503,11 +1678,17 @@ hipError_t launch_server_pass(const DeviceTables &tb, int64_t tile_begin, int64_
     int log2n = 0;
     while ((1 << log2n) < n) ++log2n;
     const int grouping_limit = 29 - log2n;
-    hipLaunchKernelGGL(k_server_pass, dim3((unsigned)blocks_for(tile_count)), dim3(kBlock), 0, s,
-                       tb.tiles, tb.chunk_tiles, tile_begin, tile_count, n, grouping_limit,
-                       wbits, bits_ld,
-                       bits_word_base, wscales, scales_ld, scales_seg_base, serr, sscales, sbits,
-                       partial);
+    // more than one batch of rows: the waves of a workgroup share each tile
+    if (n > kServerRowBatch)
+        hipLaunchKernelGGL(k_server_split, dim3((unsigned)xcd_grid(tile_count, 1)),
+                           dim3(kSplitWaves * kWave), 0, s, tb.tiles, tb.chunk_tiles, tile_begin,
+                           tile_count, n, grouping_limit, wbits, bits_ld, bits_word_base, wscales,
+                           scales_ld, scales_seg_base, serr, sscales, sbits, partial);
+    else
+        hipLaunchKernelGGL(k_server_pass, dim3((unsigned)blocks_for(tile_count)), dim3(kBlock), 0,
+                           s, tb.tiles, tb.chunk_tiles, tile_begin, tile_count, n, grouping_limit,
+                           wbits, bits_ld, bits_word_base, wscales, scales_ld, scales_seg_base,
+                           serr, sscales, sbits, partial);
     return hipGetLastError();
 }
 
