@@ -194,27 +194,13 @@ def cpu_baseline(st, plan, wl, target_s=10.0, threads=None, threaded_s=6.0):
             "single_thread": single}
 
 
-def hbm_probe(dev, nbytes=2 << 30, reps=10, rows=None):
-    """Achievable HBM bandwidth of plain streaming kernels of torch: a device
-    copy (one read stream, one write stream) and an elementwise add (two read
-    streams, one write stream: the read/write mix of the worker pass), each
-    over `nbytes` per operand; with `rows` (the workload's [n, D] gradient
-    rows), also torch's sum over the rows, the read pattern of the warm-up's
-    gradient average (read bytes only)."""
+def hbm_probe(dev, nbytes=2 << 30, reps=10):
+    """Achievable HBM bandwidth of two plain streaming kernels of torch: a
+    device copy (one read stream, one write stream) and an elementwise add
+    (two read streams, one write stream: the read/write mix of the worker
+    pass), each over `nbytes` per operand."""
     import torch
     out = {}
-    if rows is not None:
-        s = torch.sum(rows, dim=0)
-        torch.cuda.synchronize()
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        e0.record()
-        for _ in range(3):
-            torch.sum(rows, dim=0, out=s)
-        e1.record()
-        torch.cuda.synchronize()
-        ms = e0.elapsed_time(e1) / 3
-        out["sum_of_rows_read"] = rows.numel() * rows.element_size() / (ms * 1e-3) / 1e9
-        del s
     a = torch.empty(nbytes // 4, dtype=torch.float32, device=dev)
     b = torch.empty_like(a)
     c = torch.empty_like(a)
@@ -529,7 +515,7 @@ def main():
     }
     if not args.no_probe:
         del events
-        result["hbm_probe_gbps"] = hbm_probe(dev, rows=st.grads)
+        result["hbm_probe_gbps"] = hbm_probe(dev)
     if not args.no_cpu_baseline:
         log("timing the oracle on sampled segments ...")
         result["cpu_baseline"] = cpu_baseline(st, plan, wl)
