@@ -1117,8 +1117,9 @@ __device__ __forceinline__ bool server_grouped(const ServerRows &in, int n, int 
 }
 
 // ---------------------------------------------------------------------------
-// Chunk owners' pass, one wave per tile (every n): the wave walks the
-// incoming rows in batches of kServerRowBatch, then finishes the tile.  Each
+// Chunk owners' pass, one wave per tile (launched for n <= kServerRowBatch,
+// correct for any n): the wave walks the incoming rows in batches of
+// kServerRowBatch, then finishes the tile.  Each
 // wave owns its LDS staging area, so it synchronises only with itself; the
 // tile's error-state loads are issued first so that they overlap the
 // sign-word traffic, and the first batch is loaded before the exponent check.

@@ -107,16 +107,19 @@ def test_bert_large_full_size(ob, dev):
 
 
 def test_bert_large_full_size_bf16_grads(ob, dev):
-    """BERT-Large with bfloat16 gradients (the paper trains in 16-bit): chunk 7."""
-    _free_run_sampled(ob, dev, synth.get("bert_large"), warm=1, steps=2, sample_segs=[7],
+    """BERT-Large with bfloat16 gradients (the paper trains in 16-bit), 5
+    warm-up + 10 compression steps: chunk 7."""
+    wl = synth.get("bert_large")
+    _free_run_sampled(ob, dev, wl, warm=wl.warmup_steps, steps=10, sample_segs=[7],
                       grad_dtype=torch.bfloat16)
 
 
 def test_bert_base_full_size_fp16_grads(ob, dev):
-    """BERT-Base with float16 gradients: the per-tensor gradient scale puts
-    many of them in fp16's subnormal range, which the widening keeps exact:
-    chunk 3."""
-    _free_run_sampled(ob, dev, synth.get("bert_base"), warm=1, steps=2, sample_segs=[3],
+    """BERT-Base with float16 gradients, 5 warm-up + 10 compression steps:
+    the per-tensor gradient scale puts many of them in fp16's subnormal
+    range, which the widening keeps exact: chunk 3."""
+    wl = synth.get("bert_base")
+    _free_run_sampled(ob, dev, wl, warm=wl.warmup_steps, steps=10, sample_segs=[3],
                       grad_dtype=torch.float16)
 
 
