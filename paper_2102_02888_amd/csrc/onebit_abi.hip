@@ -270,131 +270,6 @@ int plan_create_impl(const int64_t *tensor_numel, int32_t num_tensors, int32_t n
     return ONEBIT_OK;
 }
 
-}  // namespace
-
-extern "C" {
-
-const char *onebit_status_str(int32_t status)
-{
-    switch (status) {
-    case ONEBIT_OK: return "ONEBIT_OK";
-    case ONEBIT_EINVAL: return "ONEBIT_EINVAL";
-    case ONEBIT_EALIGN: return "ONEBIT_EALIGN";
-    case ONEBIT_EHIP: return "ONEBIT_EHIP";
-    case ONEBIT_ENOMEM: return "ONEBIT_ENOMEM";
-    default: return "ONEBIT_UNKNOWN";
-    }
-}
-
-const char *onebit_last_error(void) { return g_last_error; }
-
-int onebit_plan_create(const int64_t *tensor_numel, int32_t num_tensors, int32_t n_workers,
-                       onebit_plan *out)
-{
-    if (!out) return fail(ONEBIT_EINVAL, "out is NULL");
-    *out = nullptr;
-    if (!tensor_numel) return fail(ONEBIT_EINVAL, "tensor_numel is NULL");
-    if (num_tensors < 1) return fail(ONEBIT_EINVAL, "num_tensors < 1");
-    if (n_workers < 1) return fail(ONEBIT_EINVAL, "n_workers < 1");
-    for (int32_t k = 0; k < num_tensors; ++k) {
-        if (tensor_numel[k] < 0) return fail(ONEBIT_EINVAL, "tensor_numel[%d] < 0", k);
-        // bounds the layout arithmetic (the padded total is limited to 2^40 below)
-        if (tensor_numel[k] > ((int64_t)1 << 40))
-            return fail(ONEBIT_EINVAL, "tensor_numel[%d] exceeds 2^40", k);
-    }
-    if ((int64_t)num_tensors * n_workers > INT32_MAX)
-        return fail(ONEBIT_EINVAL, "num_tensors * n_workers = %lld segments exceeds 2^31 - 1",
-                    (long long)num_tensors * n_workers);
-    try {
-        return plan_create_impl(tensor_numel, num_tensors, n_workers, out);
-    } catch (const std::bad_alloc &) {
-        return fail(ONEBIT_ENOMEM, "host allocation failed");
-    }
-}
-
-int onebit_plan_destroy(onebit_plan p)
-{
-    if (!p) return fail(ONEBIT_EINVAL, "plan is NULL");
-    int prev = -1;
-    (void)hipGetDevice(&prev);
-    if (prev != p->device) (void)hipSetDevice(p->device);
-    hipError_t e = hipFree(p->dev_mem);
-    if (prev >= 0 && prev != p->device) (void)hipSetDevice(prev);
-    delete p;
-    if (e != hipSuccess) return hip_fail(e, "hipFree of plan tables");
-    return ONEBIT_OK;
-}
-
-int onebit_plan_get_info(onebit_plan p, onebit_plan_sizes *info)
-{
-    if (!p) return fail(ONEBIT_EINVAL, "plan is NULL");
-    if (!info) return fail(ONEBIT_EINVAL, "info is NULL");
-    info->d = p->d;
-    info->padded_len = p->D;
-    info->words = p->W;
-    info->num_tensors = p->K;
-    info->num_segments = p->S;
-    info->num_tiles = p->T;
-    info->n_workers = p->n;
-    info->tile_elems = kTileElems;
-    info->workspace_bytes = p->workspace_bytes;
-    return ONEBIT_OK;
-}
-
-int onebit_plan_get_layout(onebit_plan p, int64_t *tensor_offset, int64_t *seg_begin,
-                           int64_t *seg_end)
-{
-    if (!p) return fail(ONEBIT_EINVAL, "plan is NULL");
-    if (tensor_offset) std::memcpy(tensor_offset, p->tensor_off.data(), p->K * sizeof(int64_t));
-    if (seg_begin) std::memcpy(seg_begin, p->seg_begin.data(), p->S * sizeof(int64_t));
-    if (seg_end) std::memcpy(seg_end, p->seg_end.data(), p->S * sizeof(int64_t));
-    return ONEBIT_OK;
-}
-
-int onebit_plan_info(onebit_plan p, int64_t *padded_len, int64_t *words, int64_t *num_segments,
-                     int64_t *chunk_len, size_t *workspace_bytes)
-{
-    if (!p) return fail(ONEBIT_EINVAL, "plan is NULL");
-    if (padded_len) *padded_len = p->D;
-    if (words) *words = p->W;
-    if (num_segments) *num_segments = p->S;
-    if (chunk_len) std::memcpy(chunk_len, p->chunk_len.data(), p->K * sizeof(int64_t));
-    if (workspace_bytes) *workspace_bytes = p->workspace_bytes;
-    return ONEBIT_OK;
-}
-
-int onebit_warmup_adam_step(onebit_plan p, float *x, float *m, float *v, const void *grads,
-                            int32_t grad_dtype, int64_t grad_ld, int32_t n_grads, float lr,
-                            float beta1,
-                            float beta2, float eps, int32_t bias_correction, int64_t step,
-                            onebit_stream stream)
-{
-    TRY(check_plan(p));
-    TRY(check_f32(p, x, "x"));
-    TRY(check_f32(p, m, "m"));
-    TRY(check_f32(p, v, "v"));
-    TRY(check_grads(p, grads, grad_dtype));
-    if (n_grads < 1) return fail(ONEBIT_EINVAL, "n_grads < 1");
-    if (step < 1) return fail(ONEBIT_EINVAL, "step < 1 (steps are 1-based)");
-    TRY(check_ld(grad_ld, p->D, n_grads > 1, "grad_ld"));
-    if (p->T == 0) return ONEBIT_OK;
-    float bc1 = 1.0f, bc2 = 1.0f;
-    if (bias_correction) {
-        bc1 = (float)(1.0 - std::pow((double)beta1, (double)step));
-        bc2 = (float)(1.0 - std::pow((double)beta2, (double)step));
-    }
-    TRY_HIP(onebit::launch_warmup(p->tb, p->T, x, m, v, grads, grad_dtype, grad_ld, n_grads, lr,
-                                  beta1,
-                                  beta2, eps, bias_correction ? 1 : 0, bc1, bc2,
-                                  (hipStream_t)stream),
-            "warm-up kernel launch");
-    return ONEBIT_OK;
-}
-
-}  // extern "C"
-
-namespace {
-
 // The three calls of a compression step, each split into its argument
 // checks and its launches, so that the fused step checks everything before
 // its first launch.
@@ -570,6 +445,123 @@ int step_impl(onebit_plan_s *p, float *x, float *m, const float *v_frozen, const
 }  // namespace
 
 extern "C" {
+
+const char *onebit_status_str(int32_t status)
+{
+    switch (status) {
+    case ONEBIT_OK: return "ONEBIT_OK";
+    case ONEBIT_EINVAL: return "ONEBIT_EINVAL";
+    case ONEBIT_EALIGN: return "ONEBIT_EALIGN";
+    case ONEBIT_EHIP: return "ONEBIT_EHIP";
+    case ONEBIT_ENOMEM: return "ONEBIT_ENOMEM";
+    default: return "ONEBIT_UNKNOWN";
+    }
+}
+
+const char *onebit_last_error(void) { return g_last_error; }
+
+int onebit_plan_create(const int64_t *tensor_numel, int32_t num_tensors, int32_t n_workers,
+                       onebit_plan *out)
+{
+    if (!out) return fail(ONEBIT_EINVAL, "out is NULL");
+    *out = nullptr;
+    if (!tensor_numel) return fail(ONEBIT_EINVAL, "tensor_numel is NULL");
+    if (num_tensors < 1) return fail(ONEBIT_EINVAL, "num_tensors < 1");
+    if (n_workers < 1) return fail(ONEBIT_EINVAL, "n_workers < 1");
+    for (int32_t k = 0; k < num_tensors; ++k) {
+        if (tensor_numel[k] < 0) return fail(ONEBIT_EINVAL, "tensor_numel[%d] < 0", k);
+        // bounds the layout arithmetic (the padded total is limited to 2^40 below)
+        if (tensor_numel[k] > ((int64_t)1 << 40))
+            return fail(ONEBIT_EINVAL, "tensor_numel[%d] exceeds 2^40", k);
+    }
+    if ((int64_t)num_tensors * n_workers > INT32_MAX)
+        return fail(ONEBIT_EINVAL, "num_tensors * n_workers = %lld segments exceeds 2^31 - 1",
+                    (long long)num_tensors * n_workers);
+    try {
+        return plan_create_impl(tensor_numel, num_tensors, n_workers, out);
+    } catch (const std::bad_alloc &) {
+        return fail(ONEBIT_ENOMEM, "host allocation failed");
+    }
+}
+
+int onebit_plan_destroy(onebit_plan p)
+{
+    if (!p) return fail(ONEBIT_EINVAL, "plan is NULL");
+    int prev = -1;
+    (void)hipGetDevice(&prev);
+    if (prev != p->device) (void)hipSetDevice(p->device);
+    hipError_t e = hipFree(p->dev_mem);
+    if (prev >= 0 && prev != p->device) (void)hipSetDevice(prev);
+    delete p;
+    if (e != hipSuccess) return hip_fail(e, "hipFree of plan tables");
+    return ONEBIT_OK;
+}
+
+int onebit_plan_get_info(onebit_plan p, onebit_plan_sizes *info)
+{
+    if (!p) return fail(ONEBIT_EINVAL, "plan is NULL");
+    if (!info) return fail(ONEBIT_EINVAL, "info is NULL");
+    info->d = p->d;
+    info->padded_len = p->D;
+    info->words = p->W;
+    info->num_tensors = p->K;
+    info->num_segments = p->S;
+    info->num_tiles = p->T;
+    info->n_workers = p->n;
+    info->tile_elems = kTileElems;
+    info->workspace_bytes = p->workspace_bytes;
+    return ONEBIT_OK;
+}
+
+int onebit_plan_get_layout(onebit_plan p, int64_t *tensor_offset, int64_t *seg_begin,
+                           int64_t *seg_end)
+{
+    if (!p) return fail(ONEBIT_EINVAL, "plan is NULL");
+    if (tensor_offset) std::memcpy(tensor_offset, p->tensor_off.data(), p->K * sizeof(int64_t));
+    if (seg_begin) std::memcpy(seg_begin, p->seg_begin.data(), p->S * sizeof(int64_t));
+    if (seg_end) std::memcpy(seg_end, p->seg_end.data(), p->S * sizeof(int64_t));
+    return ONEBIT_OK;
+}
+
+int onebit_plan_info(onebit_plan p, int64_t *padded_len, int64_t *words, int64_t *num_segments,
+                     int64_t *chunk_len, size_t *workspace_bytes)
+{
+    if (!p) return fail(ONEBIT_EINVAL, "plan is NULL");
+    if (padded_len) *padded_len = p->D;
+    if (words) *words = p->W;
+    if (num_segments) *num_segments = p->S;
+    if (chunk_len) std::memcpy(chunk_len, p->chunk_len.data(), p->K * sizeof(int64_t));
+    if (workspace_bytes) *workspace_bytes = p->workspace_bytes;
+    return ONEBIT_OK;
+}
+
+int onebit_warmup_adam_step(onebit_plan p, float *x, float *m, float *v, const void *grads,
+                            int32_t grad_dtype, int64_t grad_ld, int32_t n_grads, float lr,
+                            float beta1,
+                            float beta2, float eps, int32_t bias_correction, int64_t step,
+                            onebit_stream stream)
+{
+    TRY(check_plan(p));
+    TRY(check_f32(p, x, "x"));
+    TRY(check_f32(p, m, "m"));
+    TRY(check_f32(p, v, "v"));
+    TRY(check_grads(p, grads, grad_dtype));
+    if (n_grads < 1) return fail(ONEBIT_EINVAL, "n_grads < 1");
+    if (step < 1) return fail(ONEBIT_EINVAL, "step < 1 (steps are 1-based)");
+    TRY(check_ld(grad_ld, p->D, n_grads > 1, "grad_ld"));
+    if (p->T == 0) return ONEBIT_OK;
+    float bc1 = 1.0f, bc2 = 1.0f;
+    if (bias_correction) {
+        bc1 = (float)(1.0 - std::pow((double)beta1, (double)step));
+        bc2 = (float)(1.0 - std::pow((double)beta2, (double)step));
+    }
+    TRY_HIP(onebit::launch_warmup(p->tb, p->T, x, m, v, grads, grad_dtype, grad_ld, n_grads, lr,
+                                  beta1,
+                                  beta2, eps, bias_correction ? 1 : 0, bc1, bc2,
+                                  (hipStream_t)stream),
+            "warm-up kernel launch");
+    return ONEBIT_OK;
+}
 
 int onebit_worker_compress(onebit_plan p, const float *m, const uint64_t *m_bits,
                            const float *m_scales, const void *grads, int32_t grad_dtype,

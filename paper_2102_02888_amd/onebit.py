@@ -245,19 +245,15 @@ def onebit_decompress_update(plan, server_bits, server_scales, x, m_out, v_froze
          _ptr(v_frozen, torch.float32, "v_frozen", D), lr, eps, _stream(stream))
 
 
-def onebit_step(plan, x, m, v_frozen, grads, worker_err, server_err, worker_bits,
-                worker_scales, server_bits, server_scales, lr, beta1, eps, workspace,
-                stream=None, events=None):
-    """The fused step.  events: optional four torch.cuda.Event objects
-    (already recorded once, so that their HIP events exist) marked on the
-    stream before the worker pass, the chunk owners' pass and the update, and
-    after the update (onebit_step_events)."""
+def _step_args(name, plan, x, m, v_frozen, grads, worker_err, server_err, worker_bits,
+               worker_scales, server_bits, server_scales, lr, beta1, eps):
+    """The arguments the fused step's entry points share, up to eps."""
     n, D, W, S = plan.n, plan.D, plan.W, plan.S
     # the step addresses worker_bits / worker_scales with row strides W and S
-    for t, name, cols in ((worker_bits, "worker_bits", W), (worker_scales, "worker_scales", S)):
+    for t, tname, cols in ((worker_bits, "worker_bits", W), (worker_scales, "worker_scales", S)):
         if t is not None and t.dim() == 2 and cols > 0 and t.stride(0) != cols:
-            raise ValueError("%s must be contiguous [n, %d] for onebit_step" % (name, cols))
-    args = [plan.handle, _ptr(x, torch.float32, "x", D),
+            raise ValueError("%s must be contiguous [n, %d] for %s" % (tname, cols, name))
+    return [plan.handle, _ptr(x, torch.float32, "x", D),
             _ptr(m, torch.float32, "m", D), _ptr(v_frozen, torch.float32, "v_frozen", D),
             *_grads(grads, D, n), _ld(grads),
             _ptr(worker_err, torch.float32, "worker_err", D, n), _ld(worker_err),
@@ -265,8 +261,19 @@ def onebit_step(plan, x, m, v_frozen, grads, worker_err, server_err, worker_bits
             _ptr(worker_bits, torch.int64, "worker_bits", W, n),
             _ptr(worker_scales, torch.float32, "worker_scales", S, n),
             _ptr(server_bits, torch.int64, "server_bits", W),
-            _ptr(server_scales, torch.float32, "server_scales", S), lr, beta1, eps,
-            _ptr(workspace, torch.float64, "workspace", plan.workspace_words)]
+            _ptr(server_scales, torch.float32, "server_scales", S), lr, beta1, eps]
+
+
+def onebit_step(plan, x, m, v_frozen, grads, worker_err, server_err, worker_bits,
+                worker_scales, server_bits, server_scales, lr, beta1, eps, workspace,
+                stream=None, events=None):
+    """The fused step.  events: optional four torch.cuda.Event objects
+    (already recorded once, so that their HIP events exist) marked on the
+    stream before the worker pass, the chunk owners' pass and the update, and
+    after the update (onebit_step_events)."""
+    args = _step_args("onebit_step", plan, x, m, v_frozen, grads, worker_err, server_err,
+                      worker_bits, worker_scales, server_bits, server_scales, lr, beta1, eps)
+    args.append(_ptr(workspace, torch.float64, "workspace", plan.workspace_words))
     if events is None:
         call("onebit_step", *args, _stream(stream))
         return
@@ -286,19 +293,10 @@ def onebit_step_noalloc(plan, x, m, v_frozen, grads, worker_err, server_err, wor
     """onebit_step without a workspace: the library's static scratch array on
     the device holds the partial sums (calls on one GPU share it and must not
     overlap)."""
-    n, D, W, S = plan.n, plan.D, plan.W, plan.S
-    for t, name, cols in ((worker_bits, "worker_bits", W), (worker_scales, "worker_scales", S)):
-        if t is not None and t.dim() == 2 and cols > 0 and t.stride(0) != cols:
-            raise ValueError("%s must be contiguous [n, %d] for onebit_step_noalloc" % (name, cols))
-    call("onebit_step_noalloc", plan.handle, _ptr(x, torch.float32, "x", D),
-         _ptr(m, torch.float32, "m", D), _ptr(v_frozen, torch.float32, "v_frozen", D),
-         *_grads(grads, D, n), _ld(grads),
-         _ptr(worker_err, torch.float32, "worker_err", D, n), _ld(worker_err),
-         _ptr(server_err, torch.float32, "server_err", D),
-         _ptr(worker_bits, torch.int64, "worker_bits", W, n),
-         _ptr(worker_scales, torch.float32, "worker_scales", S, n),
-         _ptr(server_bits, torch.int64, "server_bits", W),
-         _ptr(server_scales, torch.float32, "server_scales", S), lr, beta1, eps, _stream(stream))
+    args = _step_args("onebit_step_noalloc", plan, x, m, v_frozen, grads, worker_err,
+                      server_err, worker_bits, worker_scales, server_bits, server_scales, lr,
+                      beta1, eps)
+    call("onebit_step_noalloc", *args, _stream(stream))
 
 
 def onebit_decode(plan, bits, scales, out, stream=None):
