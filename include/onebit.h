@@ -93,7 +93,11 @@ typedef struct {
     int64_t num_tiles;       /* work tiles (<= 1024 elements, one segment)  */
     int32_t n_workers;       /* n                                           */
     int32_t tile_elems;      /* elements per full tile                      */
-    size_t workspace_bytes;  /* workspace needed by the calls below         */
+    size_t workspace_bytes;  /* workspace needed by the calls below: per-tile
+                                partial sums, and the chunk owners' lookup
+                                tables (2 KB per segment and group of 8
+                                workers) when those of all S segments fit
+                                in 32 MiB                                   */
 } onebit_plan_sizes;
 
 /* Creates a plan for K = num_tensors tensors (tensor_numel[k] >= 0, host
@@ -244,11 +248,12 @@ int onebit_step(onebit_plan plan, float *x, float *m, const float *v_frozen,
  * GPU shares that GPU's array: calls that overlap on one GPU (other streams,
  * other threads, other plans) race and must be serialised by the caller.
  * Nothing in the array needs clearing between calls (each step writes every
- * partial it reads).  Errors: those of onebit_step; EINVAL when the plan's
- * workspace_bytes (about 8 (n + 1) bytes per tile of 1024 elements) exceeds
- * ONEBIT_NOALLOC_SCRATCH_BYTES -- a BERT-Large-shaped buffer of 334M
- * parameters with n = 32 needs 86 MB and fits; EHIP if the array's address
- * cannot be found. */
+ * partial and table entry it reads).  Errors: those of onebit_step; EINVAL
+ * when the plan's workspace_bytes (about 8 (n + 1) bytes per tile of 1024
+ * elements, plus 2 KB per segment and group of 8 workers when the plan keeps
+ * the chunk owners' tables) exceeds ONEBIT_NOALLOC_SCRATCH_BYTES -- a
+ * BERT-Large-shaped buffer of 334M parameters with n = 32 needs 86 MB and
+ * fits; EHIP if the array's address cannot be found. */
 #define ONEBIT_NOALLOC_SCRATCH_BYTES ((size_t)96 << 20)
 int onebit_step_noalloc(onebit_plan plan, float *x, float *m, const float *v_frozen,
                         const void *grads, int32_t grad_dtype, int64_t grad_ld,

@@ -34,6 +34,7 @@ struct onebit_plan_s {
     std::vector<int64_t> chunk_word_lo, chunk_word_hi;  // [n], words touched by chunk j
     void *dev_mem = nullptr;                            // one allocation for all tables
     DeviceTables tb{};
+    size_t table_bytes = 0;  // chunk owners' lookup tables in the workspace (0: none)
     size_t workspace_bytes = 0;
 };
 
@@ -61,12 +62,29 @@ bool aligned(const void *p, size_t a) { return ((uintptr_t)p % a) == 0; }
 size_t round_up(size_t a, size_t m) { return (a + m - 1) / m * m; }
 
 // Workspace: per-tile fp64 partial sums, n rows for the workers then one row
-// for the chunk owners.
+// for the chunk owners; then, when the plan keeps them, the chunk owners'
+// lookup tables of every segment and one flag per segment.
 size_t worker_partial_offset(const onebit_plan_s *) { return 0; }
 size_t server_partial_offset(const onebit_plan_s *p)
 {
     return round_up((size_t)p->n * (size_t)p->T * sizeof(double), 256);
 }
+size_t server_table_offset(const onebit_plan_s *p)
+{
+    return server_partial_offset(p) + round_up((size_t)p->T * sizeof(double) + 1, 256);
+}
+size_t server_flag_offset(const onebit_plan_s *p)
+{
+    return server_table_offset(p) + p->table_bytes;
+}
+
+// The tables of a plan's segments are kept in the workspace (built once per
+// chunk owners' call instead of once per tile) when all of them fit in this
+// many bytes: 256 KB for a BERT-Large-sized buffer with n = 32, 16 MB for
+// one tensor with n = 256.
+constexpr size_t kServerTableBudget = (size_t)32 << 20;
+// ... and a call uses them when its segments average at least this many tiles.
+constexpr int64_t kServerTableMinTiles = 4;
 
 int check_plan(const onebit_plan_s *p)
 {
@@ -265,7 +283,12 @@ int plan_create_impl(const int64_t *tensor_numel, int32_t num_tensors, int32_t n
     p->tb.seg_tile_begin = d_stb;
     p->tb.seg_tile_end = d_ste;
     p->tb.seg_len = d_sl;
-    p->workspace_bytes = server_partial_offset(p) + round_up((size_t)p->T * sizeof(double) + 1, 256);
+    const size_t seg_tables = onebit::server_table_bytes(p->n, 1);
+    p->table_bytes = (size_t)p->S <= kServerTableBudget / seg_tables
+                         ? onebit::server_table_bytes(p->n, p->S)
+                         : 0;
+    p->workspace_bytes = server_flag_offset(p) +
+                         (p->table_bytes ? round_up((size_t)p->S * sizeof(int32_t), 256) : 0);
     *out = owner.release();
     return ONEBIT_OK;
 }
@@ -372,11 +395,17 @@ int run_server(const onebit_plan_s *p, int32_t server_begin, int32_t server_end,
     const int64_t tb = p->chunk_tile_begin[server_begin];
     const int64_t tc = p->chunk_tile_begin[server_end] - tb;
     double *part = (double *)((char *)workspace + server_partial_offset(p));
+    const int nown = server_end - server_begin;
+    const int64_t owned = (int64_t)p->K * nown;
+    const bool use_tables = p->table_bytes > 0 && tc >= kServerTableMinTiles * owned;
+    double *tables = use_tables ? (double *)((char *)workspace + server_table_offset(p)) : nullptr;
+    int32_t *flags = use_tables ? (int32_t *)((char *)workspace + server_flag_offset(p)) : nullptr;
     if (tc > 0)
         TRY_HIP(onebit::launch_server_pass(p->tb, tb, tc, p->n, worker_bits, bits_ld,
                                            bits_word_base, worker_scales, scales_ld,
                                            scales_seg_base, server_err, server_scales,
-                                           server_bits, part, s),
+                                           server_bits, part, p->K, server_begin, nown, tables,
+                                           flags, s),
                 "server kernel launch");
     TRY_HIP(onebit::launch_finalize(p->tb, p->max_seg_tiles,
                                     (int64_t)p->K * (server_end - server_begin), p->S, 1, p->n,

@@ -78,11 +78,21 @@ hipError_t launch_finalize(const DeviceTables &tb, int64_t max_seg_tiles, int64_
                            const double *partial, int64_t part_ld, float *scales,
                            int64_t scales_ld, hipStream_t s);
 
+// Bytes of the chunk owners' lookup tables for `segments` owned segments.
+size_t server_table_bytes(int n, int64_t segments);
+
+// The chunk owners' pass over tiles [tile_begin, tile_begin + tile_count) of
+// the chunk-major tile list, for chunks [cb, cb + nown) of num_tensors
+// tensors.  tables != NULL (at least server_table_bytes(n, num_tensors *
+// nown) bytes, 256-byte aligned) and flags (num_tensors * nown int32): the
+// owned segments' tables are built there first and copied by the pass;
+// tables == NULL: the pass builds them per tile.
 hipError_t launch_server_pass(const DeviceTables &tb, int64_t tile_begin, int64_t tile_count,
                               int n, const uint64_t *wbits, int64_t bits_ld,
                               int64_t bits_word_base, const float *wscales, int64_t scales_ld,
                               int64_t scales_seg_base, float *serr, float *sscales,
-                              uint64_t *sbits, double *partial, hipStream_t s);
+                              uint64_t *sbits, double *partial, int num_tensors, int cb,
+                              int nown, double *tables, int32_t *flags, hipStream_t s);
 
 hipError_t launch_update(const DeviceTables &tb, int64_t num_tiles, const uint64_t *sbits,
                          const float *sscales, float *x, float *m_out, const float *v,

@@ -798,9 +798,9 @@ __global__ __launch_bounds__(kBlock) void k_finalize(
 // incoming messages, add the server error, write the sign words and the new
 // compensated server state, and the tile's sum of squares.
 //
-// Each wave owns one tile and its own LDS region, so it synchronises only
-// with itself (no workgroup barrier); the tile's error-state loads are issued
-// first so that they overlap the sign-word traffic.  Incoming sign words are
+// Each wave owns its own LDS region, so it synchronises only with itself (no
+// workgroup barrier); a tile's error-state loads are issued first so that
+// they overlap the sign-word traffic.  Incoming sign words are
 // staged in LDS 32 worker rows at a time (coalesced 128-byte row reads),
 // transposed so that the words of consecutive workers for one 32-element
 // half-word are adjacent.  For the table lookups each group of 8 workers is
@@ -813,9 +813,10 @@ __global__ __launch_bounds__(kBlock) void k_finalize(
 // fp64 (the scales' exponents span at most 29 - ceil(log2 n) binades; true
 // for any realistic message set) the sum is exact, so it may be formed in any
 // grouping: then each group of 8 workers is one lookup in a 256-entry table
-// of its signed scale sums, indexed by the 8 workers' bits of the element.  The 256-entry tables are sums of two
-// 16-entry tables, each built from 4 scales.  Otherwise every worker is added
-// one by one.  Both give the oracle's sum.
+// of its signed scale sums, indexed by the 8 workers' bits of the element.
+// The 256-entry tables are sums of two 16-entry tables, each built from 4
+// scales; they depend on the segment's scales only.  Otherwise every worker
+// is added one by one.  Both give the oracle's sum.
 // ---------------------------------------------------------------------------
 // Wave-wide max of an int through DPP: shifts within each 16-lane row, then
 // row broadcasts carry the row maxima up to lane 63, which every lane reads.
@@ -888,11 +889,26 @@ constexpr int kBitsStride = kServerRowBatch + 8;
 
 // One wave's LDS working set for a batch of up to kServerRowBatch incoming
 // rows of one tile: the sign words, transposed ([half-word h][row r]), the
-// rows' scales, and the lookup tables built from them.
+// rows' scales, and the lookup tables built from them (the 256-entry tables
+// of two groups of 8 rows at a time).
 struct ServerBatchLds {
     uint32_t bits[2 * kTileWords][kBitsStride];
     double lut4[kServerRowBatch / 4][16];
     double lut8[2][256];
+    float scale[kServerRowBatch];
+};
+
+// One wave's LDS working set in the one-wave pass over a run of tiles
+// (n <= kServerRowBatch): the 256-entry tables of every group of 8 rows stay
+// built while the run stays in one segment.  The 16-entry tables are only
+// needed while those are built, before the tile's words are staged, so they
+// share the staging area.
+struct ServerRunLds {
+    union {
+        uint32_t bits[2 * kTileWords][kBitsStride];
+        double lut4[kServerRowBatch / 4][16];
+    };
+    double lut8[kServerRowBatch / 8][256];
     float scale[kServerRowBatch];
 };
 
@@ -934,11 +950,10 @@ struct ServerRows {
     bool full;               // a full tile
 };
 
-// Loads rows [r0, r0 + rows) of the tile (rows <= kServerRowBatch): lane L
-// takes word wi = L % 16 of rows r0 + L/16 + 4k, and the scale of row r0 + L.
-__device__ __forceinline__ void server_load_batch(const ServerRows &in, int r0, int rows,
-                                                  int lane, uint64_t (&stg)[kServerRowBatch / 4],
-                                                  float &scl)
+// Loads the words of rows [r0, r0 + rows) of the tile (rows <=
+// kServerRowBatch): lane L takes word wi = L % 16 of rows r0 + L/16 + 4k.
+__device__ __forceinline__ void server_load_words(const ServerRows &in, int r0, int rows,
+                                                  int lane, uint64_t (&stg)[kServerRowBatch / 4])
 {
     const int wi = lane & (kTileWords - 1);
     const uint64_t *p = in.words + (int64_t)(r0 + (lane >> 4)) * in.bits_ld + wi;
@@ -953,15 +968,23 @@ __device__ __forceinline__ void server_load_batch(const ServerRows &in, int r0, 
             stg[k] = (r < rows && wi < in.nwords) ? __builtin_nontemporal_load(p + k * step) : 0ull;
         }
     }
+}
+
+// The words of rows [r0, r0 + rows) and the scale of row r0 + lane.
+__device__ __forceinline__ void server_load_batch(const ServerRows &in, int r0, int rows,
+                                                  int lane, uint64_t (&stg)[kServerRowBatch / 4],
+                                                  float &scl)
+{
+    server_load_words(in, r0, rows, lane, stg);
     scl = lane < rows ? in.scales[(int64_t)(r0 + lane) * in.scales_ld] : 0.f;
 }
 
-// Writes a loaded batch into the wave's staging area (rows past the batch's
+// Writes loaded words into the wave's staging area (rows past the batch's
 // last row, up to the next multiple of 8, get zero words).
-__device__ __forceinline__ void server_stage_batch(ServerBatchLds &L, const ServerRows &in,
-                                                   int rows, int lane,
-                                                   const uint64_t (&stg)[kServerRowBatch / 4],
-                                                   float scl)
+template <class Lds>
+__device__ __forceinline__ void server_stage_words(Lds &L, const ServerRows &in, int rows,
+                                                   int lane,
+                                                   const uint64_t (&stg)[kServerRowBatch / 4])
 {
     const int wi = lane & (kTileWords - 1);
     const int rows8 = (rows + 7) & ~7;
@@ -982,22 +1005,26 @@ __device__ __forceinline__ void server_stage_batch(ServerBatchLds &L, const Serv
             }
         }
     }
+}
+
+// Stages a loaded batch: its words, and the scale of row `lane`.
+template <class Lds>
+__device__ __forceinline__ void server_stage_batch(Lds &L, const ServerRows &in,
+                                                   int rows, int lane,
+                                                   const uint64_t (&stg)[kServerRowBatch / 4],
+                                                   float scl)
+{
+    server_stage_words(L, in, rows, lane, stg);
     if (lane < rows) L.scale[lane] = scl;
 }
 
-// sum += the staged batch's decoded messages, grouped: each group of 8 rows is
-// one lookup in a 256-entry table of its signed scale sums (exact, so any
-// grouping gives the worker-order sum).  The 16-entry tables of 4 rows are
-// built first; each (half-word, group) block is then regrouped in place by
-// four 8x8 bit transposes, after which byte e>>3 of word r8 + (e&7) is
-// element e's table index.
-__device__ __forceinline__ void server_batch_grouped(double (&sum)[kSubBlocks][4],
-                                                     ServerBatchLds &L, int rows, int lane)
+// The 16-entry tables of 4 rows, two per group of 8 (rows past the last row
+// add 0): lut4[q][idx] is the sum over k < 4 of +-scale[4q + k], + where bit
+// k of idx is set.
+template <class Lds>
+__device__ __forceinline__ void server_build_lut4(Lds &L, int rows, int lane)
 {
-    const int half = (lane >> 3) & 1;
     const int groups8 = (rows + 7) >> 3;
-    // 16-entry tables of 4 workers, two per group of 8 (rows past the last
-    // worker add 0)
     for (int e = lane; e < 32 * groups8; e += kWave) {
         const int q = e >> 4, idx = e & 15;
         double v = 0.0;
@@ -1011,6 +1038,15 @@ __device__ __forceinline__ void server_batch_grouped(double (&sum)[kSubBlocks][4
         }
         L.lut4[q][idx] = v;
     }
+}
+
+// Regroups each staged (half-word, group of 8 rows) block in place by four
+// 8x8 bit transposes, after which byte e>>3 of word r8 + (e&7) of the block is
+// element e's table index (the 8 rows' bits of e).
+template <class Lds>
+__device__ __forceinline__ void server_regroup_bits(Lds &L, int rows, int lane)
+{
+    const int groups8 = (rows + 7) >> 3;
 #pragma unroll 1
     for (int k = 0; k < (2 * kTileWords) * (kServerRowBatch / 8) / kWave; ++k) {
         const int blk = lane + kWave * k;
@@ -1025,8 +1061,54 @@ __device__ __forceinline__ void server_batch_grouped(double (&sum)[kSubBlocks][4
             *(uint4 *)(p + 4) = make_uint4(a[4], a[5], a[6], a[7]);
         }
     }
+}
+
+// sum += the group of 8 rows starting at row r8, one lookup per element in
+// its 256-entry table lut (regrouped words).  Two sub-blocks at a time: their
+// 8 table indices first, then the 8 lookups, then the adds, so that the LDS
+// round trips overlap.
+template <class Lds>
+__device__ __forceinline__ void server_lookup_group(double (&sum)[kSubBlocks][4], const Lds &L,
+                                                    int r8, const double *lut, int lane)
+{
+    const int half = (lane >> 3) & 1;
+#pragma unroll
+    for (int bh = 0; bh < kSubBlocks; bh += 2) {
+        uint32_t idx[2][4];
+#pragma unroll
+        for (int bb = 0; bb < 2; ++bb) {
+            const int hw = 2 * (4 * (bh + bb) + (lane >> 4)) + half;
+            // the lane's elements e = 4 (lane & 7) + c of the half-word:
+            // byte e >> 3 of word e & 7 holds the 8 rows' bits of e
+            const uint8_t *blk = (const uint8_t *)&L.bits[hw][r8];
+            const int o = 16 * (lane & 1) + ((lane & 7) >> 1);
+#pragma unroll
+            for (int c = 0; c < 4; ++c) idx[bb][c] = blk[o + 4 * c];
+        }
+        double val[2][4];
+#pragma unroll
+        for (int bb = 0; bb < 2; ++bb)
+#pragma unroll
+            for (int c = 0; c < 4; ++c) val[bb][c] = lut[idx[bb][c]];
+#pragma unroll
+        for (int bb = 0; bb < 2; ++bb)
+#pragma unroll
+            for (int c = 0; c < 4; ++c) sum[bh + bb][c] += val[bb][c];
+    }
+}
+
+// sum += the staged batch's decoded messages, grouped: each group of 8 rows is
+// one lookup in a 256-entry table of its signed scale sums (exact, so any
+// grouping gives the worker-order sum).  The 16-entry tables of 4 rows are
+// built first, then the staged words are regrouped; the 256-entry tables are
+// built two groups at a time.
+__device__ __forceinline__ void server_batch_grouped(double (&sum)[kSubBlocks][4],
+                                                     ServerBatchLds &L, int rows, int lane)
+{
+    const int groups8 = (rows + 7) >> 3;
+    server_build_lut4(L, rows, lane);
+    server_regroup_bits(L, rows, lane);
     wave_sync();
-    // two groups of 8 workers at a time
     for (int g0 = 0; 8 * g0 < rows; g0 += 2) {
         const int gcnt = min(2, groups8 - g0);
 #pragma unroll
@@ -1039,43 +1121,16 @@ __device__ __forceinline__ void server_batch_grouped(double (&sum)[kSubBlocks][4
             }
         }
         wave_sync();
-        for (int g = 0; g < gcnt; ++g) {
-            const int r8 = 8 * (g0 + g);
-            // two sub-blocks at a time: their 8 table indices first, then the
-            // 8 lookups, then the adds, so that the LDS round trips overlap
-#pragma unroll
-            for (int bh = 0; bh < kSubBlocks; bh += 2) {
-                uint32_t idx[2][4];
-#pragma unroll
-                for (int bb = 0; bb < 2; ++bb) {
-                    const int hw = 2 * (4 * (bh + bb) + (lane >> 4)) + half;
-                    // the lane's elements e = 4 (lane & 7) + c of the half-word:
-                    // byte e >> 3 of word e & 7 holds the 8 workers' bits of e
-                    const uint8_t *blk = (const uint8_t *)&L.bits[hw][r8];
-                    const int o = 16 * (lane & 1) + ((lane & 7) >> 1);
-#pragma unroll
-                    for (int c = 0; c < 4; ++c) idx[bb][c] = blk[o + 4 * c];
-                }
-                double val[2][4];
-#pragma unroll
-                for (int bb = 0; bb < 2; ++bb)
-#pragma unroll
-                    for (int c = 0; c < 4; ++c) val[bb][c] = L.lut8[g][idx[bb][c]];
-#pragma unroll
-                for (int bb = 0; bb < 2; ++bb)
-#pragma unroll
-                    for (int c = 0; c < 4; ++c) sum[bh + bb][c] += val[bb][c];
-            }
-        }
+        for (int g = 0; g < gcnt; ++g) server_lookup_group(sum, L, 8 * (g0 + g), L.lut8[g], lane);
         wave_sync();
     }
 }
 
 // sum += the staged batch's decoded messages one worker at a time, in row
 // order (the path for scale sets whose partial sums may round).
+template <class Lds>
 __device__ __forceinline__ void server_batch_one_by_one(double (&sum)[kSubBlocks][4],
-                                                        const ServerBatchLds &L, int rows,
-                                                        int lane)
+                                                        const Lds &L, int rows, int lane)
 {
     const int half = (lane >> 3) & 1;
     const int shift = 4 * (lane & 7);
@@ -1116,27 +1171,132 @@ __device__ __forceinline__ bool server_grouped(const ServerRows &in, int n, int 
     return emax < 255 && (emax == 0 || emax - emin <= grouping_limit);
 }
 
+// The last part of a tile for every sub-block: average, add the server error,
+// store the new compensated error state and the sign words; returns the
+// wave's fp64 sum of squares of the tile (every lane gets it).  FULL and POW2
+// are wave-uniform, so each wave runs one variant.
+__device__ __forceinline__ double server_epilogue(const double (&sum)[kSubBlocks][4],
+                                                  const v4f (&cv)[kSubBlocks], float sprev, int n,
+                                                  int lane, const Tile &tile, bool full,
+                                                  float *__restrict__ serr,
+                                                  uint64_t *__restrict__ sbits)
+{
+    const bool pow2 = (n & (n - 1)) == 0;
+    double acc = 0.0;
+#pragma unroll
+    for (int b = 0; b < kSubBlocks; ++b) {
+        if (full && pow2)
+            acc += server_epilogue_sub<true, true>(sum[b], cv[b], sprev, n, lane, tile, b, serr, sbits);
+        else if (full)
+            acc += server_epilogue_sub<true, false>(sum[b], cv[b], sprev, n, lane, tile, b, serr, sbits);
+        else if (pow2)
+            acc += server_epilogue_sub<false, true>(sum[b], cv[b], sprev, n, lane, tile, b, serr, sbits);
+        else
+            acc += server_epilogue_sub<false, false>(sum[b], cv[b], sprev, n, lane, tile, b, serr, sbits);
+    }
+    return wave_sum_dpp(acc);
+}
+
 // ---------------------------------------------------------------------------
-// Chunk owners' pass, one wave per tile (launched for n <= kServerRowBatch,
-// correct for any n): the wave walks the incoming rows in batches of
-// kServerRowBatch, then finishes the tile.  Each
-// wave owns its LDS staging area, so it synchronises only with itself; the
-// tile's error-state loads are issued first so that they overlap the
-// sign-word traffic, and the first batch is loaded before the exponent check.
+// Tables of the owned segments, built once per call when the caller's
+// workspace holds them: for owned segment u (segment q = k*n + j of chunk j
+// in [cb, cb + nown), u = k*nown + j - cb) flags[u] says whether the grouped
+// sum applies, and if so tables[(u*groups8 + g)*256 + idx] is the signed sum
+// of the scales of rows 8g .. 8g+7 (+ where bit k of idx is set; rows past n
+// add nothing).  One workgroup per (owned segment, group); each decides on
+// the segment's flag by itself, and group 0's writes it.  Every entry is an
+// exact fp64 sum when the flag is set, so it equals the in-kernel tables'.
 // ---------------------------------------------------------------------------
+__global__ __launch_bounds__(kBlock) void k_server_tables(
+    int n, int cb, int nown, int grouping_limit, const float *__restrict__ wscales,
+    int64_t scales_ld, int64_t scales_seg_base, double *__restrict__ tables,
+    int32_t *__restrict__ flags)
+{
+    const int groups8 = (n + 7) >> 3;
+    const int64_t u = blockIdx.x / groups8;
+    const int g = blockIdx.x - u * groups8;
+    const int64_t q = (u / nown) * n + cb + (u % nown);
+    const float *sc = wscales + (q - scales_seg_base);
+    const int lane = threadIdx.x & (kWave - 1);
+    const ServerRows in{nullptr, 0, sc, scales_ld, 0, false};
+    // every wave reads the n scales and reaches the same decision
+    const float first = (n <= kServerRowBatch && lane < n) ? sc[(int64_t)lane * scales_ld] : 0.f;
+    const bool ok = server_grouped(in, n, grouping_limit, lane, first);
+    if (g == 0 && threadIdx.x == 0) flags[u] = ok ? 1 : 0;
+    if (!ok) return;
+    static_assert(kBlock == 256, "one table entry per thread");
+    const int idx = threadIdx.x;
+    double v = 0.0;
+    for (int k = 0; k < 8 && 8 * g + k < n; ++k) {
+        const double s = (double)sc[(int64_t)(8 * g + k) * scales_ld];
+        v += ((idx >> k) & 1) ? s : -s;
+    }
+    tables[((u * groups8) + g) * 256 + idx] = v;
+}
+
+// Where a call's owned-segment tables are (TABLES launches), passed as is.
+struct ServerTables {
+    const double *tables;
+    const int32_t *flags;
+    int cb;    // first owned chunk
+    int nown;  // owned chunks
+};
+
+// Copies the 256-entry tables of groups [g0, g0 + gcnt) of owned segment u
+// into lut (gcnt 2 KB tables) with direct global-to-LDS loads, 1 KB per
+// instruction: lane L's 16 bytes land at byte 16 L of each kilobyte.  The
+// caller waits for them (vmcnt) before reading lut.
+__device__ __forceinline__ void server_fetch_tables(double *lut, const ServerTables &st,
+                                                    int64_t u, int groups8, int g0, int gcnt,
+                                                    int lane)
+{
+    const char *src = (const char *)(st.tables + (u * groups8 + g0) * 256) + 16 * lane;
+    for (int k = 0; k < 2 * gcnt; ++k)
+        __builtin_amdgcn_global_load_lds((const void *)(src + 1024 * k),
+                                         (__attribute__((address_space(3))) void *)((char *)lut +
+                                                                                    1024 * k),
+                                         16, 0, 0);
+}
+
+// Owned segment index of segment q.
+__device__ __forceinline__ int64_t owned_segment(int64_t q, int n, const ServerTables &st)
+{
+    const int64_t k = q / n;
+    return k * st.nown + (q - k * n) - st.cb;
+}
+
+// Waits for every vector memory operation of the wave, the direct-to-LDS
+// table loads included (the compiler does not track those).
+__device__ __forceinline__ void wait_vmem() { __builtin_amdgcn_s_waitcnt(0x0F70); }
+
+// ---------------------------------------------------------------------------
+// Chunk owners' pass for n <= kServerRowBatch, one wave per tile.  The tile's
+// error-state and sign-word loads are issued first.  With TABLES the wave
+// reads its segment's flag and copies the segment's tables from the
+// workspace; otherwise it reads the segment's scales, decides between the
+// grouped and the one-by-one sum, and builds the 256-entry tables of every
+// group of 8 workers itself (the 16-entry tables first, in the staging area,
+// before the words are staged).  The words are then staged and regrouped and
+// every group looked up, and the tile is finished.  Each wave owns its LDS
+// area, so it synchronises only with itself.
+// ---------------------------------------------------------------------------
+template <bool TABLES>
 __global__ __launch_bounds__(kBlock) void k_server_pass(
     const Tile *__restrict__ tiles, const int32_t *__restrict__ chunk_tiles, int64_t tile_begin,
     int64_t tile_count, int n,
     int grouping_limit, const uint64_t *__restrict__ wbits, int64_t bits_ld,
     int64_t bits_word_base, const float *__restrict__ wscales, int64_t scales_ld,
     int64_t scales_seg_base, float *__restrict__ serr, const float *__restrict__ sscales,
-    uint64_t *__restrict__ sbits, double *__restrict__ partial)
+    uint64_t *__restrict__ sbits, double *__restrict__ partial, ServerTables st)
 {
-    __shared__ __align__(16) ServerBatchLds s_lds[kWavesPerBlock];
+    __shared__ __align__(16) ServerRunLds s_lds[kWavesPerBlock];
     const int lane = threadIdx.x & (kWave - 1);
-    const int wv = threadIdx.x >> 6;
+    // wave-uniform: the tile and its fields live in scalar registers
+    const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int64_t rel = xcd_block() * kWavesPerBlock + wv;
     if (rel >= tile_count) return;
+    ServerRunLds &L = s_lds[wv];
+    const int groups8 = (n + 7) >> 3;
     const int64_t t = chunk_tiles[tile_begin + rel];
     const Tile tile = tiles[t];
     const int len = tile.len;
@@ -1144,9 +1304,6 @@ __global__ __launch_bounds__(kBlock) void k_server_pass(
     const ServerRows in{wbits + ((base >> 6) - bits_word_base), bits_ld,
                         wscales + ((int64_t)tile.seg - scales_seg_base), scales_ld,
                         (len + 63) >> 6, len == kTileElems};
-    ServerBatchLds &L = s_lds[wv];
-
-    // issue the error-state loads first; they are consumed at the end
     const float sprev = sscales[tile.seg];
     v4f cv[kSubBlocks];
 #pragma unroll
@@ -1155,40 +1312,50 @@ __global__ __launch_bounds__(kBlock) void k_server_pass(
         cv[b] = in.full ? ld4<true>(serr + base, li, len) : ld4<false>(serr + base, li, len);
     }
     uint64_t stg[kServerRowBatch / 4];
-    float scl = 0.f;
-    server_load_batch(in, 0, min(kServerRowBatch, n), lane, stg, scl);
-    const bool grouped = server_grouped(in, n, grouping_limit, lane, scl);
+    server_load_words(in, 0, n, lane, stg);
+    bool grouped;
+    if (TABLES) {
+        const int64_t u = owned_segment(tile.seg, n, st);
+        grouped = st.flags[u] != 0;
+        if (grouped) {
+            server_fetch_tables(&L.lut8[0][0], st, u, groups8, 0, groups8, lane);
+        } else if (lane < n) {
+            L.scale[lane] = in.scales[(int64_t)lane * in.scales_ld];
+        }
+    } else {
+        const float scl = lane < n ? in.scales[(int64_t)lane * in.scales_ld] : 0.f;
+        grouped = server_grouped(in, n, grouping_limit, lane, scl);
+        if (lane < n) L.scale[lane] = scl;
+        if (grouped) {
+            wave_sync();
+            server_build_lut4(L, n, lane);
+            wave_sync();
+#pragma unroll
+            for (int k = 0; k < (kServerRowBatch / 8) * 256 / kWave; ++k) {
+                const int e = lane + kWave * k;
+                const int g = e >> 8, idx = e & 255;  // g = k / 4: uniform
+                if (g < groups8)
+                    L.lut8[g][idx] = L.lut4[2 * g][idx & 15] + L.lut4[2 * g + 1][idx >> 4];
+            }
+            wave_sync();  // lut4 shares the staging area
+        }
+    }
+    server_stage_words(L, in, n, lane, stg);
+    if (TABLES) wait_vmem();
+    wave_sync();
     double sum[kSubBlocks][4];
 #pragma unroll
     for (int b = 0; b < kSubBlocks; ++b)
 #pragma unroll
         for (int c = 0; c < 4; ++c) sum[b][c] = 0.0;
-    for (int r0 = 0; r0 < n; r0 += kServerRowBatch) {
-        const int rows = min(kServerRowBatch, n - r0);
-        if (r0 > 0) server_load_batch(in, r0, rows, lane, stg, scl);
-        server_stage_batch(L, in, rows, lane, stg, scl);
+    if (grouped) {
+        server_regroup_bits(L, n, lane);
         wave_sync();
-        if (grouped)
-            server_batch_grouped(sum, L, rows, lane);
-        else
-            server_batch_one_by_one(sum, L, rows, lane);
-        wave_sync();
+        for (int g = 0; g < groups8; ++g) server_lookup_group(sum, L, 8 * g, L.lut8[g], lane);
+    } else {
+        server_batch_one_by_one(sum, L, n, lane);
     }
-    // FULL and POW2 are wave-uniform, so each wave runs one variant
-    const bool pow2 = (n & (n - 1)) == 0;
-    double acc = 0.0;
-#pragma unroll
-    for (int b = 0; b < kSubBlocks; ++b) {
-        if (in.full && pow2)
-            acc += server_epilogue_sub<true, true>(sum[b], cv[b], sprev, n, lane, tile, b, serr, sbits);
-        else if (in.full)
-            acc += server_epilogue_sub<true, false>(sum[b], cv[b], sprev, n, lane, tile, b, serr, sbits);
-        else if (pow2)
-            acc += server_epilogue_sub<false, true>(sum[b], cv[b], sprev, n, lane, tile, b, serr, sbits);
-        else
-            acc += server_epilogue_sub<false, false>(sum[b], cv[b], sprev, n, lane, tile, b, serr, sbits);
-    }
-    acc = wave_sum_dpp(acc);
+    const double acc = server_epilogue(sum, cv, sprev, n, lane, tile, in.full, serr, sbits);
     if (lane == 0) partial[t] = acc;
 }
 
@@ -1202,23 +1369,31 @@ __global__ __launch_bounds__(kBlock) void k_server_pass(
 // ---------------------------------------------------------------------------
 constexpr int kSplitWaves = kSubBlocks;
 
+// The per-wave LDS area of the split pass: with TABLES a batch's four tables
+// are copied in at once; otherwise they are built two at a time.
+template <bool TABLES> struct SplitBatchLds { using type = ServerBatchLds; };
+template <> struct SplitBatchLds<true> { using type = ServerRunLds; };
+
+template <bool TABLES>
 __global__ __launch_bounds__(kSplitWaves * kWave) void k_server_split(
     const Tile *__restrict__ tiles, const int32_t *__restrict__ chunk_tiles, int64_t tile_begin,
     int64_t tile_count, int n, int grouping_limit, const uint64_t *__restrict__ wbits,
     int64_t bits_ld, int64_t bits_word_base, const float *__restrict__ wscales,
     int64_t scales_ld, int64_t scales_seg_base, float *__restrict__ serr,
-    const float *__restrict__ sscales, uint64_t *__restrict__ sbits, double *__restrict__ partial)
+    const float *__restrict__ sscales, uint64_t *__restrict__ sbits, double *__restrict__ partial,
+    ServerTables st)
 {
+    using Lds = typename SplitBatchLds<TABLES>::type;
     // the staging areas while rows are summed, then the exchange of partial
     // sums: xch[sub-block][source wave][element of the sub-block]
     union SplitLds {
-        ServerBatchLds batch[kSplitWaves];
+        Lds batch[kSplitWaves];
         double xch[kSubBlocks][kSplitWaves][kWave * 4];
     };
     __shared__ __align__(16) SplitLds s_lds;
     __shared__ double s_red[kSplitWaves];
     const int lane = threadIdx.x & (kWave - 1);
-    const int wv = threadIdx.x >> 6;
+    const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int64_t rel = xcd_block();
     if (rel >= tile_count) return;  // the whole workgroup
     const int64_t t = chunk_tiles[tile_begin + rel];
@@ -1228,7 +1403,7 @@ __global__ __launch_bounds__(kSplitWaves * kWave) void k_server_split(
     const ServerRows in{wbits + ((base >> 6) - bits_word_base), bits_ld,
                         wscales + ((int64_t)tile.seg - scales_seg_base), scales_ld,
                         (len + 63) >> 6, len == kTileElems};
-    ServerBatchLds &L = s_lds.batch[wv];
+    Lds &L = s_lds.batch[wv];
 
     const float sprev = sscales[tile.seg];
     const int li = wv * (kWave * 4) + 4 * lane;  // this wave's sub-block
@@ -1237,8 +1412,12 @@ __global__ __launch_bounds__(kSplitWaves * kWave) void k_server_split(
     float scl = 0.f;
     const int rfirst = kServerRowBatch * wv;  // may be past n when n <= 96: no rows then
     server_load_batch(in, rfirst, max(0, min(kServerRowBatch, n - rfirst)), lane, stg, scl);
-    // every wave reads all n scales and reaches the same decision
-    const bool grouped = server_grouped(in, n, grouping_limit, lane, 0.f);
+    // every wave reaches the same decision (reading all n scales, or the
+    // segment's flag)
+    const int groups8 = (n + 7) >> 3;
+    const int64_t u = TABLES ? owned_segment(tile.seg, n, st) : 0;
+    const bool grouped =
+        TABLES ? st.flags[u] != 0 : server_grouped(in, n, grouping_limit, lane, 0.f);
     double sum[kSubBlocks][4];
 #pragma unroll
     for (int b = 0; b < kSubBlocks; ++b)
@@ -1248,13 +1427,28 @@ __global__ __launch_bounds__(kSplitWaves * kWave) void k_server_split(
         constexpr int kStep = kServerRowBatch * kSplitWaves;
         for (int r0 = rfirst; r0 < n; r0 += kStep) {
             const int rows = min(kServerRowBatch, n - r0);
-            server_stage_batch(L, in, rows, lane, stg, scl);
-            // the next batch's words travel while this one is summed
-            if (r0 + kStep < n)
-                server_load_batch(in, r0 + kStep, min(kServerRowBatch, n - r0 - kStep), lane, stg,
-                                  scl);
-            wave_sync();
-            server_batch_grouped(sum, L, rows, lane);
+            if constexpr (TABLES) {
+                const int g0 = r0 >> 3, gcnt = (rows + 7) >> 3;
+                server_fetch_tables(&L.lut8[0][0], st, u, groups8, g0, gcnt, lane);
+                server_stage_words(L, in, rows, lane, stg);
+                wait_vmem();  // the tables, before the next batch's words are asked for
+                if (r0 + kStep < n)
+                    server_load_words(in, r0 + kStep, min(kServerRowBatch, n - r0 - kStep), lane,
+                                      stg);
+                wave_sync();
+                server_regroup_bits(L, rows, lane);
+                wave_sync();
+                for (int g = 0; g < gcnt; ++g)
+                    server_lookup_group(sum, L, 8 * g, L.lut8[g], lane);
+            } else {
+                server_stage_batch(L, in, rows, lane, stg, scl);
+                // the next batch's words travel while this one is summed
+                if (r0 + kStep < n)
+                    server_load_batch(in, r0 + kStep, min(kServerRowBatch, n - r0 - kStep), lane,
+                                      stg, scl);
+                wave_sync();
+                server_batch_grouped(sum, L, rows, lane);
+            }
             wave_sync();
         }
     } else if (wv == 0) {
@@ -1670,26 +1864,54 @@ hipError_t launch_finalize(const DeviceTables &tb, int64_t max_seg_tiles, int64_
     return hipGetLastError();
 }
 
+size_t server_table_bytes(int n, int64_t segments)
+{
+    return (size_t)segments * (size_t)((n + 7) / 8) * 256 * sizeof(double);
+}
+
 hipError_t launch_server_pass(const DeviceTables &tb, int64_t tile_begin, int64_t tile_count,
                               int n, const uint64_t *wbits, int64_t bits_ld,
                               int64_t bits_word_base, const float *wscales, int64_t scales_ld,
                               int64_t scales_seg_base, float *serr, float *sscales,
-                              uint64_t *sbits, double *partial, hipStream_t s)
+                              uint64_t *sbits, double *partial, int num_tensors, int cb,
+                              int nown, double *tables, int32_t *flags, hipStream_t s)
 {
     int log2n = 0;
     while ((1 << log2n) < n) ++log2n;
     const int grouping_limit = 29 - log2n;
+    const ServerTables st{tables, flags, cb, nown};
+    const bool use_tables = tables != nullptr;
+    if (use_tables)
+        hipLaunchKernelGGL(k_server_tables,
+                           dim3((unsigned)((int64_t)num_tensors * nown * ((n + 7) / 8))),
+                           dim3(kBlock), 0, s, n, cb, nown, grouping_limit, wscales, scales_ld,
+                           scales_seg_base, tables, flags);
     // more than one batch of rows: the waves of a workgroup share each tile
-    if (n > kServerRowBatch)
-        hipLaunchKernelGGL(k_server_split, dim3((unsigned)xcd_grid(tile_count, 1)),
-                           dim3(kSplitWaves * kWave), 0, s, tb.tiles, tb.chunk_tiles, tile_begin,
-                           tile_count, n, grouping_limit, wbits, bits_ld, bits_word_base, wscales,
-                           scales_ld, scales_seg_base, serr, sscales, sbits, partial);
-    else
-        hipLaunchKernelGGL(k_server_pass, dim3((unsigned)blocks_for(tile_count)), dim3(kBlock), 0,
-                           s, tb.tiles, tb.chunk_tiles, tile_begin, tile_count, n, grouping_limit,
-                           wbits, bits_ld, bits_word_base, wscales, scales_ld, scales_seg_base,
-                           serr, sscales, sbits, partial);
+    if (n > kServerRowBatch) {
+        const dim3 grid((unsigned)xcd_grid(tile_count, 1)), block(kSplitWaves * kWave);
+        if (use_tables)
+            hipLaunchKernelGGL(k_server_split<true>, grid, block, 0, s, tb.tiles, tb.chunk_tiles,
+                               tile_begin, tile_count, n, grouping_limit, wbits, bits_ld,
+                               bits_word_base, wscales, scales_ld, scales_seg_base, serr, sscales,
+                               sbits, partial, st);
+        else
+            hipLaunchKernelGGL(k_server_split<false>, grid, block, 0, s, tb.tiles,
+                               tb.chunk_tiles, tile_begin, tile_count, n, grouping_limit, wbits,
+                               bits_ld, bits_word_base, wscales, scales_ld, scales_seg_base, serr,
+                               sscales, sbits, partial, st);
+    } else {
+        const dim3 grid((unsigned)blocks_for(tile_count)), block(kBlock);
+        if (use_tables)
+            hipLaunchKernelGGL(k_server_pass<true>, grid, block, 0, s, tb.tiles, tb.chunk_tiles,
+                               tile_begin, tile_count, n, grouping_limit, wbits, bits_ld,
+                               bits_word_base, wscales, scales_ld, scales_seg_base, serr, sscales,
+                               sbits, partial, st);
+        else
+            hipLaunchKernelGGL(k_server_pass<false>, grid, block, 0, s, tb.tiles, tb.chunk_tiles,
+                               tile_begin, tile_count, n, grouping_limit, wbits, bits_ld,
+                               bits_word_base, wscales, scales_ld, scales_seg_base, serr, sscales,
+                               sbits, partial, st);
+    }
     return hipGetLastError();
 }
 
