@@ -121,6 +121,16 @@ int onebit_plan_get_info(onebit_plan plan, onebit_plan_sizes *info);
 int onebit_plan_get_layout(onebit_plan plan, int64_t *tensor_offset,
                            int64_t *seg_begin, int64_t *seg_end);
 
+/* Whether the chunk owners' calls on this plan may keep their lookup tables
+ * (the signed sums of the scales of each group of 8 workers, Algorithm 1's
+ * server average) in the workspace, built once per call, instead of building
+ * them for every tile (enable != 0, the default; used when the plan reserved
+ * the space, see workspace_bytes, and the call's segments average 4 or more
+ * tiles).  Results are bit-identical either way; the switch exists to compare
+ * the two paths.  Not to be changed while a call on the plan is in flight.
+ * Errors: EINVAL (null plan). */
+int onebit_plan_set_server_tables(onebit_plan plan, int32_t enable);
+
 /* The sizes a caller allocates by, as separate host outputs (any may be
  * NULL): D, W, S, the chunk length c_k of every tensor (chunk_len[K], see
  * Layout above) and the workspace size in bytes for the calls below. */

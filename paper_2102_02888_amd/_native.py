@@ -28,6 +28,7 @@ SIGNATURES = {
     "onebit_plan_create": [_vp, _i32, _i32, _vp],
     "onebit_plan_destroy": [_vp],
     "onebit_plan_get_info": [_vp, _vp],
+    "onebit_plan_set_server_tables": [_vp, _i32],
     "onebit_plan_get_layout": [_vp, _vp, _vp, _vp],
     "onebit_plan_info": [_vp, _vp, _vp, _vp, _vp, _vp],
     "onebit_warmup_adam_step": [_vp, _vp, _vp, _vp, _vp, _i32, _i64, _i32, _f32, _f32, _f32,

@@ -32,9 +32,11 @@ struct onebit_plan_s {
     std::vector<int64_t> seg_tile_begin, seg_tile_end;  // [S]
     std::vector<int64_t> chunk_tile_begin;              // [n+1], into chunk_tiles
     std::vector<int64_t> chunk_word_lo, chunk_word_hi;  // [n], words touched by chunk j
+    std::vector<int64_t> chunk_block_begin;  // [n+1], into the shared-table workgroups
     void *dev_mem = nullptr;                            // one allocation for all tables
     DeviceTables tb{};
     size_t table_bytes = 0;  // chunk owners' lookup tables in the workspace (0: none)
+    bool server_tables = true;  // calls may use them (onebit_plan_set_server_tables)
     size_t workspace_bytes = 0;
 };
 
@@ -232,10 +234,19 @@ int plan_create_impl(const int64_t *tensor_numel, int32_t num_tensors, int32_t n
     }
     std::vector<int32_t> chunk_tiles;
     chunk_tiles.reserve(tiles.size());
+    // the chunk owners' shared-table workgroups: up to kWavesPerBlock
+    // consecutive tiles of one segment each, in the same chunk-major order
+    std::vector<int32_t> server_blocks;
+    p->chunk_block_begin.assign(n + 1, 0);
     for (int32_t j = 0; j < n; ++j) {
         p->chunk_tile_begin[j] = (int64_t)chunk_tiles.size();
+        p->chunk_block_begin[j] = (int64_t)server_blocks.size();
         for (int32_t k = 0; k < K; ++k) {
             const int64_t q = (int64_t)k * n + j;
+            const int64_t pos = (int64_t)chunk_tiles.size();
+            const int64_t cnt = p->seg_tile_end[q] - p->seg_tile_begin[q];
+            for (int64_t i = 0; i < onebit::server_blocks_of(cnt); ++i)
+                server_blocks.push_back(onebit::server_block_entry(pos, cnt, i));
             for (int64_t t = p->seg_tile_begin[q]; t < p->seg_tile_end[q]; ++t)
                 chunk_tiles.push_back((int32_t)t);
             const int64_t b = p->seg_begin[q], en = p->seg_end[q];
@@ -246,18 +257,23 @@ int plan_create_impl(const int64_t *tensor_numel, int32_t num_tensors, int32_t n
         }
     }
     p->chunk_tile_begin[n] = (int64_t)chunk_tiles.size();
+    p->chunk_block_begin[n] = (int64_t)server_blocks.size();
     p->T = (int64_t)tiles.size();
 
     const size_t tiles_bytes = round_up(tiles.size() * sizeof(Tile) + 1, 256);
     const size_t order_bytes = round_up(chunk_tiles.size() * sizeof(int32_t) + 1, 256);
     const size_t seg_bytes = round_up((size_t)p->S * sizeof(int64_t), 256);
-    const size_t total = tiles_bytes + order_bytes + 3 * seg_bytes;
+    const size_t block_bytes = round_up(server_blocks.size() * sizeof(int32_t) + 1, 256);
     const size_t seg0 = tiles_bytes + order_bytes;
+    const size_t blocks0 = seg0 + 3 * seg_bytes;
+    const size_t total = blocks0 + block_bytes;
     std::vector<char> host(total, 0);
     if (!tiles.empty()) {
         std::memcpy(host.data(), tiles.data(), tiles.size() * sizeof(Tile));
         std::memcpy(host.data() + tiles_bytes, chunk_tiles.data(),
                     chunk_tiles.size() * sizeof(int32_t));
+        std::memcpy(host.data() + blocks0, server_blocks.data(),
+                    server_blocks.size() * sizeof(int32_t));
     }
     std::memcpy(host.data() + seg0, p->seg_tile_begin.data(), p->S * sizeof(int64_t));
     std::memcpy(host.data() + seg0 + seg_bytes, p->seg_tile_end.data(), p->S * sizeof(int64_t));
@@ -283,6 +299,7 @@ int plan_create_impl(const int64_t *tensor_numel, int32_t num_tensors, int32_t n
     p->tb.seg_tile_begin = d_stb;
     p->tb.seg_tile_end = d_ste;
     p->tb.seg_len = d_sl;
+    p->tb.server_blocks = (const int32_t *)(base + blocks0);
     const size_t seg_tables = onebit::server_table_bytes(p->n, 1);
     p->table_bytes = (size_t)p->S <= kServerTableBudget / seg_tables
                          ? onebit::server_table_bytes(p->n, p->S)
@@ -397,15 +414,18 @@ int run_server(const onebit_plan_s *p, int32_t server_begin, int32_t server_end,
     double *part = (double *)((char *)workspace + server_partial_offset(p));
     const int nown = server_end - server_begin;
     const int64_t owned = (int64_t)p->K * nown;
-    const bool use_tables = p->table_bytes > 0 && tc >= kServerTableMinTiles * owned;
+    const bool use_tables =
+        p->server_tables && p->table_bytes > 0 && tc >= kServerTableMinTiles * owned;
     double *tables = use_tables ? (double *)((char *)workspace + server_table_offset(p)) : nullptr;
     int32_t *flags = use_tables ? (int32_t *)((char *)workspace + server_flag_offset(p)) : nullptr;
+    const int64_t bb = p->chunk_block_begin[server_begin];
+    const int64_t nb = p->chunk_block_begin[server_end] - bb;
     if (tc > 0)
         TRY_HIP(onebit::launch_server_pass(p->tb, tb, tc, p->n, worker_bits, bits_ld,
                                            bits_word_base, worker_scales, scales_ld,
                                            scales_seg_base, server_err, server_scales,
                                            server_bits, part, p->K, server_begin, nown, tables,
-                                           flags, s),
+                                           flags, p->tb.server_blocks + bb, nb, s),
                 "server kernel launch");
     TRY_HIP(onebit::launch_finalize(p->tb, p->max_seg_tiles,
                                     (int64_t)p->K * (server_end - server_begin), p->S, 1, p->n,
@@ -549,6 +569,13 @@ int onebit_plan_get_layout(onebit_plan p, int64_t *tensor_offset, int64_t *seg_b
     if (tensor_offset) std::memcpy(tensor_offset, p->tensor_off.data(), p->K * sizeof(int64_t));
     if (seg_begin) std::memcpy(seg_begin, p->seg_begin.data(), p->S * sizeof(int64_t));
     if (seg_end) std::memcpy(seg_end, p->seg_end.data(), p->S * sizeof(int64_t));
+    return ONEBIT_OK;
+}
+
+int onebit_plan_set_server_tables(onebit_plan p, int32_t enable)
+{
+    if (!p) return fail(ONEBIT_EINVAL, "plan is NULL");
+    p->server_tables = enable != 0;
     return ONEBIT_OK;
 }
 

@@ -56,6 +56,28 @@ ONEBIT_HD inline int64_t xcd_block_of(int64_t b, int64_t grid)
     return (b % kXcds) * (grid / kXcds) + b / kXcds;
 }
 
+// Chunk owners' workgroups that share one segment's lookup tables: each takes
+// up to kWavesPerBlock consecutive tiles of one segment in the chunk-major
+// tile list, one per wave.  A segment whose tiles sit at list positions
+// [pos, pos + count) gets server_blocks_of(count) workgroups; entry i is
+// server_block_entry(pos, count, i), from which the kernel reads the first
+// position and the number of tiles.  Positions stay below 2^25 (the plans'
+// tile limit), so an entry fits an int32.
+ONEBIT_HD inline int64_t server_blocks_of(int64_t count)
+{
+    return (count + kWavesPerBlock - 1) / kWavesPerBlock;
+}
+
+ONEBIT_HD inline int32_t server_block_entry(int64_t pos, int64_t count, int64_t i)
+{
+    const int64_t first = pos + i * kWavesPerBlock;
+    const int64_t left = pos + count - first;
+    return (int32_t)(first * 8 + (left < kWavesPerBlock ? left : kWavesPerBlock));
+}
+
+ONEBIT_HD inline int64_t server_block_first(int32_t entry) { return entry >> 3; }
+ONEBIT_HD inline int server_block_tiles(int32_t entry) { return entry & 7; }
+
 // Worker pass: items [0, num_items) are cut into kXcds contiguous ranges and
 // XCD x walks range x with its grid / kXcds blocks; a grid smaller than the
 // item count strides within the range.  Wave w of physical block b takes

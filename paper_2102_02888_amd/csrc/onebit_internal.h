@@ -30,6 +30,8 @@ struct DeviceTables {
     const int64_t *seg_tile_begin; // [S]
     const int64_t *seg_tile_end;   // [S]
     const int64_t *seg_len;        // [S]
+    const int32_t *server_blocks;  // chunk owners' shared-table workgroups, chunk-major
+                                   // (entries of onebit_grid.h's server_block_entry)
 };
 
 // Gradient element types (the values of the ONEBIT_GRAD_* constants).
@@ -85,14 +87,17 @@ size_t server_table_bytes(int n, int64_t segments);
 // the chunk-major tile list, for chunks [cb, cb + nown) of num_tensors
 // tensors.  tables != NULL (at least server_table_bytes(n, num_tensors *
 // nown) bytes, 256-byte aligned) and flags (num_tensors * nown int32): the
-// owned segments' tables are built there first and copied by the pass;
-// tables == NULL: the pass builds them per tile.
+// owned segments' tables are built there first and copied by the pass, which
+// for n <= 32 runs the num_blocks shared-table workgroups of server_blocks
+// (the call's range of DeviceTables::server_blocks); tables == NULL: the
+// pass builds them per tile.
 hipError_t launch_server_pass(const DeviceTables &tb, int64_t tile_begin, int64_t tile_count,
                               int n, const uint64_t *wbits, int64_t bits_ld,
                               int64_t bits_word_base, const float *wscales, int64_t scales_ld,
                               int64_t scales_seg_base, float *serr, float *sscales,
                               uint64_t *sbits, double *partial, int num_tensors, int cb,
-                              int nown, double *tables, int32_t *flags, hipStream_t s);
+                              int nown, double *tables, int32_t *flags,
+                              const int32_t *server_blocks, int64_t num_blocks, hipStream_t s);
 
 hipError_t launch_update(const DeviceTables &tb, int64_t num_tiles, const uint64_t *sbits,
                          const float *sscales, float *x, float *m_out, const float *v,

@@ -1270,24 +1270,22 @@ __device__ __forceinline__ int64_t owned_segment(int64_t q, int n, const ServerT
 __device__ __forceinline__ void wait_vmem() { __builtin_amdgcn_s_waitcnt(0x0F70); }
 
 // ---------------------------------------------------------------------------
-// Chunk owners' pass for n <= kServerRowBatch, one wave per tile.  The tile's
-// error-state and sign-word loads are issued first.  With TABLES the wave
-// reads its segment's flag and copies the segment's tables from the
-// workspace; otherwise it reads the segment's scales, decides between the
+// Chunk owners' pass for n <= kServerRowBatch, one wave per tile, building
+// the tables itself.  The tile's error-state and sign-word loads are issued
+// first; the wave then reads the segment's scales, decides between the
 // grouped and the one-by-one sum, and builds the 256-entry tables of every
-// group of 8 workers itself (the 16-entry tables first, in the staging area,
-// before the words are staged).  The words are then staged and regrouped and
-// every group looked up, and the tile is finished.  Each wave owns its LDS
-// area, so it synchronises only with itself.
+// group of 8 workers (the 16-entry tables first, in the staging area, before
+// the words are staged).  The words are then staged and regrouped, every
+// group is looked up, and the tile is finished.  Each wave owns its LDS area,
+// so it synchronises only with itself.
 // ---------------------------------------------------------------------------
-template <bool TABLES>
 __global__ __launch_bounds__(kBlock) void k_server_pass(
     const Tile *__restrict__ tiles, const int32_t *__restrict__ chunk_tiles, int64_t tile_begin,
     int64_t tile_count, int n,
     int grouping_limit, const uint64_t *__restrict__ wbits, int64_t bits_ld,
     int64_t bits_word_base, const float *__restrict__ wscales, int64_t scales_ld,
     int64_t scales_seg_base, float *__restrict__ serr, const float *__restrict__ sscales,
-    uint64_t *__restrict__ sbits, double *__restrict__ partial, ServerTables st)
+    uint64_t *__restrict__ sbits, double *__restrict__ partial)
 {
     __shared__ __align__(16) ServerRunLds s_lds[kWavesPerBlock];
     const int lane = threadIdx.x & (kWave - 1);
@@ -1313,35 +1311,23 @@ __global__ __launch_bounds__(kBlock) void k_server_pass(
     }
     uint64_t stg[kServerRowBatch / 4];
     server_load_words(in, 0, n, lane, stg);
-    bool grouped;
-    if (TABLES) {
-        const int64_t u = owned_segment(tile.seg, n, st);
-        grouped = st.flags[u] != 0;
-        if (grouped) {
-            server_fetch_tables(&L.lut8[0][0], st, u, groups8, 0, groups8, lane);
-        } else if (lane < n) {
-            L.scale[lane] = in.scales[(int64_t)lane * in.scales_ld];
-        }
-    } else {
-        const float scl = lane < n ? in.scales[(int64_t)lane * in.scales_ld] : 0.f;
-        grouped = server_grouped(in, n, grouping_limit, lane, scl);
-        if (lane < n) L.scale[lane] = scl;
-        if (grouped) {
-            wave_sync();
-            server_build_lut4(L, n, lane);
-            wave_sync();
+    const float scl = lane < n ? in.scales[(int64_t)lane * in.scales_ld] : 0.f;
+    const bool grouped = server_grouped(in, n, grouping_limit, lane, scl);
+    if (lane < n) L.scale[lane] = scl;
+    if (grouped) {
+        wave_sync();
+        server_build_lut4(L, n, lane);
+        wave_sync();
 #pragma unroll
-            for (int k = 0; k < (kServerRowBatch / 8) * 256 / kWave; ++k) {
-                const int e = lane + kWave * k;
-                const int g = e >> 8, idx = e & 255;  // g = k / 4: uniform
-                if (g < groups8)
-                    L.lut8[g][idx] = L.lut4[2 * g][idx & 15] + L.lut4[2 * g + 1][idx >> 4];
-            }
-            wave_sync();  // lut4 shares the staging area
+        for (int k = 0; k < (kServerRowBatch / 8) * 256 / kWave; ++k) {
+            const int e = lane + kWave * k;
+            const int g = e >> 8, idx = e & 255;  // g = k / 4: uniform
+            if (g < groups8)
+                L.lut8[g][idx] = L.lut4[2 * g][idx & 15] + L.lut4[2 * g + 1][idx >> 4];
         }
+        wave_sync();  // lut4 shares the staging area
     }
     server_stage_words(L, in, n, lane, stg);
-    if (TABLES) wait_vmem();
     wave_sync();
     double sum[kSubBlocks][4];
 #pragma unroll
@@ -1352,6 +1338,93 @@ __global__ __launch_bounds__(kBlock) void k_server_pass(
         server_regroup_bits(L, n, lane);
         wave_sync();
         for (int g = 0; g < groups8; ++g) server_lookup_group(sum, L, 8 * g, L.lut8[g], lane);
+    } else {
+        server_batch_one_by_one(sum, L, n, lane);
+    }
+    const double acc = server_epilogue(sum, cv, sprev, n, lane, tile, in.full, serr, sbits);
+    if (lane == 0) partial[t] = acc;
+}
+
+// ---------------------------------------------------------------------------
+// Chunk owners' pass for n <= kServerRowBatch with the tables in the
+// workspace: each workgroup takes up to kWavesPerBlock consecutive tiles of
+// one segment (entry b of `blocks`, one tile per wave) and shares one copy of
+// the segment's tables, wave g copying group g's.  The tile loads are issued
+// first; after one workgroup barrier (tables and staged words in place) each
+// wave regroups its own words, looks every group up and finishes its tile.
+// One shared table set instead of one per wave leaves room in LDS for four
+// workgroups per CU.
+// ---------------------------------------------------------------------------
+struct ServerSharedLds {
+    uint32_t bits[kWavesPerBlock][2 * kTileWords][kBitsStride];
+    double lut8[kServerRowBatch / 8][256];
+    float scale[kServerRowBatch];
+};
+
+// One wave's part of it, in the form the staging and summing helpers take.
+struct ServerWaveLds {
+    uint32_t (&bits)[2 * kTileWords][kBitsStride];
+    float (&scale)[kServerRowBatch];
+};
+
+__global__ __launch_bounds__(kBlock) void k_server_shared(
+    const Tile *__restrict__ tiles, const int32_t *__restrict__ chunk_tiles,
+    const int32_t *__restrict__ blocks, int64_t num_blocks, int n,
+    const uint64_t *__restrict__ wbits, int64_t bits_ld, int64_t bits_word_base,
+    const float *__restrict__ wscales, int64_t scales_ld, int64_t scales_seg_base,
+    float *__restrict__ serr, const float *__restrict__ sscales, uint64_t *__restrict__ sbits,
+    double *__restrict__ partial, ServerTables st)
+{
+    __shared__ __align__(16) ServerSharedLds S;
+    const int lane = threadIdx.x & (kWave - 1);
+    const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int64_t b = xcd_block();
+    if (b >= num_blocks) return;  // the whole workgroup
+    const int32_t entry = blocks[b];
+    const int64_t first = server_block_first(entry);
+    const bool has = wv < server_block_tiles(entry);
+    const int groups8 = (n + 7) >> 3;
+    // every tile of the workgroup is in this segment
+    const int seg = tiles[chunk_tiles[first]].seg;
+    const int64_t u = owned_segment(seg, n, st);
+    const bool grouped = st.flags[u] != 0;
+    const int64_t t = chunk_tiles[first + (has ? wv : 0)];
+    const Tile tile = tiles[t];
+    const int len = tile.len;
+    const int64_t base = tile.start;
+    const ServerRows in{wbits + ((base >> 6) - bits_word_base), bits_ld,
+                        wscales + ((int64_t)seg - scales_seg_base), scales_ld,
+                        (len + 63) >> 6, len == kTileElems};
+    const float sprev = sscales[seg];
+    v4f cv[kSubBlocks];
+    uint64_t stg[kServerRowBatch / 4];
+    if (has) {
+#pragma unroll
+        for (int k = 0; k < kSubBlocks; ++k) {
+            const int li = k * (kWave * 4) + 4 * lane;
+            cv[k] = in.full ? ld4<true>(serr + base, li, len) : ld4<false>(serr + base, li, len);
+        }
+        server_load_words(in, 0, n, lane, stg);
+    }
+    if (grouped) {
+        if (wv < groups8) server_fetch_tables(&S.lut8[wv][0], st, u, groups8, wv, 1, lane);
+    } else if (wv == 0 && lane < n) {
+        S.scale[lane] = in.scales[(int64_t)lane * in.scales_ld];
+    }
+    ServerWaveLds L{S.bits[wv], S.scale};
+    if (has) server_stage_words(L, in, n, lane, stg);
+    wait_vmem();
+    __syncthreads();
+    if (!has) return;
+    double sum[kSubBlocks][4];
+#pragma unroll
+    for (int k = 0; k < kSubBlocks; ++k)
+#pragma unroll
+        for (int c = 0; c < 4; ++c) sum[k][c] = 0.0;
+    if (grouped) {
+        server_regroup_bits(L, n, lane);
+        wave_sync();
+        for (int g = 0; g < groups8; ++g) server_lookup_group(sum, L, 8 * g, S.lut8[g], lane);
     } else {
         server_batch_one_by_one(sum, L, n, lane);
     }
@@ -1874,7 +1947,8 @@ hipError_t launch_server_pass(const DeviceTables &tb, int64_t tile_begin, int64_
                               int64_t bits_word_base, const float *wscales, int64_t scales_ld,
                               int64_t scales_seg_base, float *serr, float *sscales,
                               uint64_t *sbits, double *partial, int num_tensors, int cb,
-                              int nown, double *tables, int32_t *flags, hipStream_t s)
+                              int nown, double *tables, int32_t *flags,
+                              const int32_t *server_blocks, int64_t num_blocks, hipStream_t s)
 {
     int log2n = 0;
     while ((1 << log2n) < n) ++log2n;
@@ -1899,18 +1973,16 @@ hipError_t launch_server_pass(const DeviceTables &tb, int64_t tile_begin, int64_
                                tb.chunk_tiles, tile_begin, tile_count, n, grouping_limit, wbits,
                                bits_ld, bits_word_base, wscales, scales_ld, scales_seg_base, serr,
                                sscales, sbits, partial, st);
+    } else if (use_tables) {
+        hipLaunchKernelGGL(k_server_shared, dim3((unsigned)xcd_grid(num_blocks, 1)), dim3(kBlock),
+                           0, s, tb.tiles, tb.chunk_tiles, server_blocks, num_blocks, n, wbits,
+                           bits_ld, bits_word_base, wscales, scales_ld, scales_seg_base, serr,
+                           sscales, sbits, partial, st);
     } else {
-        const dim3 grid((unsigned)blocks_for(tile_count)), block(kBlock);
-        if (use_tables)
-            hipLaunchKernelGGL(k_server_pass<true>, grid, block, 0, s, tb.tiles, tb.chunk_tiles,
-                               tile_begin, tile_count, n, grouping_limit, wbits, bits_ld,
-                               bits_word_base, wscales, scales_ld, scales_seg_base, serr, sscales,
-                               sbits, partial, st);
-        else
-            hipLaunchKernelGGL(k_server_pass<false>, grid, block, 0, s, tb.tiles, tb.chunk_tiles,
-                               tile_begin, tile_count, n, grouping_limit, wbits, bits_ld,
-                               bits_word_base, wscales, scales_ld, scales_seg_base, serr, sscales,
-                               sbits, partial, st);
+        hipLaunchKernelGGL(k_server_pass, dim3((unsigned)blocks_for(tile_count)), dim3(kBlock), 0,
+                           s, tb.tiles, tb.chunk_tiles, tile_begin, tile_count, n, grouping_limit,
+                           wbits, bits_ld, bits_word_base, wscales, scales_ld, scales_seg_base,
+                           serr, sscales, sbits, partial);
     }
     return hipGetLastError();
 }

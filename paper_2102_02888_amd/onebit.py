@@ -156,6 +156,11 @@ class Plan:
             raise ValueError("plan is closed")
         return self._h
 
+    def set_server_tables(self, enable):
+        """Whether the chunk owners' calls may keep their lookup tables in the
+        workspace (the default) or build them per tile; results are identical."""
+        call("onebit_plan_set_server_tables", self.handle, 1 if enable else 0)
+
     def workspace(self, device):
         nbytes = max(self.workspace_bytes, 256)
         return torch.empty(nbytes // 8 + 32, dtype=torch.float64, device=device)

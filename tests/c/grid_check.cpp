@@ -40,6 +40,43 @@ static void check_tiles(int64_t tiles, int waves_per_block)
         if (!seen[(size_t)t]) fail("tile not taken", t, tiles);
 }
 
+// The chunk owners' shared-table workgroups of a list of segments with the
+// given tile counts, laid out one after another from list position base:
+// every tile is taken once, by a workgroup of that segment, as wave
+// (position - first).
+static void check_server_blocks(const std::vector<int64_t> &counts, int64_t base = 0)
+{
+    ++cases;
+    int64_t total = 0;
+    for (int64_t c : counts) total += c;
+    std::vector<int> owner((size_t)total, -1);
+    std::vector<int> seen((size_t)total, 0);
+    int64_t pos = 0;
+    for (size_t q = 0; q < counts.size(); ++q) {
+        for (int64_t t = pos; t < pos + counts[q]; ++t) owner[(size_t)t] = (int)q;
+        pos += counts[q];
+    }
+    pos = 0;
+    for (size_t q = 0; q < counts.size(); ++q) {
+        const int64_t nb = server_blocks_of(counts[q]);
+        for (int64_t i = 0; i < nb; ++i) {
+            const int32_t e = server_block_entry(base + pos, counts[q], i);
+            const int64_t first = server_block_first(e) - base;
+            const int tiles = server_block_tiles(e);
+            if (tiles < 1 || tiles > kWavesPerBlock) fail("workgroup tile count", tiles, (long long)q);
+            for (int w = 0; w < tiles; ++w) {
+                const int64_t t = first + w;
+                if (t < 0 || t >= total) { fail("workgroup tile out of range", t, total); break; }
+                if (owner[(size_t)t] != (int)q) fail("workgroup crosses a segment", t, (long long)q);
+                ++seen[(size_t)t];
+            }
+        }
+        pos += counts[q];
+    }
+    for (int64_t t = 0; t < total; ++t)
+        if (seen[(size_t)t] != 1) { fail("tile taken other than once", t, seen[(size_t)t]); break; }
+}
+
 // The worker pass: items walked per XCD with a grid capped at max_blocks.
 static void check_worker(int64_t items, int64_t max_blocks)
 {
@@ -69,6 +106,16 @@ int main()
         for (int64_t t = 1; t <= 600; ++t) check_tiles(t, wpb);
         // BERT-Large (326,288 tiles) and the stress workload's tile counts
         for (int64_t t : {326288LL, 542089LL, 106344LL, 1275LL}) check_tiles(t, wpb);
+    }
+
+    // segments of 0..40 tiles, BERT-Large's 32 segments of about 10,200 tiles
+    // and entries near the 2^25-tile limit
+    {
+        std::vector<int64_t> counts;
+        for (int64_t c = 0; c <= 40; ++c) counts.push_back(c);
+        check_server_blocks(counts);
+        check_server_blocks(std::vector<int64_t>(32, 10196));
+        check_server_blocks({9, 5, 1, 2}, (1LL << 25) - 17);
     }
 
     for (int64_t items = 1; items <= 700; ++items)

@@ -146,7 +146,12 @@ def test_worker_compress_packed_momentum_parity(ob, dev, numel, n):
 
 SERVER_CASES = [c + ("lognormal",) for c in CASES] + [
     ([1 << 20], 4, "wide"), ([5000, 300, 64], 5, "wide"), ([70_000], 37, "lognormal"),
-    ([70_000], 37, "zeros"), ([100_000], 256, "lognormal"), ([100_000], 256, "wide")]
+    ([70_000], 37, "zeros"), ([100_000], 256, "lognormal"), ([100_000], 256, "wide"),
+    # segments of 4 or more tiles: the chunk owners' tables are built once per
+    # call in the workspace (n = 32: four groups of 8; n = 37 and 100: the
+    # split pass, whose last group has 5 and 4 rows)
+    ([1 << 20], 32, "lognormal"), ([1 << 20], 4, "zeros"), ([300_000], 37, "lognormal"),
+    ([300_000], 37, "wide"), ([300_000], 37, "zeros"), ([700_000], 100, "lognormal")]
 
 
 @pytest.mark.parametrize("numel,n,scales", SERVER_CASES)
@@ -455,6 +460,41 @@ def test_server_received_chunk_form(ob, dev):
     sb = res[0][1]
     assert not sb[:w0].any() and not sb[w1:].any()
     assert np.count_nonzero(res[0][2]) == 1
+    plan.close()
+
+
+@pytest.mark.parametrize("numel,n,scales", [
+    ([1 << 20], 4, "lognormal"), ([1 << 20], 32, "lognormal"), ([1 << 20], 32, "wide"),
+    ([300_000], 37, "zeros"), ([700_000], 100, "lognormal"), ([600_000, 3000, 70], 8, "zeros")])
+def test_server_tables_and_per_tile_paths_agree(ob, dev, numel, n, scales):
+    """The chunk owners' lookup tables built once per call in the workspace
+    and the tables built per tile give the same words, scales and error
+    state, bit for bit (both sums are exact, or both one by one)."""
+    L = oracle.Layout(numel, n)
+    plan = ob.Plan(numel, n)
+    rng = np.random.default_rng(40 + n)
+    wbits = rng.integers(0, np.iinfo(np.uint64).max, size=(n, L.W), dtype=np.uint64,
+                         endpoint=True)
+    wscales = np.exp(rng.normal(-7, 0.5, size=(n, L.S))).astype(np.float32)
+    if scales == "wide":
+        wscales *= np.float32(2.0) ** rng.integers(-40, 40, size=(n, L.S)).astype(np.float32)
+    elif scales == "zeros":
+        wscales[rng.random((n, L.S)) < 0.3] = 0
+    serr0 = rng.normal(0, 1e-3, size=L.D).astype(np.float32)
+    sscales0 = np.exp(rng.normal(-8, 0.5, size=L.S)).astype(np.float32)
+    wb, ws_ = _put(wbits, dev), _put(wscales, dev)
+    res = []
+    for tables in (True, False):
+        plan.set_server_tables(tables)
+        serr = _put(serr0, dev)
+        sscales = _put(sscales0, dev)
+        sbits = torch.zeros(L.W, dtype=torch.int64, device=dev)
+        ws = plan.workspace(dev)
+        ob.onebit_server_reduce_compress(plan, 0, n, wb, ws_, serr, sbits, sscales, ws)
+        torch.cuda.synchronize()
+        res.append((host(serr), host(sbits), host(sscales)))
+    for name, a, c in zip(("server_err", "server_bits", "server_scales"), res[0], res[1]):
+        assert a.tobytes() == c.tobytes(), name
     plan.close()
 
 
