@@ -507,7 +507,10 @@ def main():
                     for name, ms, nbytes, kname in (
                         ("worker_compress", part_ms[0], worker_bytes,
                          "k_worker_pass<true, %s>" % gname),
-                        ("server_reduce_compress", part_ms[1], d * bs, "k_server_pass"),
+                        # the BERT-shaped plans keep the chunk owners' tables in
+                        # the workspace: the shared-table pass for n <= 32
+                        ("server_reduce_compress", part_ms[1], d * bs,
+                         "k_server_shared" if n <= 32 else "k_server_split<true>"),
                         ("decompress_update", part_ms[2], d * bu, "k_update"),
                         ("warmup_adam_step", warm_avg, d * (n * gbytes + 24),
                          "k_warmup<%s>" % gname))
