@@ -121,15 +121,20 @@ int onebit_plan_get_info(onebit_plan plan, onebit_plan_sizes *info);
 int onebit_plan_get_layout(onebit_plan plan, int64_t *tensor_offset,
                            int64_t *seg_begin, int64_t *seg_end);
 
-/* Whether the chunk owners' calls on this plan may keep their lookup tables
+/* Where the chunk owners' calls on this plan take their lookup tables from
  * (the signed sums of the scales of each group of 8 workers, Algorithm 1's
- * server average) in the workspace, built once per call, instead of building
- * them for every tile (enable != 0, the default; used when the plan reserved
- * the space, see workspace_bytes, and the call's segments average 4 or more
- * tiles).  Results are bit-identical either way; the switch exists to compare
- * the two paths.  Not to be changed while a call on the plan is in flight.
- * Errors: EINVAL (null plan). */
-int onebit_plan_set_server_tables(onebit_plan plan, int32_t enable);
+ * server average): built once per call in the workspace (possible when the
+ * plan reserved the space, see workspace_bytes) or built for every tile.
+ * ONEBIT_SERVER_TABLES_AUTO (the default) uses the workspace when the call's
+ * segments average 4 or more tiles and its tiles times its groups of 8
+ * workers reach 32768; ON uses it whenever the space is there; OFF never.
+ * Results are bit-identical either way; the switch exists to compare the two
+ * paths.  Not to be changed while a call on the plan is in flight.
+ * Errors: EINVAL (null plan, another mode). */
+#define ONEBIT_SERVER_TABLES_OFF 0
+#define ONEBIT_SERVER_TABLES_AUTO 1
+#define ONEBIT_SERVER_TABLES_ON 2
+int onebit_plan_set_server_tables(onebit_plan plan, int32_t mode);
 
 /* The sizes a caller allocates by, as separate host outputs (any may be
  * NULL): D, W, S, the chunk length c_k of every tensor (chunk_len[K], see

@@ -36,7 +36,7 @@ struct onebit_plan_s {
     void *dev_mem = nullptr;                            // one allocation for all tables
     DeviceTables tb{};
     size_t table_bytes = 0;  // chunk owners' lookup tables in the workspace (0: none)
-    bool server_tables = true;  // calls may use them (onebit_plan_set_server_tables)
+    int32_t server_tables = ONEBIT_SERVER_TABLES_AUTO;  // onebit_plan_set_server_tables
     size_t workspace_bytes = 0;
 };
 
@@ -85,8 +85,12 @@ size_t server_flag_offset(const onebit_plan_s *p)
 // many bytes: 256 KB for a BERT-Large-sized buffer with n = 32, 16 MB for
 // one tensor with n = 256.
 constexpr size_t kServerTableBudget = (size_t)32 << 20;
-// ... and a call uses them when its segments average at least this many tiles.
+// ... and a call uses them when its segments average at least this many tiles
+// and its tiles times its groups of 8 workers (the table builds it saves) reach
+// kServerTableMinWork: below that the table kernel's own launch costs more
+// (1-3 us on calls of 1,024 to 16,384 tiles with n = 4 to 32).
 constexpr int64_t kServerTableMinTiles = 4;
+constexpr int64_t kServerTableMinWork = 32768;
 
 int check_plan(const onebit_plan_s *p)
 {
@@ -414,8 +418,11 @@ int run_server(const onebit_plan_s *p, int32_t server_begin, int32_t server_end,
     double *part = (double *)((char *)workspace + server_partial_offset(p));
     const int nown = server_end - server_begin;
     const int64_t owned = (int64_t)p->K * nown;
-    const bool use_tables =
-        p->server_tables && p->table_bytes > 0 && tc >= kServerTableMinTiles * owned;
+    const bool worth = tc >= kServerTableMinTiles * owned &&
+                       tc * ((p->n + 7) / 8) >= kServerTableMinWork;
+    const bool use_tables = p->table_bytes > 0 &&
+                            (p->server_tables == ONEBIT_SERVER_TABLES_ON ||
+                             (p->server_tables == ONEBIT_SERVER_TABLES_AUTO && worth));
     double *tables = use_tables ? (double *)((char *)workspace + server_table_offset(p)) : nullptr;
     int32_t *flags = use_tables ? (int32_t *)((char *)workspace + server_flag_offset(p)) : nullptr;
     const int64_t bb = p->chunk_block_begin[server_begin];
@@ -572,10 +579,13 @@ int onebit_plan_get_layout(onebit_plan p, int64_t *tensor_offset, int64_t *seg_b
     return ONEBIT_OK;
 }
 
-int onebit_plan_set_server_tables(onebit_plan p, int32_t enable)
+int onebit_plan_set_server_tables(onebit_plan p, int32_t mode)
 {
     if (!p) return fail(ONEBIT_EINVAL, "plan is NULL");
-    p->server_tables = enable != 0;
+    if (mode != ONEBIT_SERVER_TABLES_OFF && mode != ONEBIT_SERVER_TABLES_AUTO &&
+        mode != ONEBIT_SERVER_TABLES_ON)
+        return fail(ONEBIT_EINVAL, "server table mode %d is not 0, 1 or 2", mode);
+    p->server_tables = mode;
     return ONEBIT_OK;
 }
 

@@ -107,6 +107,12 @@ def chunk_extent(chunk_word_lo, chunk_word_hi, K, n, server_begin, server_end):
     return int(lo[owned].min()), int(hi.max()), (K - 1) * n + server_end - 1
 
 
+# Modes of Plan.set_server_tables (the ONEBIT_SERVER_TABLES_* constants).
+SERVER_TABLES_OFF = 0
+SERVER_TABLES_AUTO = 1
+SERVER_TABLES_ON = 2
+
+
 class Plan:
     """Layout of K tensors cut into n chunks, with its device tile tables."""
 
@@ -156,10 +162,12 @@ class Plan:
             raise ValueError("plan is closed")
         return self._h
 
-    def set_server_tables(self, enable):
-        """Whether the chunk owners' calls may keep their lookup tables in the
-        workspace (the default) or build them per tile; results are identical."""
-        call("onebit_plan_set_server_tables", self.handle, 1 if enable else 0)
+    def set_server_tables(self, mode):
+        """Where the chunk owners' calls take their lookup tables from:
+        SERVER_TABLES_AUTO (the default), SERVER_TABLES_ON (the workspace
+        whenever the plan reserved it) or SERVER_TABLES_OFF (built per tile);
+        results are identical."""
+        call("onebit_plan_set_server_tables", self.handle, int(mode))
 
     def workspace(self, device):
         nbytes = max(self.workspace_bytes, 256)

@@ -147,20 +147,23 @@ def test_worker_compress_packed_momentum_parity(ob, dev, numel, n):
 SERVER_CASES = [c + ("lognormal",) for c in CASES] + [
     ([1 << 20], 4, "wide"), ([5000, 300, 64], 5, "wide"), ([70_000], 37, "lognormal"),
     ([70_000], 37, "zeros"), ([100_000], 256, "lognormal"), ([100_000], 256, "wide"),
-    # segments of 4 or more tiles: the chunk owners' tables are built once per
-    # call in the workspace (n = 32: four groups of 8; n = 37 and 100: the
-    # split pass, whose last group has 5 and 4 rows)
+    # n = 32: four groups of 8; n = 37 and 100: the split pass, whose last
+    # group has 5 and 4 rows
     ([1 << 20], 32, "lognormal"), ([1 << 20], 4, "zeros"), ([300_000], 37, "lognormal"),
     ([300_000], 37, "wide"), ([300_000], 37, "zeros"), ([700_000], 100, "lognormal")]
 
 
+@pytest.mark.parametrize("tables", ["on", "off"])
 @pytest.mark.parametrize("numel,n,scales", SERVER_CASES)
-def test_server_parity(ob, dev, numel, n, scales):
+def test_server_parity(ob, dev, numel, n, scales, tables):
     """Incoming scales 'lognormal' have a narrow exponent span (the grouped
     summation path); 'wide' spans ~80 binades (one-by-one path); 'zeros'
-    mixes zero scales in."""
+    mixes zero scales in.  tables 'on': the chunk owners' tables are built
+    once per call in the workspace (every plan here reserves it); 'off': per
+    tile."""
     L = oracle.Layout(numel, n)
     plan = ob.Plan(numel, n)
+    plan.set_server_tables(ob.SERVER_TABLES_ON if tables == "on" else ob.SERVER_TABLES_OFF)
     *_, dbar = _random_state(L, 20 + n, n)
     rng = np.random.default_rng(n)
     wbits = rng.integers(0, np.iinfo(np.uint64).max, size=(n, L.W), dtype=np.uint64,
@@ -465,11 +468,13 @@ def test_server_received_chunk_form(ob, dev):
 
 @pytest.mark.parametrize("numel,n,scales", [
     ([1 << 20], 4, "lognormal"), ([1 << 20], 32, "lognormal"), ([1 << 20], 32, "wide"),
-    ([300_000], 37, "zeros"), ([700_000], 100, "lognormal"), ([600_000, 3000, 70], 8, "zeros")])
+    ([300_000], 37, "zeros"), ([700_000], 100, "lognormal"), ([600_000, 3000, 70], 8, "zeros"),
+    ([1 << 23], 32, "lognormal")])
 def test_server_tables_and_per_tile_paths_agree(ob, dev, numel, n, scales):
     """The chunk owners' lookup tables built once per call in the workspace
-    and the tables built per tile give the same words, scales and error
-    state, bit for bit (both sums are exact, or both one by one)."""
+    (ON), built per tile (OFF) and the default choice (AUTO: the workspace for
+    the 2^23-element case, 8,192 tiles x 4 groups) give the same words, scales
+    and error state, bit for bit (both sums are exact, or both one by one)."""
     L = oracle.Layout(numel, n)
     plan = ob.Plan(numel, n)
     rng = np.random.default_rng(40 + n)
@@ -483,9 +488,11 @@ def test_server_tables_and_per_tile_paths_agree(ob, dev, numel, n, scales):
     serr0 = rng.normal(0, 1e-3, size=L.D).astype(np.float32)
     sscales0 = np.exp(rng.normal(-8, 0.5, size=L.S)).astype(np.float32)
     wb, ws_ = _put(wbits, dev), _put(wscales, dev)
+    with pytest.raises(ob.OnebitError):
+        plan.set_server_tables(3)
     res = []
-    for tables in (True, False):
-        plan.set_server_tables(tables)
+    for mode in (ob.SERVER_TABLES_ON, ob.SERVER_TABLES_OFF, ob.SERVER_TABLES_AUTO):
+        plan.set_server_tables(mode)
         serr = _put(serr0, dev)
         sscales = _put(sscales0, dev)
         sbits = torch.zeros(L.W, dtype=torch.int64, device=dev)
@@ -493,8 +500,9 @@ def test_server_tables_and_per_tile_paths_agree(ob, dev, numel, n, scales):
         ob.onebit_server_reduce_compress(plan, 0, n, wb, ws_, serr, sbits, sscales, ws)
         torch.cuda.synchronize()
         res.append((host(serr), host(sbits), host(sscales)))
-    for name, a, c in zip(("server_err", "server_bits", "server_scales"), res[0], res[1]):
-        assert a.tobytes() == c.tobytes(), name
+    for other in res[1:]:
+        for name, a, c in zip(("server_err", "server_bits", "server_scales"), res[0], other):
+            assert a.tobytes() == c.tobytes(), name
     plan.close()
 
 
