@@ -898,12 +898,12 @@ struct ServerBatchLds {
     float scale[kServerRowBatch];
 };
 
-// One wave's LDS working set in the one-wave pass over a run of tiles
-// (n <= kServerRowBatch): the 256-entry tables of every group of 8 rows stay
-// built while the run stays in one segment.  The 16-entry tables are only
-// needed while those are built, before the tile's words are staged, so they
-// share the staging area.
-struct ServerRunLds {
+// One wave's LDS working set when the 256-entry tables of all four groups of
+// 8 rows of a batch are held at once: in the one-wave-per-tile pass
+// (n <= kServerRowBatch), which builds them from the 16-entry tables before
+// the tile's words are staged (so those share the staging area), and in the
+// split pass when it copies each batch's tables from the workspace.
+struct ServerTileLds {
     union {
         uint32_t bits[2 * kTileWords][kBitsStride];
         double lut4[kServerRowBatch / 4][16];
@@ -1234,7 +1234,8 @@ __global__ __launch_bounds__(kBlock) void k_server_tables(
     tables[((u * groups8) + g) * 256 + idx] = v;
 }
 
-// Where a call's owned-segment tables are (TABLES launches), passed as is.
+// Where a call's owned-segment tables and flags are, for the passes that copy
+// them (passed by value as a kernel argument).
 struct ServerTables {
     const double *tables;
     const int32_t *flags;
@@ -1266,7 +1267,9 @@ __device__ __forceinline__ int64_t owned_segment(int64_t q, int n, const ServerT
 }
 
 // Waits for every vector memory operation of the wave, the direct-to-LDS
-// table loads included (the compiler does not track those).
+// table loads included (the compiler does not track those): s_waitcnt with
+// vmcnt 0 (bits 3:0 and 15:14) and the expcnt (6:4) and lgkmcnt (11:8) fields
+// at their maxima, which wait for nothing.
 __device__ __forceinline__ void wait_vmem() { __builtin_amdgcn_s_waitcnt(0x0F70); }
 
 // ---------------------------------------------------------------------------
@@ -1287,13 +1290,13 @@ __global__ __launch_bounds__(kBlock) void k_server_pass(
     int64_t scales_seg_base, float *__restrict__ serr, const float *__restrict__ sscales,
     uint64_t *__restrict__ sbits, double *__restrict__ partial)
 {
-    __shared__ __align__(16) ServerRunLds s_lds[kWavesPerBlock];
+    __shared__ __align__(16) ServerTileLds s_lds[kWavesPerBlock];
     const int lane = threadIdx.x & (kWave - 1);
     // wave-uniform: the tile and its fields live in scalar registers
     const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int64_t rel = xcd_block() * kWavesPerBlock + wv;
     if (rel >= tile_count) return;
-    ServerRunLds &L = s_lds[wv];
+    ServerTileLds &L = s_lds[wv];
     const int groups8 = (n + 7) >> 3;
     const int64_t t = chunk_tiles[tile_begin + rel];
     const Tile tile = tiles[t];
@@ -1438,14 +1441,17 @@ __global__ __launch_bounds__(kBlock) void k_server_shared(
 // applies, wave w takes row batches w, w + kSplitWaves, ...; the waves' exact
 // partial sums are then added through LDS (exact, so in any order), and wave
 // w finishes sub-block w of the tile.  Otherwise wave 0 adds every row one by
-// one in worker order and hands the other waves their sub-blocks.
+// one in worker order and hands the other waves their sub-blocks.  With
+// TABLES the segment's flag and each batch's four tables come from the
+// workspace (k_server_tables); otherwise every wave reads the n scales and
+// builds each batch's tables itself.
 // ---------------------------------------------------------------------------
 constexpr int kSplitWaves = kSubBlocks;
 
 // The per-wave LDS area of the split pass: with TABLES a batch's four tables
 // are copied in at once; otherwise they are built two at a time.
 template <bool TABLES> struct SplitBatchLds { using type = ServerBatchLds; };
-template <> struct SplitBatchLds<true> { using type = ServerRunLds; };
+template <> struct SplitBatchLds<true> { using type = ServerTileLds; };
 
 template <bool TABLES>
 __global__ __launch_bounds__(kSplitWaves * kWave) void k_server_split(
