@@ -1,7 +1,9 @@
 """onebit_step_noalloc, the step for callers that cannot allocate, against
 onebit_step with a caller workspace: identical results, bit for bit, over
 two runs in a row on one device (the second plan smaller than the first, so
-the second run reuses the library's scratch array with less of it live)."""
+the second run reuses the library's scratch array with less of it live),
+with the chunk owners' tables built per tile (the default for plans this
+small) and kept in the workspace, here the scratch array."""
 import ctypes
 
 import pytest
@@ -16,8 +18,9 @@ NAMES = ("x", "m", "worker_err", "worker_bits", "worker_scales", "server_err", "
          "server_scales")
 
 
-def _compare_runs(ob, dev, numel, n, steps, seed):
+def _compare_runs(ob, dev, numel, n, steps, seed, tables):
     plan = ob.Plan(numel, n)
+    plan.set_server_tables(tables)
     assert plan.workspace_bytes <= (96 << 20)
     wl = synth.Workload(name="noalloc", numel=numel, n=n, warmup_steps=1, steps=steps,
                         seed_grads=seed)
@@ -45,11 +48,14 @@ def _compare_runs(ob, dev, numel, n, steps, seed):
     plan.close()
 
 
-def test_noalloc_step_matches_workspace_step(dev):
+@pytest.mark.parametrize("tables", ["auto", "on"])
+def test_noalloc_step_matches_workspace_step(dev, tables):
     import paper_2102_02888_amd as ob
+    mode = ob.SERVER_TABLES_AUTO if tables == "auto" else ob.SERVER_TABLES_ON
     # a plan of 1,079 tiles, then a smaller one of 96 tiles
-    _compare_runs(ob, dev, [1_000_000, 70_001, 5000, 64, 0, 300], 8, steps=3, seed=21)
-    _compare_runs(ob, dev, [90_000, 3000, 1], 4, steps=2, seed=22)
+    _compare_runs(ob, dev, [1_000_000, 70_001, 5000, 64, 0, 300], 8, steps=3, seed=21,
+                  tables=mode)
+    _compare_runs(ob, dev, [90_000, 3000, 1], 4, steps=2, seed=22, tables=mode)
 
 
 def test_noalloc_step_refuses_plans_beyond_its_scratch(dev):
