@@ -54,6 +54,20 @@ def kernels_source_sha256():
     return h.hexdigest()
 
 
+def server_kernel(plan):
+    """The chunk owners' kernel that a whole-range call on this plan runs, by
+    the rule include/onebit.h states for onebit_plan_set_server_tables' AUTO
+    mode: the tables come from the workspace when those of all S segments fit
+    in 32 MiB (2 KB per segment and group of 8 workers), the segments average
+    4 or more tiles and tiles times groups reach 32768."""
+    groups = (plan.n + 7) // 8
+    tables = (plan.S * groups * 2048 <= (32 << 20) and plan.T >= 4 * plan.S
+              and plan.T * groups >= 32768)
+    if plan.n > 32:
+        return "k_server_split<%s>" % ("true" if tables else "false")
+    return "k_server_shared" if tables else "k_server_pass"
+
+
 def measured_traffic(workload, kernel):
     """HBM bytes per launch of `kernel` from the committed rocprofv3 counter
     summary (FETCH_SIZE + WRITE_SIZE, each calibrated on a plain device copy),
@@ -507,10 +521,8 @@ def main():
                     for name, ms, nbytes, kname in (
                         ("worker_compress", part_ms[0], worker_bytes,
                          "k_worker_pass<true, %s>" % gname),
-                        # the BERT-shaped plans keep the chunk owners' tables in
-                        # the workspace: the shared-table pass for n <= 32
                         ("server_reduce_compress", part_ms[1], d * bs,
-                         "k_server_shared" if n <= 32 else "k_server_split<true>"),
+                         server_kernel(plan)),
                         ("decompress_update", part_ms[2], d * bu, "k_update"),
                         ("warmup_adam_step", warm_avg, d * (n * gbytes + 24),
                          "k_warmup<%s>" % gname))
