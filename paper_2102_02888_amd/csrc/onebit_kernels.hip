@@ -903,12 +903,15 @@ struct ServerBatchLds {
 // (n <= kServerRowBatch), which builds them from the 16-entry tables before
 // the tile's words are staged (so those share the staging area), and in the
 // split pass when it copies each batch's tables from the workspace.
+// G8 tables of 256 entries: n <= 8 G8 (the one-wave-per-tile pass sizes them
+// by n, so that smaller n leave room for more workgroups per CU).
+template <int G8 = kServerRowBatch / 8>
 struct ServerTileLds {
     union {
         uint32_t bits[2 * kTileWords][kBitsStride];
         double lut4[kServerRowBatch / 4][16];
     };
-    double lut8[kServerRowBatch / 8][256];
+    double lut8[G8][256];
     float scale[kServerRowBatch];
 };
 
@@ -1282,6 +1285,7 @@ __device__ __forceinline__ void wait_vmem() { __builtin_amdgcn_s_waitcnt(0x0F70)
 // group is looked up, and the tile is finished.  Each wave owns its LDS area,
 // so it synchronises only with itself.
 // ---------------------------------------------------------------------------
+template <int G8>  // groups of 8 workers the LDS tables hold: n <= 8 G8
 __global__ __launch_bounds__(kBlock) void k_server_pass(
     const Tile *__restrict__ tiles, const int32_t *__restrict__ chunk_tiles, int64_t tile_begin,
     int64_t tile_count, int n,
@@ -1290,13 +1294,13 @@ __global__ __launch_bounds__(kBlock) void k_server_pass(
     int64_t scales_seg_base, float *__restrict__ serr, const float *__restrict__ sscales,
     uint64_t *__restrict__ sbits, double *__restrict__ partial)
 {
-    __shared__ __align__(16) ServerTileLds s_lds[kWavesPerBlock];
+    __shared__ __align__(16) ServerTileLds<G8> s_lds[kWavesPerBlock];
     const int lane = threadIdx.x & (kWave - 1);
     // wave-uniform: the tile and its fields live in scalar registers
     const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int64_t rel = xcd_block() * kWavesPerBlock + wv;
     if (rel >= tile_count) return;
-    ServerTileLds &L = s_lds[wv];
+    ServerTileLds<G8> &L = s_lds[wv];
     const int groups8 = (n + 7) >> 3;
     const int64_t t = chunk_tiles[tile_begin + rel];
     const Tile tile = tiles[t];
@@ -1322,7 +1326,7 @@ __global__ __launch_bounds__(kBlock) void k_server_pass(
         server_build_lut4(L, n, lane);
         wave_sync();
 #pragma unroll
-        for (int k = 0; k < (kServerRowBatch / 8) * 256 / kWave; ++k) {
+        for (int k = 0; k < G8 * 256 / kWave; ++k) {
             const int e = lane + kWave * k;
             const int g = e >> 8, idx = e & 255;  // g = k / 4: uniform
             if (g < groups8)
@@ -1451,7 +1455,7 @@ constexpr int kSplitWaves = kSubBlocks;
 // The per-wave LDS area of the split pass: with TABLES a batch's four tables
 // are copied in at once; otherwise they are built two at a time.
 template <bool TABLES> struct SplitBatchLds { using type = ServerBatchLds; };
-template <> struct SplitBatchLds<true> { using type = ServerTileLds; };
+template <> struct SplitBatchLds<true> { using type = ServerTileLds<>; };
 
 template <bool TABLES>
 __global__ __launch_bounds__(kSplitWaves * kWave) void k_server_split(
@@ -1985,10 +1989,24 @@ hipError_t launch_server_pass(const DeviceTables &tb, int64_t tile_begin, int64_
                            bits_ld, bits_word_base, wscales, scales_ld, scales_seg_base, serr,
                            sscales, sbits, partial, st);
     } else {
-        hipLaunchKernelGGL(k_server_pass, dim3((unsigned)blocks_for(tile_count)), dim3(kBlock), 0,
-                           s, tb.tiles, tb.chunk_tiles, tile_begin, tile_count, n, grouping_limit,
-                           wbits, bits_ld, bits_word_base, wscales, scales_ld, scales_seg_base,
-                           serr, sscales, sbits, partial);
+        // tables for as many groups of 8 as n needs: more workgroups per CU
+        // for small n
+        const dim3 grid((unsigned)blocks_for(tile_count)), block(kBlock);
+        if (n <= 8)
+            hipLaunchKernelGGL(k_server_pass<1>, grid, block, 0, s, tb.tiles, tb.chunk_tiles,
+                               tile_begin, tile_count, n, grouping_limit, wbits, bits_ld,
+                               bits_word_base, wscales, scales_ld, scales_seg_base, serr, sscales,
+                               sbits, partial);
+        else if (n <= 16)
+            hipLaunchKernelGGL(k_server_pass<2>, grid, block, 0, s, tb.tiles, tb.chunk_tiles,
+                               tile_begin, tile_count, n, grouping_limit, wbits, bits_ld,
+                               bits_word_base, wscales, scales_ld, scales_seg_base, serr, sscales,
+                               sbits, partial);
+        else
+            hipLaunchKernelGGL(k_server_pass<4>, grid, block, 0, s, tb.tiles, tb.chunk_tiles,
+                               tile_begin, tile_count, n, grouping_limit, wbits, bits_ld,
+                               bits_word_base, wscales, scales_ld, scales_seg_base, serr, sscales,
+                               sbits, partial);
     }
     return hipGetLastError();
 }
