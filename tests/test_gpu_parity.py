@@ -150,7 +150,10 @@ SERVER_CASES = [c + ("lognormal",) for c in CASES] + [
     # n = 32: four groups of 8; n = 37 and 100: the split pass, whose last
     # group has 5 and 4 rows
     ([1 << 20], 32, "lognormal"), ([1 << 20], 4, "zeros"), ([300_000], 37, "lognormal"),
-    ([300_000], 37, "wide"), ([300_000], 37, "zeros"), ([700_000], 100, "lognormal")]
+    ([300_000], 37, "wide"), ([300_000], 37, "zeros"), ([700_000], 100, "lognormal"),
+    # 32 batches of 32 rows; chunks of 256 elements, 782 non-empty (tables of
+    # all 1,000 segments would take 250 MB, so the plan keeps none)
+    ([200_000], 1000, "lognormal"), ([200_000], 1000, "wide")]
 
 
 @pytest.mark.parametrize("tables", ["on", "off"])
