@@ -26,12 +26,16 @@ def test_plain_c_program_matches_oracle(dev):
     assert r.returncode == 0 and r.stdout.strip() == "ok", (r.returncode, r.stdout, r.stderr)
 
 
-def test_step_replays_from_a_hip_graph(dev):
+@pytest.mark.parametrize("tables", ["auto", "on"])
+def test_step_replays_from_a_hip_graph(dev, tables):
     """onebit_step captured once in a graph and replayed gives the eager
-    result bit for bit, replay after replay (fresh gradients each time)."""
+    result bit for bit, replay after replay (fresh gradients each time);
+    'on': the chunk owners' tables are built in the workspace by their own
+    kernel and copied into LDS by direct loads, inside the graph too."""
     import paper_2102_02888_amd as ob
     numel, n = [200_000, 3000, 64], 4
     plan = ob.Plan(numel, n)
+    plan.set_server_tables(ob.SERVER_TABLES_ON if tables == "on" else ob.SERVER_TABLES_AUTO)
     wl = synth.Workload(name="graph", numel=numel, n=n, warmup_steps=2, steps=0)
     states = [ob.State(plan, dev), ob.State(plan, dev)]
     x0 = torch.from_numpy(synth.host_params(wl, plan.D)).to(dev)
