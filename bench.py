@@ -355,7 +355,7 @@ def bench_share(args, wl):
 def main():
     ap = argparse.ArgumentParser(description=__doc__)
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--steps", type=int, default=100)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="bert_large",
                     choices=["tiny", "bert_base", "bert_large", "stress", "share256"])
