@@ -64,8 +64,8 @@ def server_kernel(plan):
     tables = (plan.S * groups * 2048 <= (32 << 20) and plan.T >= 4 * plan.S
               and plan.T * groups >= 32768)
     if plan.n > 32:
-        return "k_server_split<%s>" % ("true" if tables else "false")
-    return "k_server_shared" if tables else "k_server_pass"
+        return "k_server_subblocks" if tables else "k_server_split"
+    return "k_server_shared" if tables else "k_server_pass<%d>" % min(4, groups)
 
 
 def measured_traffic(workload, kernel):

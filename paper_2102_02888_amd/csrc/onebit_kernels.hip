@@ -898,14 +898,12 @@ struct ServerBatchLds {
     float scale[kServerRowBatch];
 };
 
-// One wave's LDS working set when the 256-entry tables of all four groups of
-// 8 rows of a batch are held at once: in the one-wave-per-tile pass
-// (n <= kServerRowBatch), which builds them from the 16-entry tables before
-// the tile's words are staged (so those share the staging area), and in the
-// split pass when it copies each batch's tables from the workspace.
-// G8 tables of 256 entries: n <= 8 G8 (the one-wave-per-tile pass sizes them
-// by n, so that smaller n leave room for more workgroups per CU).
-template <int G8 = kServerRowBatch / 8>
+// One wave's LDS working set in the one-wave-per-tile pass (n <= 8 G8 <=
+// kServerRowBatch): the 256-entry tables of all G8 groups of 8 rows, held at
+// once, are built from the 16-entry tables before the tile's words are staged
+// (so those share the staging area).  G8 follows n, so that smaller n leave
+// room for more workgroups per CU.
+template <int G8>
 struct ServerTileLds {
     union {
         uint32_t bits[2 * kTileWords][kBitsStride];
@@ -1440,37 +1438,186 @@ __global__ __launch_bounds__(kBlock) void k_server_shared(
 }
 
 // ---------------------------------------------------------------------------
+// Chunk owners' pass for many workers (n > kServerRowBatch) with the tables in
+// the workspace: one workgroup per tile, wave w owning sub-block w of it (256
+// elements: words 4w .. 4w+3).  The waves walk the incoming rows together in
+// batches of kServerRowBatch: each loads and stages its own sub-block's words
+// of the batch (4 words of each of 32 rows), the four share the batch's
+// tables (wave g copies group g's), and the next batch's words and tables are
+// on their way while a batch is looked up (two table buffers, one workgroup
+// barrier per batch).  No partial sums are exchanged: each wave finishes its
+// own sub-block, and the tile's sum of squares adds the four waves' in a
+// fixed order.
+// ---------------------------------------------------------------------------
+struct ServerSubLds {
+    uint32_t bits[kSubBlocks][2 * kTileWords / kSubBlocks][kBitsStride];  // each wave's 8 half-words
+    double lut8[2][kServerRowBatch / 8][256];  // batch b's tables in lut8[b & 1]
+    float scale[2][kServerRowBatch];           // batch b's scales (one-by-one sum)
+    double red[kSubBlocks];
+};
+
+// Loads the words of sub-block w of rows [r0, r0 + rows) of the tile (rows <=
+// kServerRowBatch): lane L takes word 4w + L % 4 of rows r0 + L/4 and
+// r0 + L/4 + 16 (zero past the batch's rows and the tile's words).
+__device__ __forceinline__ void server_load_sub_words(const ServerRows &in, int w, int r0,
+                                                      int rows, int lane, uint64_t (&stg)[2])
+{
+    const int wi = 4 * w + (lane & 3);
+#pragma unroll
+    for (int k = 0; k < 2; ++k) {
+        const int r = (lane >> 2) + 16 * k;
+        stg[k] = (r < rows && wi < in.nwords)
+                     ? __builtin_nontemporal_load(in.words + (int64_t)(r0 + r) * in.bits_ld + wi)
+                     : 0ull;
+    }
+}
+
+// Writes them into the wave's staging area ([local half-word][row]; the
+// rows past the batch's last row, up to the next multiple of 8, get zero
+// words).
+__device__ __forceinline__ void server_stage_sub_words(uint32_t (&bits)[2 * kTileWords /
+                                                                          kSubBlocks][kBitsStride],
+                                                       int rows, int lane,
+                                                       const uint64_t (&stg)[2])
+{
+    const int j = lane & 3;
+    const int rows8 = (rows + 7) & ~7;
+#pragma unroll
+    for (int k = 0; k < 2; ++k) {
+        const int r = (lane >> 2) + 16 * k;
+        if (r < rows8) {
+            bits[2 * j][r] = (uint32_t)stg[k];
+            bits[2 * j + 1][r] = (uint32_t)(stg[k] >> 32);
+        }
+    }
+}
+
+__global__ __launch_bounds__(kSubBlocks * kWave) void k_server_subblocks(
+    const Tile *__restrict__ tiles, const int32_t *__restrict__ chunk_tiles, int64_t tile_begin,
+    int64_t tile_count, int n, const uint64_t *__restrict__ wbits, int64_t bits_ld,
+    int64_t bits_word_base, const float *__restrict__ wscales, int64_t scales_ld,
+    int64_t scales_seg_base, float *__restrict__ serr, const float *__restrict__ sscales,
+    uint64_t *__restrict__ sbits, double *__restrict__ partial, ServerTables st)
+{
+    __shared__ __align__(16) ServerSubLds S;
+    const int lane = threadIdx.x & (kWave - 1);
+    const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int64_t rel = xcd_block();
+    if (rel >= tile_count) return;  // the whole workgroup
+    const int64_t t = chunk_tiles[tile_begin + rel];
+    const Tile tile = tiles[t];
+    const int len = tile.len;
+    const int64_t base = tile.start;
+    const ServerRows in{wbits + ((base >> 6) - bits_word_base), bits_ld,
+                        wscales + ((int64_t)tile.seg - scales_seg_base), scales_ld,
+                        (len + 63) >> 6, len == kTileElems};
+    const int groups8 = (n + 7) >> 3;
+    const int64_t u = owned_segment(tile.seg, n, st);
+    const bool grouped = st.flags[u] != 0;
+    const float sprev = sscales[tile.seg];
+    const int li = wv * (kWave * 4) + 4 * lane;  // this wave's sub-block
+    const v4f cv = in.full ? ld4<true>(serr + base, li, len) : ld4<false>(serr + base, li, len);
+    uint64_t stg[2];
+    const int rows0 = min(kServerRowBatch, n);
+    server_load_sub_words(in, wv, 0, rows0, lane, stg);
+    if (grouped && wv < ((rows0 + 7) >> 3))
+        server_fetch_tables(&S.lut8[0][wv][0], st, u, groups8, wv, 1, lane);
+    auto &bits = S.bits[wv];
+    const int hw = lane >> 3;  // the lane's half-word of the sub-block
+    const int o = 16 * (lane & 1) + ((lane & 7) >> 1);
+    double sum[4] = {0.0, 0.0, 0.0, 0.0};
+    for (int r0 = 0; r0 < n; r0 += kServerRowBatch) {  // workgroup-uniform
+        const int cur = (r0 / kServerRowBatch) & 1;
+        const int rows = min(kServerRowBatch, n - r0);
+        const int g8 = (rows + 7) >> 3;
+        if (!grouped && wv == 0 && lane < rows)
+            S.scale[cur][lane] = in.scales[(int64_t)(r0 + lane) * in.scales_ld];
+        server_stage_sub_words(bits, rows, lane, stg);
+        wait_vmem();
+        // this batch's tables, scales and words are in place, and every wave
+        // is done with the previous batch (whose buffers come next)
+        __syncthreads();
+        const int r1 = r0 + kServerRowBatch;
+        if (r1 < n) {
+            const int rows1 = min(kServerRowBatch, n - r1);
+            if (grouped && wv < ((rows1 + 7) >> 3))
+                server_fetch_tables(&S.lut8[cur ^ 1][wv][0], st, u, groups8, (r1 >> 3) + wv, 1,
+                                    lane);
+            server_load_sub_words(in, wv, r1, rows1, lane, stg);
+        }
+        if (grouped) {
+            // regroup the sub-block's (half-word, group of 8 rows) blocks
+            if (lane < 8 * g8) {
+                uint32_t *p = &bits[lane & 7][8 * (lane >> 3)];
+                const uint4 u0 = *(const uint4 *)p;
+                const uint4 u1 = *(const uint4 *)(p + 4);
+                uint32_t a[8] = {u0.x, u0.y, u0.z, u0.w, u1.x, u1.y, u1.z, u1.w};
+                transpose_bits8x8(a);
+                *(uint4 *)p = make_uint4(a[0], a[1], a[2], a[3]);
+                *(uint4 *)(p + 4) = make_uint4(a[4], a[5], a[6], a[7]);
+            }
+            wave_sync();
+            for (int g = 0; g < g8; ++g) {
+                const uint8_t *blk = (const uint8_t *)&bits[hw][8 * g];
+                uint32_t idx[4];
+#pragma unroll
+                for (int c = 0; c < 4; ++c) idx[c] = blk[o + 4 * c];
+                double val[4];
+#pragma unroll
+                for (int c = 0; c < 4; ++c) val[c] = S.lut8[cur][g][idx[c]];
+#pragma unroll
+                for (int c = 0; c < 4; ++c) sum[c] += val[c];
+            }
+        } else {
+            const int shift = 4 * (lane & 7);
+            for (int r = 0; r < rows; ++r) {
+                const double sp = (double)S.scale[cur][r];
+                const uint32_t nib = (bits[hw][r] >> shift) & 0xFu;
+#pragma unroll
+                for (int c = 0; c < 4; ++c) sum[c] += ((nib >> c) & 1u) ? sp : -sp;
+            }
+        }
+        wave_sync();  // before this wave's staging area takes the next batch
+    }
+    const bool pow2 = (n & (n - 1)) == 0;
+    double acc;
+    if (in.full && pow2)
+        acc = server_epilogue_sub<true, true>(sum, cv, sprev, n, lane, tile, wv, serr, sbits);
+    else if (in.full)
+        acc = server_epilogue_sub<true, false>(sum, cv, sprev, n, lane, tile, wv, serr, sbits);
+    else if (pow2)
+        acc = server_epilogue_sub<false, true>(sum, cv, sprev, n, lane, tile, wv, serr, sbits);
+    else
+        acc = server_epilogue_sub<false, false>(sum, cv, sprev, n, lane, tile, wv, serr, sbits);
+    acc = wave_sum_dpp(acc);
+    if (lane == 0) S.red[wv] = acc;
+    __syncthreads();
+    if (threadIdx.x == 0) partial[t] = (S.red[0] + S.red[1]) + (S.red[2] + S.red[3]);
+}
+
+// ---------------------------------------------------------------------------
 // Chunk owners' pass for many workers (n > kServerRowBatch): the
 // kSplitWaves waves of a workgroup share one tile.  When the grouped sum
 // applies, wave w takes row batches w, w + kSplitWaves, ...; the waves' exact
 // partial sums are then added through LDS (exact, so in any order), and wave
 // w finishes sub-block w of the tile.  Otherwise wave 0 adds every row one by
-// one in worker order and hands the other waves their sub-blocks.  With
-// TABLES the segment's flag and each batch's four tables come from the
-// workspace (k_server_tables); otherwise every wave reads the n scales and
-// builds each batch's tables itself.
+// one in worker order and hands the other waves their sub-blocks.  Every wave
+// reads the n scales and builds each batch's tables itself (the pass with the
+// tables in the workspace is k_server_subblocks).
 // ---------------------------------------------------------------------------
 constexpr int kSplitWaves = kSubBlocks;
 
-// The per-wave LDS area of the split pass: with TABLES a batch's four tables
-// are copied in at once; otherwise they are built two at a time.
-template <bool TABLES> struct SplitBatchLds { using type = ServerBatchLds; };
-template <> struct SplitBatchLds<true> { using type = ServerTileLds<>; };
-
-template <bool TABLES>
 __global__ __launch_bounds__(kSplitWaves * kWave) void k_server_split(
     const Tile *__restrict__ tiles, const int32_t *__restrict__ chunk_tiles, int64_t tile_begin,
     int64_t tile_count, int n, int grouping_limit, const uint64_t *__restrict__ wbits,
     int64_t bits_ld, int64_t bits_word_base, const float *__restrict__ wscales,
     int64_t scales_ld, int64_t scales_seg_base, float *__restrict__ serr,
-    const float *__restrict__ sscales, uint64_t *__restrict__ sbits, double *__restrict__ partial,
-    ServerTables st)
+    const float *__restrict__ sscales, uint64_t *__restrict__ sbits, double *__restrict__ partial)
 {
-    using Lds = typename SplitBatchLds<TABLES>::type;
     // the staging areas while rows are summed, then the exchange of partial
     // sums: xch[sub-block][source wave][element of the sub-block]
     union SplitLds {
-        Lds batch[kSplitWaves];
+        ServerBatchLds batch[kSplitWaves];
         double xch[kSubBlocks][kSplitWaves][kWave * 4];
     };
     __shared__ __align__(16) SplitLds s_lds;
@@ -1486,7 +1633,7 @@ __global__ __launch_bounds__(kSplitWaves * kWave) void k_server_split(
     const ServerRows in{wbits + ((base >> 6) - bits_word_base), bits_ld,
                         wscales + ((int64_t)tile.seg - scales_seg_base), scales_ld,
                         (len + 63) >> 6, len == kTileElems};
-    Lds &L = s_lds.batch[wv];
+    ServerBatchLds &L = s_lds.batch[wv];
 
     const float sprev = sscales[tile.seg];
     const int li = wv * (kWave * 4) + 4 * lane;  // this wave's sub-block
@@ -1495,12 +1642,8 @@ __global__ __launch_bounds__(kSplitWaves * kWave) void k_server_split(
     float scl = 0.f;
     const int rfirst = kServerRowBatch * wv;  // may be past n when n <= 96: no rows then
     server_load_batch(in, rfirst, max(0, min(kServerRowBatch, n - rfirst)), lane, stg, scl);
-    // every wave reaches the same decision (reading all n scales, or the
-    // segment's flag)
-    const int groups8 = (n + 7) >> 3;
-    const int64_t u = TABLES ? owned_segment(tile.seg, n, st) : 0;
-    const bool grouped =
-        TABLES ? st.flags[u] != 0 : server_grouped(in, n, grouping_limit, lane, 0.f);
+    // every wave reads all n scales and reaches the same decision
+    const bool grouped = server_grouped(in, n, grouping_limit, lane, 0.f);
     double sum[kSubBlocks][4];
 #pragma unroll
     for (int b = 0; b < kSubBlocks; ++b)
@@ -1510,28 +1653,13 @@ __global__ __launch_bounds__(kSplitWaves * kWave) void k_server_split(
         constexpr int kStep = kServerRowBatch * kSplitWaves;
         for (int r0 = rfirst; r0 < n; r0 += kStep) {
             const int rows = min(kServerRowBatch, n - r0);
-            if constexpr (TABLES) {
-                const int g0 = r0 >> 3, gcnt = (rows + 7) >> 3;
-                server_fetch_tables(&L.lut8[0][0], st, u, groups8, g0, gcnt, lane);
-                server_stage_words(L, in, rows, lane, stg);
-                wait_vmem();  // the tables, before the next batch's words are asked for
-                if (r0 + kStep < n)
-                    server_load_words(in, r0 + kStep, min(kServerRowBatch, n - r0 - kStep), lane,
-                                      stg);
-                wave_sync();
-                server_regroup_bits(L, rows, lane);
-                wave_sync();
-                for (int g = 0; g < gcnt; ++g)
-                    server_lookup_group(sum, L, 8 * g, L.lut8[g], lane);
-            } else {
-                server_stage_batch(L, in, rows, lane, stg, scl);
-                // the next batch's words travel while this one is summed
-                if (r0 + kStep < n)
-                    server_load_batch(in, r0 + kStep, min(kServerRowBatch, n - r0 - kStep), lane,
-                                      stg, scl);
-                wave_sync();
-                server_batch_grouped(sum, L, rows, lane);
-            }
+            server_stage_batch(L, in, rows, lane, stg, scl);
+            // the next batch's words travel while this one is summed
+            if (r0 + kStep < n)
+                server_load_batch(in, r0 + kStep, min(kServerRowBatch, n - r0 - kStep), lane, stg,
+                                  scl);
+            wave_sync();
+            server_batch_grouped(sum, L, rows, lane);
             wave_sync();
         }
     } else if (wv == 0) {
@@ -1974,15 +2102,15 @@ hipError_t launch_server_pass(const DeviceTables &tb, int64_t tile_begin, int64_
     if (n > kServerRowBatch) {
         const dim3 grid((unsigned)xcd_grid(tile_count, 1)), block(kSplitWaves * kWave);
         if (use_tables)
-            hipLaunchKernelGGL(k_server_split<true>, grid, block, 0, s, tb.tiles, tb.chunk_tiles,
+            hipLaunchKernelGGL(k_server_subblocks, dim3((unsigned)xcd_grid(tile_count, 1)),
+                               dim3(kSubBlocks * kWave), 0, s, tb.tiles, tb.chunk_tiles,
+                               tile_begin, tile_count, n, wbits, bits_ld, bits_word_base, wscales,
+                               scales_ld, scales_seg_base, serr, sscales, sbits, partial, st);
+        else
+            hipLaunchKernelGGL(k_server_split, grid, block, 0, s, tb.tiles, tb.chunk_tiles,
                                tile_begin, tile_count, n, grouping_limit, wbits, bits_ld,
                                bits_word_base, wscales, scales_ld, scales_seg_base, serr, sscales,
-                               sbits, partial, st);
-        else
-            hipLaunchKernelGGL(k_server_split<false>, grid, block, 0, s, tb.tiles,
-                               tb.chunk_tiles, tile_begin, tile_count, n, grouping_limit, wbits,
-                               bits_ld, bits_word_base, wscales, scales_ld, scales_seg_base, serr,
-                               sscales, sbits, partial, st);
+                               sbits, partial);
     } else if (use_tables) {
         hipLaunchKernelGGL(k_server_shared, dim3((unsigned)xcd_grid(num_blocks, 1)), dim3(kBlock),
                            0, s, tb.tiles, tb.chunk_tiles, server_blocks, num_blocks, n, wbits,
