@@ -1,7 +1,8 @@
 /* Drives the C ABI with plain HIP allocations (no Python, no torch): a plan,
  * the warm-up, three compression steps, then the error state made explicit,
- * each result compared with the CPU oracle on the same inputs.  Prints "ok"
- * and exits 0 on success. */
+ * each result compared with the CPU oracle on the same inputs.  An optional
+ * argument sets the plan's chunk-owner table mode (onebit_plan_set_server_tables:
+ * 0 off, 1 auto, 2 on).  Prints "ok" and exits 0 on success. */
 #include <hip/hip_runtime_api.h>
 #include <math.h>
 #include <stdint.h>
@@ -55,7 +56,7 @@ static int compare(const char *name, const float *a, const float *b, int64_t len
     return bad != 0;
 }
 
-int main(void)
+int main(int argc, char **argv)
 {
     const int64_t numel[3] = {70001, 4096, 33};
     const int32_t K = 3, n = 4;
@@ -65,6 +66,7 @@ int main(void)
 
     onebit_plan plan;
     CHECK_OB(onebit_plan_create(numel, K, n, &plan));
+    if (argc > 1) CHECK_OB(onebit_plan_set_server_tables(plan, atoi(argv[1])));
     onebit_plan_sizes info;
     CHECK_OB(onebit_plan_get_info(plan, &info));
     if (info.padded_len != D || info.num_segments != S) { fprintf(stderr, "layout differs\n"); return 4; }

@@ -16,13 +16,16 @@ pytestmark = pytest.mark.gpu
 HERE = os.path.dirname(os.path.abspath(__file__))
 
 
-def test_plain_c_program_matches_oracle(dev):
+@pytest.mark.parametrize("tables", ["1", "2"])
+def test_plain_c_program_matches_oracle(dev, tables):
     """tests/c/abi_step_check.c: hipMalloc'd buffers, warm-up + compression
-    steps through the C ABI, compared with the oracle in the same process."""
+    steps through the C ABI, compared with the oracle in the same process;
+    with the chunk owners' tables chosen by the default rule (1: built per
+    tile for this small plan) and kept in the workspace (2)."""
     from tests.c import build as cb
     if not os.path.exists(cb.BIN):
         cb.build()
-    r = subprocess.run([cb.BIN], capture_output=True, text=True, timeout=120)
+    r = subprocess.run([cb.BIN, tables], capture_output=True, text=True, timeout=120)
     assert r.returncode == 0 and r.stdout.strip() == "ok", (r.returncode, r.stdout, r.stderr)
 
 
