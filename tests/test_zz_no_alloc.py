@@ -72,3 +72,41 @@ def test_noalloc_step_refuses_plans_beyond_its_scratch(dev):
                                vp(torch.cuda.current_stream().cuda_stream))
     assert rc == -1 and b"scratch" in L.onebit_last_error()
     plan.close()
+
+
+def test_noalloc_step_bert_large_matches_workspace_step(dev):
+    """At the BERT-Large shape (d = 334,088,192, n = 32: an 86 MB workspace
+    with the chunk owners' tables, inside the scratch array), two States fed
+    one shared gradient tensor run 3 compression steps, one through
+    onebit_step with its workspace and one through onebit_step_noalloc (fp32
+    momentum first, then packed): every word, scale and element agrees bit for
+    bit over all of d and all 32 rows."""
+    import paper_2102_02888_amd as ob
+    wl = synth.get("bert_large")
+    plan = ob.Plan(wl.numel, wl.n)
+    assert plan.workspace_bytes <= (96 << 20)
+    ref = ob.State(plan, dev)
+    new = ob.State(plan, dev, grads=ref.grads)
+    scale_vec = torch.from_numpy(synth.grad_scale_per_element(wl, plan.D, plan.tensor_off)).to(dev)
+    ref.x.copy_(synth.device_params(wl, plan.D, dev))
+    synth.device_grads(wl, plan.D, plan.tensor_off, 1, ref.grads, scale_vec)
+    ref.warmup(wl.lr, wl.beta1, wl.beta2, wl.eps, 1)
+    for name in ("x", "m", "v"):
+        getattr(new, name).copy_(getattr(ref, name))
+    for t in (2, 3, 4):
+        synth.device_grads(wl, plan.D, plan.tensor_off, t, ref.grads, scale_vec)
+        packed = t > 2
+        ref.step(wl.lr, wl.beta1, wl.eps)
+        ob.onebit_step_noalloc(plan, new.x, None if packed else new.m, new.v, new.grads,
+                               new.worker_err, new.server_err, new.worker_bits,
+                               new.worker_scales, new.server_bits, new.server_scales, wl.lr,
+                               wl.beta1, wl.eps)
+        torch.cuda.synchronize()
+        for name in NAMES:
+            u, w = getattr(ref, name), getattr(new, name)
+            if u.dtype == torch.float32:
+                u, w = u.view(torch.int32), w.view(torch.int32)
+            assert torch.equal(u, w), (t, name, int((u != w).sum()))
+    del ref, new
+    plan.close()
+    torch.cuda.empty_cache()
