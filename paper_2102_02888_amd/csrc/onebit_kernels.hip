@@ -30,13 +30,40 @@ namespace {
 // and stores are non-temporal (they do not displace other data in the caches
 // on the way to HBM).
 typedef float v4f __attribute__((ext_vector_type(4)));
+typedef uint32_t v4u32 __attribute__((ext_vector_type(4)));
+typedef uint32_t v2u32 __attribute__((ext_vector_type(2)));
+
+// Full tiles move through raw buffer instructions: the base sits in scalar
+// registers and each lane adds a 32-bit byte offset, and the cache policy is
+// an operand.  Loads are non-temporal (nt); stores are non-temporal at device
+// scope (nt and sc1), which drains the streams of written state to HBM faster
+// than nt alone.  The resource covers 2 GiB from the base, far more than a
+// tile; its fourth word is the gfx9-family buffer format word.
+constexpr int kStreamLoad = 2;        // nt
+constexpr int kStreamStore = 2 | 16;  // nt, sc1
+
+// Resource for a wave-uniform base p (a tile's start in some row: every
+// caller's p is the same in all lanes).  p is read from the first active lane,
+// so the base stays in scalar registers even where the compiler holds it in
+// vector registers, with no per-access loop over distinct lane values.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t stream_rsrc(const void *p)
+{
+    const uint64_t a = (uint64_t)p;
+    const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)a);
+    const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(a >> 32));
+    return __builtin_amdgcn_make_buffer_rsrc((void *)(((uint64_t)hi << 32) | lo), (short)0,
+                                             0x7FFFFFFF, 0x00020000);
+}
 
 // Loads elements li..li+3 of p; FULL means the whole tile is in range (a
 // wave-uniform fact), otherwise lanes past len read zeros.
 template <bool FULL>
 __device__ __forceinline__ v4f ld4(const float *__restrict__ p, int li, int len)
 {
-    if (FULL || li + 4 <= len) return __builtin_nontemporal_load((const v4f *)(p + li));
+    if (FULL)
+        return __builtin_bit_cast(
+            v4f, __builtin_amdgcn_raw_buffer_load_b128(stream_rsrc(p), li * 4, 0, kStreamLoad));
+    if (li + 4 <= len) return __builtin_nontemporal_load((const v4f *)(p + li));
     v4f r = {0.f, 0.f, 0.f, 0.f};
     if (li < len) r.x = p[li];
     if (li + 1 < len) r.y = p[li + 1];
@@ -51,7 +78,8 @@ template <bool FULL>
 __device__ __forceinline__ void st4(float *__restrict__ p, int li, int len, v4f v)
 {
     if (FULL) {
-        __builtin_nontemporal_store(v, (v4f *)(p + li));
+        __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(v4u32, v), stream_rsrc(p),
+                                               li * 4, 0, kStreamStore);
         return;
     }
     if (li + 4 <= len) {
@@ -91,12 +119,15 @@ __device__ __forceinline__ v4f ldg4(const typename G::T *__restrict__ p, int li,
     } else {
         v4f r = {0.f, 0.f, 0.f, 0.f};
         if (FULL || li + 4 <= len) {
-            if constexpr (sizeof(typename G::T) == 2 && __is_same(typename G::T, uint16_t)) {
-                const v4u16 h = __builtin_nontemporal_load((const v4u16 *)(p + li));
+            const v2u32 w =
+                FULL ? __builtin_amdgcn_raw_buffer_load_b64(stream_rsrc(p), li * 2, 0, kStreamLoad)
+                     : __builtin_nontemporal_load((const v2u32 *)(p + li));
+            if constexpr (__is_same(typename G::T, uint16_t)) {
+                const v4u16 h = __builtin_bit_cast(v4u16, w);
 #pragma unroll
                 for (int c = 0; c < 4; ++c) r[c] = widen((uint16_t)h[c]);
             } else {
-                const v4f16 h = __builtin_nontemporal_load((const v4f16 *)(p + li));
+                const v4f16 h = __builtin_bit_cast(v4f16, w);
 #pragma unroll
                 for (int c = 0; c < 4; ++c) r[c] = widen((_Float16)h[c]);
             }
@@ -173,6 +204,13 @@ __device__ __forceinline__ double wave_sum_dpp(double a)
 // This block's logical number in a grid launched by xcd_grid (one contiguous
 // eighth of the logical blocks per XCD).
 __device__ __forceinline__ int64_t xcd_block() { return xcd_block_of(blockIdx.x, gridDim.x); }
+
+// This wave's number within its workgroup, as a wave-uniform (scalar) value,
+// so that tile indices, tile descriptors and the addresses derived from them
+// stay in scalar registers.  The chunk owners' kernels use it; the streaming
+// kernels keep the plain form, since with the scalar one the compiler spills
+// their scalar registers (their buffer bases are made uniform by stream_rsrc).
+__device__ __forceinline__ int wave_id() { return __builtin_amdgcn_readfirstlane(threadIdx.x >> 6); }
 
 // Error from the compensated form: z - C[z] given z and its segment scale s.
 __device__ __forceinline__ float error_of(float z, float s) { return z >= 0.f ? z - s : z + s; }
@@ -1295,7 +1333,7 @@ __global__ __launch_bounds__(kBlock) void k_server_pass(
     __shared__ __align__(16) ServerTileLds<G8> s_lds[kWavesPerBlock];
     const int lane = threadIdx.x & (kWave - 1);
     // wave-uniform: the tile and its fields live in scalar registers
-    const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int wv = wave_id();
     const int64_t rel = xcd_block() * kWavesPerBlock + wv;
     if (rel >= tile_count) return;
     ServerTileLds<G8> &L = s_lds[wv];
@@ -1382,7 +1420,7 @@ __global__ __launch_bounds__(kBlock) void k_server_shared(
 {
     __shared__ __align__(16) ServerSharedLds S;
     const int lane = threadIdx.x & (kWave - 1);
-    const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int wv = wave_id();
     const int64_t b = xcd_block();
     if (b >= num_blocks) return;  // the whole workgroup
     const int32_t entry = blocks[b];
@@ -1501,7 +1539,7 @@ __global__ __launch_bounds__(kSubBlocks * kWave) void k_server_subblocks(
 {
     __shared__ __align__(16) ServerSubLds S;
     const int lane = threadIdx.x & (kWave - 1);
-    const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int wv = wave_id();
     const int64_t rel = xcd_block();
     if (rel >= tile_count) return;  // the whole workgroup
     const int64_t t = chunk_tiles[tile_begin + rel];
@@ -1623,7 +1661,7 @@ __global__ __launch_bounds__(kSplitWaves * kWave) void k_server_split(
     __shared__ __align__(16) SplitLds s_lds;
     __shared__ double s_red[kSplitWaves];
     const int lane = threadIdx.x & (kWave - 1);
-    const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int wv = wave_id();
     const int64_t rel = xcd_block();
     if (rel >= tile_count) return;  // the whole workgroup
     const int64_t t = chunk_tiles[tile_begin + rel];
