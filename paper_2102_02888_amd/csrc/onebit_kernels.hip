@@ -3,11 +3,11 @@
 // Every kernel streams over the flat parameter buffer and, except for the
 // chunk owners' decode-and-average (bound by vector ALU issue), is bound by
 // HBM bandwidth; no MFMA (nothing here is a dense contraction).  Work is cut
-// into tiles of up
-// to 1024 elements that never cross a segment; one wavefront (64 lanes) owns
-// one tile, each lane holding 4 sub-blocks x float4 = 16 elements, so every
-// global load/store is a 128-bit access and a wave moves 1 KiB per
-// instruction.  A sub-block of 256 elements spans four 16-lane DPP rows, and
+// into tiles of up to 1024 elements that never cross a segment; one
+// wavefront (64 lanes) owns one tile, each lane holding 4 sub-blocks x float4
+// = 16 elements (in the packed worker pass two waves share a tile, 2
+// sub-blocks each), so every global load/store is a 128-bit access and a
+// wave moves 1 KiB per instruction.  A sub-block of 256 elements spans four 16-lane DPP rows, and
 // each row's 64 elements form one LSB-first uint64 sign word (bit b of word w
 // of the tile <=> element 64w+b), assembled with a row-wide OR of the lanes'
 // 4-bit nibbles.
@@ -528,22 +528,30 @@ __global__ __launch_bounds__(kRowBlock) void k_warmup(
 // sign words of z_i, per-tile partial sum of z_i^2, and z_i written back as the
 // new compensated error state.
 //
-// Packed momentum (every step after the first): a wave handles one tile for
-// a group of consecutive workers (one worker in practice), and the items run
-// group-major, split into one contiguous eighth per XCD: the waves in flight
-// on an XCD work on the same few worker rows, so each XCD streams through
-// 2 x group rows of (g, error state) at a time instead of all 2n.  The
-// momentum of a tile is re-derived by every worker, 1/8 byte per element per
-// worker from a sign array small enough to stay in the last-level cache.
-// An fp32 momentum (the first compression step) is read once per tile for
-// all local workers instead, by k_worker_rows.
+// Packed momentum (every step after the first): a two-wave workgroup handles
+// one tile for a group of consecutive workers (one worker in practice), wave h
+// holding sub-blocks 2h and 2h+1, and the items run group-major, split into
+// one contiguous eighth per XCD: the waves in flight on an XCD work on the
+// same few worker rows, so each XCD streams through 2 x group rows of
+// (g, error state) at a time instead of all 2n.  Half a tile per wave keeps
+// fewer bytes in flight per wave at a higher occupancy (80 instead of ~120
+// VGPRs), which the mix of two read streams and one written stream favours.
+// The momentum of a tile is re-derived by every worker, 1/8 byte per element
+// per worker from a sign array small enough to stay in the last-level cache.
+// An fp32 momentum (the first compression step) is read once per tile for all
+// local workers instead, by k_worker_rows.
 // ---------------------------------------------------------------------------
-// The shared momentum m_{t-1} of the tile times beta1.  PACKED: m_{t-1} is
-// the previous step's gathered server message, decoded from its sign words
-// and segment scale (+-scale, exactly the fp32 value the update would have
-// stored), so no fp32 momentum buffer is read.
-template <bool FULL, bool PACKED>
-__device__ __forceinline__ void beta1_momentum(v4f (&bm)[kSubBlocks], const Tile &tile, int lane,
+// Sub-blocks per wave of the packed worker pass, and its waves per tile.
+constexpr int kWorkerSubBlocks = 2;
+static_assert(kSubBlocks / kWorkerSubBlocks == kWorkerWavesPerBlock,
+              "the packed worker pass gives each wave of a workgroup part of one tile");
+
+// The shared momentum m_{t-1} of sub-blocks sb0 .. sb0+SB-1 of the tile times
+// beta1.  PACKED: m_{t-1} is the previous step's gathered server message,
+// decoded from its sign words and segment scale (+-scale, exactly the fp32
+// value the update would have stored), so no fp32 momentum buffer is read.
+template <bool FULL, bool PACKED, int SB>
+__device__ __forceinline__ void beta1_momentum(v4f (&bm)[SB], const Tile &tile, int lane, int sb0,
                                                const float *__restrict__ m,
                                                const uint64_t *__restrict__ m_bits,
                                                const float *__restrict__ m_scales, float beta1)
@@ -553,51 +561,56 @@ __device__ __forceinline__ void beta1_momentum(v4f (&bm)[kSubBlocks], const Tile
     if (PACKED) {
         const float s = m_scales[tile.seg];
 #pragma unroll
-        for (int b = 0; b < kSubBlocks; ++b) {
-            const int li = b * (kWave * 4) + 4 * lane;
-            const uint64_t word = (FULL || li < len) ? m_bits[(base >> 6) + 4 * b + (lane >> 4)] : 0ull;
+        for (int b = 0; b < SB; ++b) {
+            const int sb = sb0 + b;
+            const int li = sb * (kWave * 4) + 4 * lane;
+            const uint64_t word =
+                (FULL || li < len) ? m_bits[(base >> 6) + 4 * sb + (lane >> 4)] : 0ull;
             const uint32_t nib = (uint32_t)(word >> (4 * (lane & 15))) & 0xFu;
 #pragma unroll
             for (int c = 0; c < 4; ++c) bm[b][c] = beta1 * (((nib >> c) & 1u) ? s : -s);
         }
     } else {
 #pragma unroll
-        for (int b = 0; b < kSubBlocks; ++b)
-            bm[b] = beta1 * ld4<FULL>(m + base, b * (kWave * 4) + 4 * lane, len);
+        for (int b = 0; b < SB; ++b)
+            bm[b] = beta1 * ld4<FULL>(m + base, (sb0 + b) * (kWave * 4) + 4 * lane, len);
     }
 }
 
-// Worker i's row of the tile: z_i from the momentum term bm = beta1 m, the
-// gradient row and the previous compensated value; its sign words, tile sum
-// of squares and new compensated value.  Split into the loads of the row and
-// the arithmetic and stores, so that a caller can issue the next row's loads
-// before this row's stores.
-template <bool FULL, class G>
-__device__ __forceinline__ void worker_row_load(const Tile &tile, int lane, int i,
+// Worker i's row over sub-blocks sb0 .. sb0+SB-1 of the tile: z_i from the
+// momentum term bm = beta1 m, the gradient row and the previous compensated
+// value; its sign words, sum of squares and new compensated value.  Split into
+// the loads of the row and the arithmetic and stores, so that a caller can
+// issue the next row's loads before this row's stores.
+template <bool FULL, class G, int SB>
+__device__ __forceinline__ void worker_row_load(const Tile &tile, int lane, int sb0, int i,
                                                 const typename G::T *__restrict__ g, int64_t g_ld,
                                                 const float *__restrict__ err, int64_t err_ld,
                                                 const float *__restrict__ scales,
-                                                int64_t scales_ld, v4f (&gv)[kSubBlocks],
-                                                v4f (&cv)[kSubBlocks], float &sp)
+                                                int64_t scales_ld, v4f (&gv)[SB], v4f (&cv)[SB],
+                                                float &sp)
 {
     const int len = tile.len;
     sp = scales[(int64_t)i * scales_ld + tile.seg];
     const typename G::T *gi = g + (int64_t)i * g_ld + tile.start;
     const float *ei = err + (int64_t)i * err_ld + tile.start;
 #pragma unroll
-    for (int b = 0; b < kSubBlocks; ++b) {
-        const int li = b * (kWave * 4) + 4 * lane;
+    for (int b = 0; b < SB; ++b) {
+        const int li = (sb0 + b) * (kWave * 4) + 4 * lane;
         gv[b] = ldg4<FULL, G>(gi, li, len);
         cv[b] = ld4<FULL>(ei, li, len);
     }
 }
 
-template <bool FULL>
-__device__ __forceinline__ void worker_row_store(
-    const Tile &tile, int64_t t, int lane, int64_t num_tiles, const v4f (&bm)[kSubBlocks], int i,
-    const v4f (&gv)[kSubBlocks], const v4f (&cv)[kSubBlocks], float sp, float *__restrict__ err,
-    int64_t err_ld, uint64_t *__restrict__ bits, int64_t bits_ld, double *__restrict__ partial,
-    float omb1)
+// Returns this wave's sum of z_i^2 over its sub-blocks (lanes summed in a
+// fixed order); the caller writes the tile's partial sum.
+template <bool FULL, int SB>
+__device__ __forceinline__ double worker_row_store(const Tile &tile, int lane, int sb0,
+                                                   const v4f (&bm)[SB], int i, const v4f (&gv)[SB],
+                                                   const v4f (&cv)[SB], float sp,
+                                                   float *__restrict__ err, int64_t err_ld,
+                                                   uint64_t *__restrict__ bits, int64_t bits_ld,
+                                                   float omb1)
 {
     const int len = tile.len;
     const int64_t base = tile.start;
@@ -606,8 +619,8 @@ __device__ __forceinline__ void worker_row_store(
     uint64_t *bi = bits + (int64_t)i * bits_ld + (base >> 6);
     double acc = 0.0;
 #pragma unroll
-    for (int b = 0; b < kSubBlocks; ++b) {
-        const int li = b * (kWave * 4) + 4 * lane;
+    for (int b = 0; b < SB; ++b) {
+        const int li = (sb0 + b) * (kWave * 4) + 4 * lane;
         v4f zv;
         uint32_t nib = 0;
 #pragma unroll
@@ -624,45 +637,52 @@ __device__ __forceinline__ void worker_row_store(
         }
         st4<FULL>(ei, li, len, zv);
         const uint64_t word = row_sign_word(nib, lane);
-        const int w = 4 * b + (lane >> 4);
+        const int w = 4 * (sb0 + b) + (lane >> 4);
         if ((lane & 15) == 0 && (FULL || w < nwords)) bi[w] = word;
     }
-    acc = wave_sum(acc);
-    if (lane == 0) partial[(int64_t)i * num_tiles + t] = acc;
+    return wave_sum(acc);
 }
 
-template <bool FULL, class G>
-__device__ __forceinline__ void worker_row(
-    const Tile &tile, int64_t t, int lane, int64_t num_tiles, const v4f (&bm)[kSubBlocks], int i,
-    const typename G::T *__restrict__ g, int64_t g_ld, float *__restrict__ err, int64_t err_ld,
-    const float *__restrict__ scales, int64_t scales_ld, uint64_t *__restrict__ bits,
-    int64_t bits_ld, double *__restrict__ partial, float omb1)
-{
-    v4f gv[kSubBlocks], cv[kSubBlocks];
-    float sp;
-    worker_row_load<FULL, G>(tile, lane, i, g, g_ld, err, err_ld, scales, scales_ld, gv, cv, sp);
-    worker_row_store<FULL>(tile, t, lane, num_tiles, bm, i, gv, cv, sp, err, err_ld, bits,
-                           bits_ld, partial, omb1);
-}
-
-// The tile for workers [i0, i1), the momentum term loaded or decoded once.
+// The tile for workers [i0, i1), this wave's sub-blocks of the momentum term
+// loaded or decoded once.  The waves' sums of each row meet in red (two slots,
+// alternating by row: a wave can be at most one row ahead of the other, so
+// the slot it writes is never the one still being read) and wave 0 adds them
+// in wave order.  Every wave of the workgroup runs the same rows, so every
+// wave reaches every barrier.
 template <bool FULL, bool PACKED, class G>
 __device__ __forceinline__ void worker_tile(
-    const Tile &tile, int64_t t, int lane, int64_t num_tiles, const float *__restrict__ m,
-    const uint64_t *__restrict__ m_bits, const float *__restrict__ m_scales,
-    const typename G::T *__restrict__ g, int64_t g_ld, float *__restrict__ err, int64_t err_ld,
-    const float *__restrict__ scales, int64_t scales_ld, uint64_t *__restrict__ bits,
-    int64_t bits_ld, double *__restrict__ partial, int i0, int i1, float beta1, float omb1)
+    double (&red)[2][kWorkerWavesPerBlock], int &slot, const Tile &tile, int64_t t, int lane,
+    int wv, int64_t num_tiles, const float *__restrict__ m, const uint64_t *__restrict__ m_bits,
+    const float *__restrict__ m_scales, const typename G::T *__restrict__ g, int64_t g_ld,
+    float *__restrict__ err, int64_t err_ld, const float *__restrict__ scales, int64_t scales_ld,
+    uint64_t *__restrict__ bits, int64_t bits_ld, double *__restrict__ partial, int i0, int i1,
+    float beta1, float omb1)
 {
-    v4f bm[kSubBlocks];
-    beta1_momentum<FULL, PACKED>(bm, tile, lane, m, m_bits, m_scales, beta1);
-    for (int i = i0; i < i1; ++i)
-        worker_row<FULL, G>(tile, t, lane, num_tiles, bm, i, g, g_ld, err, err_ld, scales,
-                            scales_ld, bits, bits_ld, partial, omb1);
+    constexpr int SB = kWorkerSubBlocks;
+    const int sb0 = wv * SB;
+    v4f bm[SB];
+    beta1_momentum<FULL, PACKED, SB>(bm, tile, lane, sb0, m, m_bits, m_scales, beta1);
+    for (int i = i0; i < i1; ++i) {
+        v4f gv[SB], cv[SB];
+        float sp;
+        worker_row_load<FULL, G, SB>(tile, lane, sb0, i, g, g_ld, err, err_ld, scales, scales_ld,
+                                     gv, cv, sp);
+        const double acc = worker_row_store<FULL, SB>(tile, lane, sb0, bm, i, gv, cv, sp, err,
+                                                      err_ld, bits, bits_ld, omb1);
+        if (lane == 0) red[slot][wv] = acc;
+        __syncthreads();
+        if (wv == 0 && lane == 0) {
+            double sum = red[slot][0];
+#pragma unroll
+            for (int k = 1; k < kWorkerWavesPerBlock; ++k) sum += red[slot][k];
+            partial[(int64_t)i * num_tiles + t] = sum;
+        }
+        slot ^= 1;
+    }
 }
 
 template <bool PACKED, class G>
-__global__ __launch_bounds__(kWorkerBlock) void k_worker_pass(
+__global__ __launch_bounds__(kWorkerBlock) __attribute__((amdgpu_waves_per_eu(6))) void k_worker_pass(
     const Tile *__restrict__ tiles, int64_t num_tiles, const float *__restrict__ m,
     const uint64_t *__restrict__ m_bits, const float *__restrict__ m_scales,
     const typename G::T *__restrict__ g, int64_t g_ld, float *__restrict__ err, int64_t err_ld,
@@ -670,10 +690,12 @@ __global__ __launch_bounds__(kWorkerBlock) void k_worker_pass(
     int64_t bits_ld, double *__restrict__ partial, int n_local, int group, int64_t num_items,
     float beta1, float omb1)
 {
+    __shared__ double red[2][kWorkerWavesPerBlock];
     const int lane = threadIdx.x & (kWave - 1);
-    // each XCD walks one contiguous eighth of the items
-    const ItemWalk walk = xcd_item_walk(blockIdx.x, gridDim.x, threadIdx.x >> 6,
-                                        kWorkerWavesPerBlock, num_items);
+    const int wv = threadIdx.x >> 6;
+    int slot = 0;
+    // each XCD walks one contiguous eighth of the items, one item per workgroup
+    const ItemWalk walk = xcd_item_walk(blockIdx.x, gridDim.x, num_items);
     for (int64_t item = walk.first; item < walk.end; item += walk.stride) {
         const int64_t grp = item / num_tiles;
         const int64_t t = item - grp * num_tiles;
@@ -681,13 +703,13 @@ __global__ __launch_bounds__(kWorkerBlock) void k_worker_pass(
         const int i1 = min(n_local, i0 + group);
         const Tile tile = tiles[t];
         if (tile.len == kTileElems)
-            worker_tile<true, PACKED, G>(tile, t, lane, num_tiles, m, m_bits, m_scales, g, g_ld,
-                                         err, err_ld, scales, scales_ld, bits, bits_ld, partial,
-                                         i0, i1, beta1, omb1);
+            worker_tile<true, PACKED, G>(red, slot, tile, t, lane, wv, num_tiles, m, m_bits,
+                                         m_scales, g, g_ld, err, err_ld, scales, scales_ld, bits,
+                                         bits_ld, partial, i0, i1, beta1, omb1);
         else
-            worker_tile<false, PACKED, G>(tile, t, lane, num_tiles, m, m_bits, m_scales, g, g_ld,
-                                          err, err_ld, scales, scales_ld, bits, bits_ld, partial,
-                                          i0, i1, beta1, omb1);
+            worker_tile<false, PACKED, G>(red, slot, tile, t, lane, wv, num_tiles, m, m_bits,
+                                          m_scales, g, g_ld, err, err_ld, scales, scales_ld, bits,
+                                          bits_ld, partial, i0, i1, beta1, omb1);
     }
 }
 
@@ -711,11 +733,15 @@ __device__ __forceinline__ void worker_rows_walk(
 {
     v4f ga[kSubBlocks], ca[kSubBlocks], gb[kSubBlocks], cb[kSubBlocks];
     float sa = 0.f, sb = 0.f;
-#define ROW_LOAD(i, gv, cv, sp) \
-    worker_row_load<FULL, G>(tile, lane, i, g, g_ld, err, err_ld, scales, scales_ld, gv, cv, sp)
-#define ROW_STORE(i, gv, cv, sp)                                                           \
-    worker_row_store<FULL>(tile, t, lane, num_tiles, bm, i, gv, cv, sp, err, err_ld, bits, \
-                           bits_ld, partial, omb1)
+#define ROW_LOAD(i, gv, cv, sp)                                                         \
+    worker_row_load<FULL, G, kSubBlocks>(tile, lane, 0, i, g, g_ld, err, err_ld, scales, \
+                                         scales_ld, gv, cv, sp)
+#define ROW_STORE(i, gv, cv, sp)                                                              \
+    do {                                                                                      \
+        const double acc = worker_row_store<FULL, kSubBlocks>(tile, lane, 0, bm, i, gv, cv, sp, \
+                                                              err, err_ld, bits, bits_ld, omb1); \
+        if (lane == 0) partial[(int64_t)(i) * num_tiles + t] = acc;                         \
+    } while (0)
     if (active) ROW_LOAD(0, ga, ca, sa);
     int i = 0;
     // rows i, i+1 and i+2 exist: unconditional loads inside the loop (the
@@ -760,11 +786,11 @@ __global__ __launch_bounds__(kRowBlock) void k_worker_rows(
     // every wave of the workgroup takes one of the two walks, which run the
     // same number of barriers
     if (full) {
-        beta1_momentum<true, false>(bm, tile, lane, m, nullptr, nullptr, beta1);
+        beta1_momentum<true, false, kSubBlocks>(bm, tile, lane, 0, m, nullptr, nullptr, beta1);
         worker_rows_walk<true, G>(tile, t, lane, num_tiles, true, bm, g, g_ld, err, err_ld,
                                   scales, scales_ld, bits, bits_ld, partial, n_local, omb1);
     } else {
-        beta1_momentum<false, false>(bm, tile, lane, m, nullptr, nullptr, beta1);
+        beta1_momentum<false, false, kSubBlocks>(bm, tile, lane, 0, m, nullptr, nullptr, beta1);
         worker_rows_walk<false, G>(tile, t, lane, num_tiles, active, bm, g, g_ld, err, err_ld,
                                    scales, scales_ld, bits, bits_ld, partial, n_local, omb1);
     }
@@ -1973,7 +1999,7 @@ static void launch_worker_t(const DeviceTables &tb, int64_t num_tiles, const flo
     if constexpr (PACKED) {
         const int64_t groups = (n_local + group - 1) / group;
         const int64_t items = groups * num_tiles;
-        const int64_t blocks = worker_grid(items, kWorkerWavesPerBlock, kMaxWorkerGridBlocks);
+        const int64_t blocks = worker_grid(items, kMaxWorkerGridBlocks);
         hipLaunchKernelGGL((k_worker_pass<PACKED, G>), dim3((unsigned)blocks), dim3(kWorkerBlock),
                            0, s, tb.tiles, num_tiles, m, m_bits, m_scales,
                            (const typename G::T *)g, g_ld, err, err_ld, scales, scales_ld, bits,

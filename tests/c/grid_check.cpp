@@ -77,22 +77,21 @@ static void check_server_blocks(const std::vector<int64_t> &counts, int64_t base
         if (seen[(size_t)t] != 1) { fail("tile taken other than once", t, seen[(size_t)t]); break; }
 }
 
-// The worker pass: items walked per XCD with a grid capped at max_blocks.
+// The worker pass: items walked per XCD, one workgroup per item, with a grid
+// capped at max_blocks.
 static void check_worker(int64_t items, int64_t max_blocks)
 {
     ++cases;
-    const int64_t grid = worker_grid(items, kWorkerWavesPerBlock, max_blocks);
+    const int64_t grid = worker_grid(items, max_blocks);
     if (grid % kXcds) fail("worker grid not a multiple of the XCD count", items, grid);
     if (grid > max_blocks + kXcds - 1) fail("worker grid above its cap", items, grid);
     std::vector<unsigned char> seen((size_t)items, 0);
     for (int64_t b = 0; b < grid; ++b) {
-        for (int w = 0; w < kWorkerWavesPerBlock; ++w) {
-            const ItemWalk walk = xcd_item_walk(b, grid, w, kWorkerWavesPerBlock, items);
-            if (walk.stride <= 0) { fail("non-positive stride", items, grid); return; }
-            for (int64_t i = walk.first; i < walk.end; i += walk.stride) {
-                if (i < 0 || i >= items) { fail("item out of range", i, items); break; }
-                if (seen[(size_t)i]++) fail("item taken twice", i, items);
-            }
+        const ItemWalk walk = xcd_item_walk(b, grid, items);
+        if (walk.stride <= 0) { fail("non-positive stride", items, grid); return; }
+        for (int64_t i = walk.first; i < walk.end; i += walk.stride) {
+            if (i < 0 || i >= items) { fail("item out of range", i, items); break; }
+            if (seen[(size_t)i]++) fail("item taken twice", i, items);
         }
     }
     for (int64_t i = 0; i < items; ++i)
