@@ -26,6 +26,9 @@ constexpr int kWorkerBlock = kWave * kWorkerWavesPerBlock;
 // comparison step) run 16-wave workgroups over 16 consecutive tiles.
 constexpr int kRowWaves = 16;
 constexpr int kRowBlock = kWave * kRowWaves;
+// The first compression step's row walk gives two waves to each tile (half a
+// tile each), so its 16-wave workgroups cover 8 tiles.
+constexpr int kWorkerRowTiles = kRowWaves / kWorkerWavesPerBlock;
 
 // Workgroups are dispatched to the chip's 8 XCDs round-robin (block b runs on
 // XCD (b + c) % 8 for a fixed c), and each XCD has its own L2.  Grids are

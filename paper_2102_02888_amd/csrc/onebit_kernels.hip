@@ -722,51 +722,72 @@ __global__ __launch_bounds__(kWorkerBlock) __attribute__((amdgpu_waves_per_eu(6)
 // two rows of loads in flight and never waits on a load issued right after
 // its own stores (measured 23.75 against 23.86 ms for one row at a time, and
 // 24.76 ms without the barriers, on the BERT-Large shape, same buffers).
+// As in the packed pass, two waves share each tile, half a tile each (8 tiles
+// per workgroup); the pair's sums of squares of row i meet in red[i & 1] at
+// the barrier after row i, and the pair's first wave adds them in wave order
+// and writes the partial sum.  A wave writes red[i & 1] again only after the
+// next barrier, by which time the read of row i is done.
 // ---------------------------------------------------------------------------
-template <bool FULL, class G>
+template <bool FULL, class G, int SB>
 __device__ __forceinline__ void worker_rows_walk(
-    const Tile &tile, int64_t t, int lane, int64_t num_tiles, bool active,
-    const v4f (&bm)[kSubBlocks], const typename G::T *__restrict__ g, int64_t g_ld,
+    double (&red)[2][kRowWaves], const Tile &tile, int64_t t, int lane, int wv, int64_t num_tiles,
+    bool active, const v4f (&bm)[SB], const typename G::T *__restrict__ g, int64_t g_ld,
     float *__restrict__ err, int64_t err_ld, const float *__restrict__ scales, int64_t scales_ld,
     uint64_t *__restrict__ bits, int64_t bits_ld, double *__restrict__ partial, int n_local,
     float omb1)
 {
-    v4f ga[kSubBlocks], ca[kSubBlocks], gb[kSubBlocks], cb[kSubBlocks];
+    constexpr int W = kSubBlocks / SB;
+    const int sb0 = (wv % W) * SB;
+    v4f ga[SB], ca[SB], gb[SB], cb[SB];
     float sa = 0.f, sb = 0.f;
-#define ROW_LOAD(i, gv, cv, sp)                                                         \
-    worker_row_load<FULL, G, kSubBlocks>(tile, lane, 0, i, g, g_ld, err, err_ld, scales, \
-                                         scales_ld, gv, cv, sp)
-#define ROW_STORE(i, gv, cv, sp)                                                              \
-    do {                                                                                      \
-        const double acc = worker_row_store<FULL, kSubBlocks>(tile, lane, 0, bm, i, gv, cv, sp, \
-                                                              err, err_ld, bits, bits_ld, omb1); \
-        if (lane == 0) partial[(int64_t)(i) * num_tiles + t] = acc;                         \
+#define ROW_LOAD(i, gv, cv, sp) \
+    worker_row_load<FULL, G, SB>(tile, lane, sb0, i, g, g_ld, err, err_ld, scales, scales_ld, gv, cv, sp)
+#define ROW_STORE(i, gv, cv, sp)                                                                   \
+    do {                                                                                           \
+        const double acc = worker_row_store<FULL, SB>(tile, lane, sb0, bm, i, gv, cv, sp, err,     \
+                                                      err_ld, bits, bits_ld, omb1);                \
+        if (W == 1) {                                                                              \
+            if (lane == 0) partial[(int64_t)(i) * num_tiles + t] = acc;                            \
+        } else if (lane == 0) {                                                                    \
+            red[(i) & 1][wv] = acc;                                                                \
+        }                                                                                          \
+    } while (0)
+#define ROW_SUM(i)                                                                                 \
+    do {                                                                                           \
+        if (W > 1 && active && wv % W == 0 && lane == 0) {                                         \
+            double s_ = red[(i) & 1][wv];                                                          \
+            for (int k_ = 1; k_ < W; ++k_) s_ += red[(i) & 1][wv + k_];                            \
+            partial[(int64_t)(i) * num_tiles + t] = s_;                                            \
+        }                                                                                          \
     } while (0)
     if (active) ROW_LOAD(0, ga, ca, sa);
     int i = 0;
-    // rows i, i+1 and i+2 exist: unconditional loads inside the loop (the
-    // last one or two rows are peeled off), so the wait before row i's
-    // arithmetic leaves row i+1's loads in flight
     for (; i + 2 < n_local; i += 2) {
         if (active) ROW_LOAD(i + 1, gb, cb, sb);
         if (active) ROW_STORE(i, ga, ca, sa);
-        __builtin_amdgcn_s_barrier();  // the workgroup reads each worker row together
+        __builtin_amdgcn_s_barrier();
+        ROW_SUM(i);
         if (active) ROW_LOAD(i + 2, ga, ca, sa);
         if (active) ROW_STORE(i + 1, gb, cb, sb);
         __builtin_amdgcn_s_barrier();
+        ROW_SUM(i + 1);
     }
-    if (i + 1 < n_local) {  // rows i and i+1 remain (n_local is uniform)
+    if (i + 1 < n_local) {
         if (active) ROW_LOAD(i + 1, gb, cb, sb);
         if (active) ROW_STORE(i, ga, ca, sa);
         __builtin_amdgcn_s_barrier();
+        ROW_SUM(i);
         if (active) ROW_STORE(i + 1, gb, cb, sb);
         __builtin_amdgcn_s_barrier();
-    } else {  // row i remains
+        ROW_SUM(i + 1);
+    } else {
         if (active) ROW_STORE(i, ga, ca, sa);
         __builtin_amdgcn_s_barrier();
+        ROW_SUM(i);
     }
 #undef ROW_LOAD
 #undef ROW_STORE
+#undef ROW_SUM
 }
 
 template <class G>
@@ -776,23 +797,27 @@ __global__ __launch_bounds__(kRowBlock) void k_worker_rows(
     const float *__restrict__ scales, int64_t scales_ld, uint64_t *__restrict__ bits,
     int64_t bits_ld, double *__restrict__ partial, int n_local, float beta1, float omb1)
 {
+    constexpr int SB = kWorkerSubBlocks;
+    constexpr int W = kSubBlocks / SB;
+    static_assert(W * kWorkerRowTiles == kRowWaves, "two waves per tile");
+    __shared__ double red[2][kRowWaves];
     const int lane = threadIdx.x & (kWave - 1);
-    const int64_t t = xcd_block() * kRowWaves + (threadIdx.x >> 6);
+    const int wv = threadIdx.x >> 6;
+    const int64_t t = xcd_block() * kWorkerRowTiles + wv / W;
     const bool active = t < num_tiles;
     Tile tile{0, 0, 0};
     if (active) tile = tiles[t];
     const bool full = tile.len == kTileElems;
-    v4f bm[kSubBlocks];
-    // every wave of the workgroup takes one of the two walks, which run the
-    // same number of barriers
+    v4f bm[SB];
     if (full) {
-        beta1_momentum<true, false, kSubBlocks>(bm, tile, lane, 0, m, nullptr, nullptr, beta1);
-        worker_rows_walk<true, G>(tile, t, lane, num_tiles, true, bm, g, g_ld, err, err_ld,
-                                  scales, scales_ld, bits, bits_ld, partial, n_local, omb1);
+        beta1_momentum<true, false, SB>(bm, tile, lane, (wv % W) * SB, m, nullptr, nullptr, beta1);
+        worker_rows_walk<true, G, SB>(red, tile, t, lane, wv, num_tiles, true, bm, g, g_ld, err,
+                                      err_ld, scales, scales_ld, bits, bits_ld, partial, n_local, omb1);
     } else {
-        beta1_momentum<false, false, kSubBlocks>(bm, tile, lane, 0, m, nullptr, nullptr, beta1);
-        worker_rows_walk<false, G>(tile, t, lane, num_tiles, active, bm, g, g_ld, err, err_ld,
-                                   scales, scales_ld, bits, bits_ld, partial, n_local, omb1);
+        beta1_momentum<false, false, SB>(bm, tile, lane, (wv % W) * SB, m, nullptr, nullptr, beta1);
+        worker_rows_walk<false, G, SB>(red, tile, t, lane, wv, num_tiles, active, bm, g, g_ld, err,
+                                       err_ld, scales, scales_ld, bits, bits_ld, partial, n_local,
+                                       omb1);
     }
 }
 
@@ -2008,7 +2033,7 @@ static void launch_worker_t(const DeviceTables &tb, int64_t num_tiles, const flo
         (void)m_bits;
         (void)m_scales;
         (void)group;
-        hipLaunchKernelGGL(k_worker_rows<G>, dim3((unsigned)xcd_grid(num_tiles, kRowWaves)),
+        hipLaunchKernelGGL(k_worker_rows<G>, dim3((unsigned)xcd_grid(num_tiles, kWorkerRowTiles)),
                            dim3(kRowBlock), 0, s, tb.tiles, num_tiles, m,
                            (const typename G::T *)g, g_ld, err, err_ld, scales, scales_ld, bits,
                            bits_ld, partial, n_local, beta1, omb1);

@@ -18,7 +18,8 @@ static void fail(const char *what, long long a, long long b)
     ++failures;
 }
 
-// One wave per tile, waves_per_block waves per block, logical block order.
+// waves_per_block tiles per block (one wave per tile, or one pair of waves),
+// logical block order.
 static void check_tiles(int64_t tiles, int waves_per_block)
 {
     ++cases;
@@ -100,8 +101,10 @@ static void check_worker(int64_t items, int64_t max_blocks)
 
 int main()
 {
-    // the streaming kernels (kWavesPerBlock) and the row-summing ones (kRowWaves)
-    for (int wpb : {kWavesPerBlock, kRowWaves}) {
+    // tiles per block: the streaming kernels (kWavesPerBlock), the row-summing
+    // ones (kRowWaves) and the first compression step (kWorkerRowTiles, two
+    // waves per tile)
+    for (int wpb : {kWavesPerBlock, kRowWaves, kWorkerRowTiles}) {
         for (int64_t t = 1; t <= 600; ++t) check_tiles(t, wpb);
         // BERT-Large (326,288 tiles) and the stress workload's tile counts
         for (int64_t t : {326288LL, 542089LL, 106344LL, 1275LL}) check_tiles(t, wpb);
