@@ -202,7 +202,8 @@ int plan_create_impl(const int64_t *tensor_numel, int32_t num_tensors, int32_t n
         if (e <= b) return 0;
         return (e - 1) / kTileElems - b / kTileElems + 1;
     };
-    // One wave per tile must stay far inside a launch's 2^32 work items.
+    // Below 2^25 tiles every launch stays below 2^32 work-items (the grid
+    // header's launch shapes and pieces).
     int64_t tile_count = 0;
     for (int64_t q = 0; q < p->S; ++q) tile_count += tiles_of(p->seg_begin[q], p->seg_end[q]);
     if (tile_count >= ((int64_t)1 << 25))

@@ -41,9 +41,20 @@ constexpr int kXcds = 8;
 // far below the 2^32 work-item limit.  Kernels over larger pair counts cap
 // their grid at kMaxGridBlocks and stride.  The worker grid (128-thread
 // blocks) may reach 2^24 blocks, 2^31 work-items, so that a BERT-Large-sized
-// pass (n = 32) runs one item per workgroup.
+// pass (n = 32) runs one item per workgroup.  Kernels that give more than 64
+// threads to a tile (the first compression step: 128; the chunk owners'
+// per-tile workgroups: up to 256) are launched over at most kMaxLaunchTiles
+// tiles (or table-sharing workgroups) at a time, at most 2^30 work-items per
+// launch.
 constexpr int64_t kMaxGridBlocks = (int64_t)1 << 22;
 constexpr int64_t kMaxWorkerGridBlocks = (int64_t)1 << 24;
+constexpr int64_t kMaxLaunchTiles = (int64_t)1 << 22;
+
+// Tiles (or workgroups) of the launch that starts at base, of total.
+ONEBIT_HD inline int64_t launch_piece(int64_t total, int64_t base)
+{
+    return total - base < kMaxLaunchTiles ? total - base : kMaxLaunchTiles;
+}
 
 // Blocks for one wave per item at waves_per_block waves per block, rounded up
 // to a multiple of kXcds (0 for no items).

@@ -45,8 +45,8 @@ hipError_t launch_warmup(const DeviceTables &tb, int64_t num_tiles, float *x, fl
                          float bc2, hipStream_t s);
 
 // m != NULL: fp32 momentum; m == NULL: momentum decoded from (m_bits, m_scales).
-// group: workers handled by one wave per tile (1..n_local); the grid runs
-// over groups first, then tiles.
+// group: workers handled by one workgroup per tile (1..n_local); the grid
+// runs over groups first, then tiles.
 hipError_t launch_worker_pass(const DeviceTables &tb, int64_t num_tiles, const float *m,
                               const uint64_t *m_bits, const float *m_scales, const void *g,
                               int grad_dtype, int64_t g_ld, float *err, int64_t err_ld,

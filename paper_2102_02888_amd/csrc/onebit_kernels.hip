@@ -806,7 +806,8 @@ __global__ __launch_bounds__(kRowBlock) void k_worker_rows(
     const Tile *__restrict__ tiles, int64_t num_tiles, const float *__restrict__ m,
     const typename G::T *__restrict__ g, int64_t g_ld, float *__restrict__ err, int64_t err_ld,
     const float *__restrict__ scales, int64_t scales_ld, uint64_t *__restrict__ bits,
-    int64_t bits_ld, double *__restrict__ partial, int n_local, float beta1, float omb1)
+    int64_t bits_ld, double *__restrict__ partial, int n_local, float beta1, float omb1,
+    int64_t tile_base)
 {
     constexpr int SB = kWorkerSubBlocks;
     constexpr int W = kSubBlocks / SB;
@@ -814,7 +815,7 @@ __global__ __launch_bounds__(kRowBlock) void k_worker_rows(
     __shared__ double red[2][kRowWaves];
     const int lane = threadIdx.x & (kWave - 1);
     const int wv = threadIdx.x >> 6;
-    const int64_t t = xcd_block() * kWorkerRowTiles + wv / W;
+    const int64_t t = tile_base + xcd_block() * kWorkerRowTiles + wv / W;
     const bool active = t < num_tiles;
     Tile tile{0, 0, 0};
     if (active) tile = tiles[t];
@@ -2044,10 +2045,17 @@ static void launch_worker_t(const DeviceTables &tb, int64_t num_tiles, const flo
         (void)m_bits;
         (void)m_scales;
         (void)group;
-        hipLaunchKernelGGL(k_worker_rows<G>, dim3((unsigned)xcd_grid(num_tiles, kWorkerRowTiles)),
-                           dim3(kRowBlock), 0, s, tb.tiles, num_tiles, m,
-                           (const typename G::T *)g, g_ld, err, err_ld, scales, scales_ld, bits,
-                           bits_ld, partial, n_local, beta1, omb1);
+        // every launch but the last covers exactly kMaxLaunchTiles tiles (its
+        // grid has no spare workgroups), and the last one's spare waves see
+        // t >= num_tiles
+        static_assert(kMaxLaunchTiles % (kWorkerRowTiles * kXcds) == 0, "whole grids");
+        for (int64_t base = 0; base < num_tiles; base += kMaxLaunchTiles) {
+            const int64_t count = launch_piece(num_tiles, base);
+            hipLaunchKernelGGL(k_worker_rows<G>, dim3((unsigned)xcd_grid(count, kWorkerRowTiles)),
+                               dim3(kRowBlock), 0, s, tb.tiles, num_tiles, m,
+                               (const typename G::T *)g, g_ld, err, err_ld, scales, scales_ld,
+                               bits, bits_ld, partial, n_local, beta1, omb1, base);
+        }
     }
 }
 
@@ -2199,23 +2207,31 @@ hipError_t launch_server_pass(const DeviceTables &tb, int64_t tile_begin, int64_
                            dim3(kBlock), 0, s, n, cb, nown, grouping_limit, wscales, scales_ld,
                            scales_seg_base, tables, flags);
     // more than one batch of rows: the waves of a workgroup share each tile
+    // (one workgroup per tile, launched kMaxLaunchTiles tiles at a time)
     if (n > kServerRowBatch) {
-        const dim3 grid((unsigned)xcd_grid(tile_count, 1)), block(kSplitWaves * kWave);
-        if (use_tables)
-            hipLaunchKernelGGL(k_server_subblocks, dim3((unsigned)xcd_grid(tile_count, 1)),
-                               dim3(kSubBlocks * kWave), 0, s, tb.tiles, tb.chunk_tiles,
-                               tile_begin, tile_count, n, wbits, bits_ld, bits_word_base, wscales,
-                               scales_ld, scales_seg_base, serr, sscales, sbits, partial, st);
-        else
-            hipLaunchKernelGGL(k_server_split, grid, block, 0, s, tb.tiles, tb.chunk_tiles,
-                               tile_begin, tile_count, n, grouping_limit, wbits, bits_ld,
-                               bits_word_base, wscales, scales_ld, scales_seg_base, serr, sscales,
-                               sbits, partial);
+        for (int64_t off = 0; off < tile_count; off += kMaxLaunchTiles) {
+            const int64_t count = launch_piece(tile_count, off);
+            const dim3 grid((unsigned)xcd_grid(count, 1));
+            if (use_tables)
+                hipLaunchKernelGGL(k_server_subblocks, grid, dim3(kSubBlocks * kWave), 0, s,
+                                   tb.tiles, tb.chunk_tiles, tile_begin + off, count, n, wbits,
+                                   bits_ld, bits_word_base, wscales, scales_ld, scales_seg_base,
+                                   serr, sscales, sbits, partial, st);
+            else
+                hipLaunchKernelGGL(k_server_split, grid, dim3(kSplitWaves * kWave), 0, s,
+                                   tb.tiles, tb.chunk_tiles, tile_begin + off, count, n,
+                                   grouping_limit, wbits, bits_ld, bits_word_base, wscales,
+                                   scales_ld, scales_seg_base, serr, sscales, sbits, partial);
+        }
     } else if (use_tables) {
-        hipLaunchKernelGGL(k_server_shared, dim3((unsigned)xcd_grid(num_blocks, 1)), dim3(kBlock),
-                           0, s, tb.tiles, tb.chunk_tiles, server_blocks, num_blocks, n, wbits,
-                           bits_ld, bits_word_base, wscales, scales_ld, scales_seg_base, serr,
-                           sscales, sbits, partial, st);
+        // a workgroup per entry of the block list (up to one per tile)
+        for (int64_t off = 0; off < num_blocks; off += kMaxLaunchTiles) {
+            const int64_t count = launch_piece(num_blocks, off);
+            hipLaunchKernelGGL(k_server_shared, dim3((unsigned)xcd_grid(count, 1)), dim3(kBlock),
+                               0, s, tb.tiles, tb.chunk_tiles, server_blocks + off, count, n,
+                               wbits, bits_ld, bits_word_base, wscales, scales_ld,
+                               scales_seg_base, serr, sscales, sbits, partial, st);
+        }
     } else {
         // tables for as many groups of 8 as n needs: more workgroups per CU
         // for small n

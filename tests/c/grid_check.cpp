@@ -99,8 +99,65 @@ static void check_worker(int64_t items, int64_t max_blocks)
         if (!seen[(size_t)i]) { fail("item not taken", i, items); break; }
 }
 
+// The first compression step's launches: pieces of at most kMaxLaunchTiles
+// tiles, kWorkerRowTiles tiles per 16-wave workgroup, two waves per tile
+// (wave w of logical block lb takes half w % 2 of tile base + lb * 8 + w / 2,
+// active below the plan's tile count).  Every half tile is taken once and no
+// launch reaches 2^32 work-items.  enumerate = false checks the launch sizes
+// only (for counts too large to enumerate here).
+static void check_row_pieces(int64_t tiles, bool enumerate)
+{
+    ++cases;
+    std::vector<unsigned char> seen(enumerate ? (size_t)tiles * 2 : 0, 0);
+    int64_t covered = 0;
+    for (int64_t base = 0; base < tiles; base += kMaxLaunchTiles) {
+        const int64_t count = launch_piece(tiles, base);
+        if (count <= 0 || count > kMaxLaunchTiles) { fail("bad piece", base, count); return; }
+        const int64_t grid = xcd_grid(count, kWorkerRowTiles);
+        if (grid * kRowBlock >= ((int64_t)1 << 32)) fail("row launch of 2^32 work-items", tiles, grid);
+        if (base + count < tiles && grid * kWorkerRowTiles != count)
+            fail("spare workgroups in a piece before the last", tiles, base);
+        covered += count;
+        if (!enumerate) continue;
+        for (int64_t b = 0; b < grid; ++b) {
+            const int64_t lb = xcd_block_of(b, grid);
+            for (int w = 0; w < kRowWaves; ++w) {
+                const int64_t t = base + lb * kWorkerRowTiles + w / 2;
+                if (t >= tiles) continue;
+                if (seen[(size_t)(2 * t + w % 2)]++) fail("half tile taken twice", t, tiles);
+            }
+        }
+    }
+    if (covered != tiles) fail("pieces do not cover the tiles", covered, tiles);
+    for (size_t i = 0; i < seen.size(); ++i)
+        if (!seen[i]) { fail("half tile not taken", (long long)i / 2, tiles); break; }
+}
+
+// The chunk owners' launches with one 256-thread workgroup per tile (or per
+// entry of the shared-table block list): pieces below 2^32 work-items that
+// cover the range.
+static void check_server_pieces(int64_t count_total)
+{
+    ++cases;
+    int64_t covered = 0;
+    for (int64_t off = 0; off < count_total; off += kMaxLaunchTiles) {
+        const int64_t count = launch_piece(count_total, off);
+        const int64_t grid = xcd_grid(count, 1);
+        if (grid * 256 >= ((int64_t)1 << 32)) fail("server launch of 2^32 work-items", count_total, grid);
+        covered += count;
+    }
+    if (covered != count_total) fail("server pieces do not cover the range", covered, count_total);
+}
+
 int main()
 {
+    for (int64_t t : {1LL, 7LL, 8LL, 63LL, 64LL, 65LL, 326288LL, (1LL << 22) - 1, 1LL << 22,
+                      (1LL << 22) + 1, 3 * (1LL << 22) + 5})
+        check_row_pieces(t, true);
+    for (int64_t t : {(1LL << 25) - 1, (1LL << 25) - 64, (1LL << 24) + 3})
+        check_row_pieces(t, false);
+    for (int64_t t : {1LL, 1275LL, 326288LL, (1LL << 22) + 1, (1LL << 24) - 1, (1LL << 25) - 1})
+        check_server_pieces(t);
     // tiles per block: the streaming kernels (kWavesPerBlock), the row-summing
     // ones (kRowWaves) and the first compression step (kWorkerRowTiles, two
     // waves per tile)
