@@ -318,3 +318,55 @@ def test_update_full_size_exact(ob, dev):
     del xg, mg
     plan.close()
     torch.cuda.empty_cache()
+
+
+def test_first_step_over_two_launch_pieces(ob, dev):
+    """The first compression step's kernel (two waves per tile) is launched
+    over at most 2^22 tiles at a time.  One tensor of 2^22 + 3 tiles (a short
+    last tile), n = 1: the step runs as two launches.  The error state starts
+    at zero, so every element's new compensated value must be the first step's
+    z = fl(beta1 m) + fl((1 - beta1) g) (Algorithm 1's momentum step with a
+    zero error); an element processed twice or not at all would differ.  A
+    plain fp32 torch reference checks all 4.3e9 elements, in chunks; the sign
+    words around the boundary between the launches and the segment's scale
+    are checked too.  (The step's update overwrites m with the decoded server
+    message, so the reference uses a copy of m taken before the step.)  Needs
+    about 125 GB of device memory."""
+    torch.cuda.empty_cache()
+    tiles = (1 << 22) + 3
+    d = tiles * 1024 - 100
+    plan = ob.Plan([d], 1)
+    assert plan.T == tiles
+    st = ob.State(plan, dev)
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(2102)
+    st.m[:d].normal_(0.0, 1e-3, generator=gen)
+    st.grads[0, :d].normal_(0.0, 1e-2, generator=gen)
+    st.v[:d].uniform_(1e-8, 1e-6, generator=gen)
+    beta1, lr, eps = 0.9, 1e-4, 1e-8
+    m0 = st.m.clone()
+    st.step(lr, beta1, eps)  # first compression step: fp32 momentum, k_worker_rows
+    torch.cuda.synchronize()
+    b1 = torch.tensor(beta1, dtype=torch.float32, device=dev)
+    omb1 = torch.tensor(1.0, dtype=torch.float32, device=dev) - b1
+    chunk = 1 << 28
+    sq = torch.zeros((), dtype=torch.float64, device=dev)
+    for c0 in range(0, plan.D, chunk):
+        c1 = min(plan.D, c0 + chunk)
+        z = b1 * m0[c0:c1] + omb1 * st.grads[0, c0:c1]
+        got = st.worker_err[0, c0:c1]
+        bad = int((got != z).sum())
+        assert bad == 0, "%d elements of [%d, %d) differ from the first step's z" % (bad, c0, c1)
+        sq += (z.double() ** 2).sum()
+        del z, got
+    # sign words of the tiles on both sides of the boundary between the launches
+    t0, t1 = (1 << 22) - 2, (1 << 22) + 2
+    zb = (b1 * m0[t0 * 1024:t1 * 1024] + omb1 * st.grads[0, t0 * 1024:t1 * 1024]).cpu().numpy()
+    want = np.packbits((zb >= 0).reshape(-1, 64)[:, ::-1], axis=1).view(">u8").ravel()
+    got_w = host(st.worker_bits[0, t0 * 16:t1 * 16]).view(np.uint64)
+    np.testing.assert_array_equal(got_w, want.astype(np.uint64))
+    scale = float(np.sqrt(float(sq) / d).astype(np.float32))
+    assert abs(float(st.worker_scales[0, 0]) - scale) <= 1e-6 * scale
+    del st, m0
+    plan.close()
+    torch.cuda.empty_cache()
