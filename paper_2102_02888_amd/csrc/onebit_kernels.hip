@@ -692,6 +692,8 @@ __device__ __forceinline__ void worker_tile(
     }
 }
 
+// Six waves per SIMD: the kernel's register count sits at that limit (80
+// VGPRs); without the hint the compiler settles on 85 and five waves.
 template <bool PACKED, class G>
 __global__ __launch_bounds__(kWorkerBlock) __attribute__((amdgpu_waves_per_eu(6))) void k_worker_pass(
     const Tile *__restrict__ tiles, int64_t num_tiles, const float *__restrict__ m,
