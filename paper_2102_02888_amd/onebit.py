@@ -375,11 +375,21 @@ class State:
         self.x = torch.zeros(D, **f)
         self.m = torch.zeros(D, **f)
         self.v = torch.zeros(D, **f)
-        if grads is None:
-            grads = torch.zeros((n if grad_rows is None else grad_rows, D), dtype=grad_dtype,
-                                device=device)
-        self.grads = grads
-        self.worker_err = torch.zeros((n, D), **f)
+        if grads is None and grad_dtype == torch.float32 and grad_rows in (None, n):
+            # worker i's gradient and error rows side by side in one allocation
+            # ([n, 2, D], rows addressed with a leading dimension of 2D): the
+            # two rows that the worker pass streams together then keep one
+            # fixed offset from each other in memory, where two separate
+            # allocations land wherever the allocator puts them, and some of
+            # those placements run the pass up to 5% slower
+            pair = torch.zeros((n, 2, D), **f)
+            self.grads, self.worker_err = pair[:, 0, :], pair[:, 1, :]
+        else:
+            if grads is None:
+                grads = torch.zeros((n if grad_rows is None else grad_rows, D), dtype=grad_dtype,
+                                    device=device)
+            self.grads = grads
+            self.worker_err = torch.zeros((n, D), **f)
         self.worker_bits = torch.zeros((n, W), dtype=torch.int64, device=device)
         self.worker_scales = torch.zeros((n, S), **f)
         self.server_err = torch.zeros(D, **f)
