@@ -603,13 +603,11 @@ __device__ __forceinline__ void worker_row_load(const Tile &tile, int lane, int 
 }
 
 // Returns this wave's sum of z_i^2 over its sub-blocks (lanes summed in a
-// fixed order); the caller writes the tile's partial sum.  Every sub-block is
-// computed before the first store: a wave's vector memory counter completes
-// in issue order, so a wait for a later sub-block's loads issued after an
-// earlier sub-block's stores would also wait for those stores.  (The
-// sign-word stores sit under a lane condition, so the compiler counts as if
-// they had not been issued, and its wait then covers the error-state store
-// issued before them too.)
+// fixed order); the caller writes the tile's partial sum.  Each sub-block is
+// stored as soon as it is computed: computing every sub-block first keeps
+// more values live, and at the worker pass's 80 VGPRs the compiler then
+// issues a 16-bit-gradient row's loads one after another (measured 5.7%
+// slower for bf16 gradients, no faster for fp32).
 template <bool FULL, int SB>
 __device__ __forceinline__ double worker_row_store(const Tile &tile, int lane, int sb0,
                                                    const v4f (&bm)[SB], int i, const v4f (&gv)[SB],
@@ -624,30 +622,25 @@ __device__ __forceinline__ double worker_row_store(const Tile &tile, int lane, i
     float *ei = err + (int64_t)i * err_ld + base;
     uint64_t *bi = bits + (int64_t)i * bits_ld + (base >> 6);
     double acc = 0.0;
-    v4f zv[SB];
-    uint32_t nib[SB];
 #pragma unroll
     for (int b = 0; b < SB; ++b) {
         const int li = (sb0 + b) * (kWave * 4) + 4 * lane;
-        nib[b] = 0;
+        v4f zv;
+        uint32_t nib = 0;
 #pragma unroll
         for (int c = 0; c < 4; ++c) {
             const float d = error_of(cv[b][c], sp);
             float mi = omb1 * gv[b][c];
             mi = bm[b][c] + mi;
             const float z = mi + d;
-            zv[b][c] = z;
+            zv[c] = z;
             const bool valid = FULL || li + c < len;
             const double zd = valid ? (double)z : 0.0;
             acc += zd * zd;
-            nib[b] |= (valid && z >= 0.f) ? (1u << c) : 0u;
+            nib |= (valid && z >= 0.f) ? (1u << c) : 0u;
         }
-    }
-#pragma unroll
-    for (int b = 0; b < SB; ++b) st4<FULL>(ei, (sb0 + b) * (kWave * 4) + 4 * lane, len, zv[b]);
-#pragma unroll
-    for (int b = 0; b < SB; ++b) {
-        const uint64_t word = row_sign_word(nib[b], lane);
+        st4<FULL>(ei, li, len, zv);
+        const uint64_t word = row_sign_word(nib, lane);
         const int w = 4 * (sb0 + b) + (lane >> 4);
         if ((lane & 15) == 0 && (FULL || w < nwords)) bi[w] = word;
     }

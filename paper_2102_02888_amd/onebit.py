@@ -375,15 +375,18 @@ class State:
         self.x = torch.zeros(D, **f)
         self.m = torch.zeros(D, **f)
         self.v = torch.zeros(D, **f)
-        if grads is None and grad_dtype == torch.float32 and grad_rows in (None, n):
+        if grads is None and grad_rows in (None, n) and D > 0:
             # worker i's gradient and error rows side by side in one allocation
-            # ([n, 2, D], rows addressed with a leading dimension of 2D): the
-            # two rows that the worker pass streams together then keep one
-            # fixed offset from each other in memory, where two separate
-            # allocations land wherever the allocator puts them, and some of
-            # those placements run the pass up to 5% slower
-            pair = torch.zeros((n, 2, D), **f)
-            self.grads, self.worker_err = pair[:, 0, :], pair[:, 1, :]
+            # (row i: D gradients, then D fp32 errors; D is a multiple of 64, so
+            # every row stays 16-byte aligned): the two rows that the worker
+            # pass streams together then keep one fixed offset from each
+            # other in memory, where two separate allocations land wherever
+            # the allocator puts them, and some of those placements run the
+            # pass up to 5% slower
+            gsize = torch.empty((), dtype=grad_dtype).element_size()
+            pair = torch.zeros((n, (gsize + 4) * D), dtype=torch.uint8, device=device)
+            self.grads = pair[:, :gsize * D].view(grad_dtype)
+            self.worker_err = pair[:, gsize * D:].view(torch.float32)
         else:
             if grads is None:
                 grads = torch.zeros((n if grad_rows is None else grad_rows, D), dtype=grad_dtype,
