@@ -354,6 +354,21 @@ def onebit_error_materialize(plan, err_state, scales, delta_out, rows=None, stre
          _ptr(delta_out, torch.float32, "delta_out", D, r), _ld(delta_out), _stream(stream))
 
 
+def paired_rows(n, D, grad_dtype, device):
+    """(grads, worker_err): [n, D] row views into one zeroed allocation whose
+    row i holds worker i's D gradients (grad_dtype) and then its D fp32
+    errors.  The two rows that the worker pass streams together then keep one
+    fixed offset from each other in memory, where two separate allocations
+    land wherever the allocator puts them, and some of those placements run
+    the pass up to 5% slower.  D must be a positive multiple of 64 (a plan's
+    padded length), which keeps every row 16-byte aligned."""
+    if D <= 0 or D % 64:
+        raise ValueError("D must be a positive multiple of 64, got %d" % D)
+    gsize = torch.empty((), dtype=grad_dtype).element_size()
+    pair = torch.zeros((n, (gsize + 4) * D), dtype=torch.uint8, device=device)
+    return pair[:, :gsize * D].view(grad_dtype), pair[:, gsize * D:].view(torch.float32)
+
+
 class State:
     """Device buffers of one compression-stage run with n_local simulated
     workers (all zero-initialised except x, m, v which the caller fills).
@@ -376,17 +391,7 @@ class State:
         self.m = torch.zeros(D, **f)
         self.v = torch.zeros(D, **f)
         if grads is None and grad_rows in (None, n) and D > 0:
-            # worker i's gradient and error rows side by side in one allocation
-            # (row i: D gradients, then D fp32 errors; D is a multiple of 64, so
-            # every row stays 16-byte aligned): the two rows that the worker
-            # pass streams together then keep one fixed offset from each
-            # other in memory, where two separate allocations land wherever
-            # the allocator puts them, and some of those placements run the
-            # pass up to 5% slower
-            gsize = torch.empty((), dtype=grad_dtype).element_size()
-            pair = torch.zeros((n, (gsize + 4) * D), dtype=torch.uint8, device=device)
-            self.grads = pair[:, :gsize * D].view(grad_dtype)
-            self.worker_err = pair[:, gsize * D:].view(torch.float32)
+            self.grads, self.worker_err = paired_rows(n, D, grad_dtype, device)
         else:
             if grads is None:
                 grads = torch.zeros((n if grad_rows is None else grad_rows, D), dtype=grad_dtype,

@@ -1,10 +1,12 @@
 """Host-side logic of the Python binding (no GPU): the per-chunk word ranges
 that size a chunk owners' call, against brute force, and their per-call cost
-on the 5,000-tensor stress layout."""
+on the 5,000-tensor stress layout; the paired gradient and error rows that
+State allocates."""
 import time
 
 import numpy as np
 import pytest
+import torch
 
 import oracle
 import synth
@@ -54,3 +56,32 @@ def test_chunk_extent_cost_on_stress_layout():
     assert ext == _brute_extent(L, 0, L.n)
     for j in (0, 3, L.n - 1):
         assert chunk_extent(lo, hi, L.K, L.n, j, j + 1) == _brute_extent(L, j, j + 1)
+
+
+@pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16, torch.float16])
+def test_paired_rows_layout(dtype):
+    """State's gradient and error rows share one allocation: row i holds D
+    gradients and then D fp32 errors.  The views have the shapes and leading
+    dimensions the ABI is given, every row starts 16-byte aligned, and a
+    worker's two rows do not overlap each other or the next worker's."""
+    from paper_2102_02888_amd.onebit import paired_rows
+    n, D = 5, 192
+    g, e = paired_rows(n, D, dtype, "cpu")
+    gs = g.element_size()
+    assert g.dtype == dtype and e.dtype == torch.float32
+    assert g.shape == (n, D) and e.shape == (n, D)
+    row_bytes = (gs + 4) * D
+    assert g.stride() == (row_bytes // gs, 1) and e.stride() == (row_bytes // 4, 1)
+    base = g.data_ptr()
+    for i in range(n):
+        g0, e0 = g[i].data_ptr() - base, e[i].data_ptr() - base
+        assert g0 == i * row_bytes and e0 == i * row_bytes + gs * D
+        assert g0 % 16 == 0 and e0 % 16 == 0
+    g.fill_(1)
+    assert float(e.abs().sum()) == 0.0
+    e.fill_(2)
+    assert bool((g == 1).all())
+    with pytest.raises(ValueError):
+        paired_rows(n, 100, dtype, "cpu")
+    with pytest.raises(ValueError):
+        paired_rows(n, 0, dtype, "cpu")
