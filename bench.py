@@ -45,12 +45,42 @@ def algorithmic_bytes_per_param(n, grad_bytes=4):
 KERNEL_SOURCES = ("onebit_kernels.hip", "onebit_abi.hip", "onebit_internal.h", "onebit_grid.h")
 
 
+def code_text(src):
+    """C/C++ source without its comments, each run of whitespace one space:
+    what the compiler sees, so that editing a comment keeps recorded counters
+    valid.  String and character literals are kept as written."""
+    out, i, n = [], 0, len(src)
+    while i < n:
+        c = src[i]
+        if src.startswith("//", i):
+            j = src.find("\n", i)
+            i = n if j < 0 else j
+            out.append(" ")
+        elif src.startswith("/*", i):
+            j = src.find("*/", i + 2)
+            i = n if j < 0 else j + 2
+            out.append(" ")
+        elif c in "\"'":
+            j = i + 1
+            while j < n and src[j] != c:
+                j += 2 if src[j] == "\\" else 1
+            out.append(src[i:j + 1])
+            i = j + 1
+        else:
+            out.append(c)
+            i += 1
+    return " ".join("".join(out).split())
+
+
 def kernels_source_sha256():
-    """Digest of KERNEL_SOURCES, in that order."""
+    """Digest of the code of KERNEL_SOURCES (comments and layout aside), in
+    that order."""
     import hashlib
     h = hashlib.sha256()
     for f in KERNEL_SOURCES:
-        h.update(open(os.path.join(ROOT, "paper_2102_02888_amd", "csrc", f), "rb").read())
+        with open(os.path.join(ROOT, "paper_2102_02888_amd", "csrc", f)) as fh:
+            h.update(code_text(fh.read()).encode())
+        h.update(b"\0")
     return h.hexdigest()
 
 

@@ -354,9 +354,10 @@ int run_worker(const onebit_plan_s *p, const float *m, const uint64_t *m_bits,
                void *workspace, hipStream_t s)
 {
     double *part = (double *)((char *)workspace + worker_partial_offset(p));
-    // Packed momentum costs 1/8 byte per element to re-derive, so each wave
-    // takes one worker and the grid streams two rows at a time; an fp32
-    // momentum is read once per tile for all local workers instead.
+    // Packed momentum costs 1/8 byte per element to re-derive, so each
+    // workgroup takes one (worker, tile) item and all workgroups in flight
+    // stream the same two rows (gradient and error state of one worker); an
+    // fp32 momentum is read once per tile for all local workers instead.
     const int group = m ? n_local : 1;
     if (p->T > 0)
         TRY_HIP(onebit::launch_worker_pass(p->tb, p->T, m, m_bits, m_scales, grads, grad_dtype,

@@ -22,18 +22,30 @@ def test_measured_traffic_requires_matching_kernel_source(tmp_path, monkeypatch)
     src = tmp_path / "paper_2102_02888_amd" / "csrc"
     src.mkdir(parents=True)
     for f in bench.KERNEL_SOURCES:
-        (src / f).write_text("// %s v1\n" % f)
+        (src / f).write_text("// %s\nint v = 1;\n" % f)
     import hashlib
-    sha = hashlib.sha256("".join("// %s v1\n" % f for f in bench.KERNEL_SOURCES).encode()).hexdigest()
-    info = {"kernels_source_sha256": sha,
+    h = hashlib.sha256()
+    for f in bench.KERNEL_SOURCES:
+        h.update(b"int v = 1;\0")
+    info = {"kernels_source_sha256": h.hexdigest(),
             "kernels": {"k_update": {"traffic_bytes": 123.0}}}
     (prof / "pmc_traffic_w.md").write_text("x\n```json\n%s\n```\n" % json.dumps(info))
     monkeypatch.setattr(bench, "ROOT", str(tmp_path))
     assert bench.measured_traffic("w", "k_update") == 123.0
     assert bench.measured_traffic("w", "k_other") is None
     assert bench.measured_traffic("missing", "k_update") is None
-    (src / "onebit_grid.h").write_text("// launch shapes v2\n")
+    # a comment or layout edit keeps the counters, a code change drops them
+    (src / "onebit_grid.h").write_text("/* launch shapes */ int v =\n  1; // v2\n")
+    assert bench.measured_traffic("w", "k_update") == 123.0
+    (src / "onebit_grid.h").write_text("int v = 2;\n")
     assert bench.measured_traffic("w", "k_update") is None
+
+
+def test_code_text_drops_comments_only():
+    src = ('int a; // "x"\n/* b\n c */ const char *s = "// kept /* \\" q";'
+           " char q = '/';  x  =\t1 / 2;")
+    assert bench.code_text(src) == ('int a; const char *s = "// kept /* \\" q";'
+                                    " char q = '/'; x = 1 / 2;")
 
 
 def test_multi_gpu_request_is_refused():
