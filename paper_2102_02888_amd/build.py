@@ -1,4 +1,5 @@
-"""Builds libonebit.so (the gfx950 HIP kernels and the C ABI) in-tree."""
+"""Builds libonebit.so (the gfx950 HIP kernels and the C ABI) in-tree, and
+the standalone HBM streaming probe lib/hbm_probe."""
 import os
 import subprocess
 import sys
@@ -7,6 +8,8 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 SOURCES = [os.path.join(HERE, "csrc", f) for f in ("onebit_kernels.hip", "onebit_abi.hip")]
 LIB = os.path.join(HERE, "lib", "libonebit.so")
+PROBE_SOURCE = os.path.join(HERE, "csrc", "hbm_probe.hip")
+PROBE = os.path.join(HERE, "lib", "hbm_probe")
 
 # -ffp-contract=off: every fp32 operation is rounded once, as the method's
 # arithmetic is specified (no fused multiply-add contraction).
@@ -19,10 +22,10 @@ HIPCC_FLAGS = [
 ]
 
 
-def build(verbose: bool = False) -> str:
-    os.makedirs(os.path.dirname(LIB), exist_ok=True)
-    tmp = LIB + ".tmp%d" % os.getpid()
-    cmd = ["hipcc"] + HIPCC_FLAGS + ["-o", tmp] + SOURCES
+def _hipcc(flags, sources, target, verbose):
+    os.makedirs(os.path.dirname(target), exist_ok=True)
+    tmp = target + ".tmp%d" % os.getpid()
+    cmd = ["hipcc"] + flags + ["-o", tmp] + sources
     if verbose:
         print(" ".join(cmd), flush=True)
     r = subprocess.run(cmd, capture_output=True, text=True)
@@ -30,10 +33,17 @@ def build(verbose: bool = False) -> str:
                     if "packed-fp32-ops" not in l and "unused during compilation" not in l)
     if r.returncode != 0:
         sys.stderr.write(out + "\n")
-        raise RuntimeError("hipcc failed building libonebit.so")
+        raise RuntimeError("hipcc failed building " + os.path.basename(target))
     if verbose and out.strip():
         print(out)
-    os.replace(tmp, LIB)
+    os.replace(tmp, target)
+    return target
+
+
+def build(verbose: bool = False) -> str:
+    _hipcc(HIPCC_FLAGS, SOURCES, LIB, verbose)
+    probe_flags = [f for f in HIPCC_FLAGS if f not in ("-fPIC", "-shared")]
+    _hipcc(probe_flags, [PROBE_SOURCE], PROBE, verbose)
     return LIB
 
 
