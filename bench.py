@@ -266,6 +266,31 @@ def hbm_probe(dev, nbytes=2 << 30, reps=10):
     return out
 
 
+def hbm_ceilings(dev, nbytes=2 << 30):
+    """Best rates of the hand-written streaming kernels (the passes' 128-bit
+    non-temporal buffer loads and stores, XCD-contiguous grids) over `nbytes`
+    per stream: one stream read, a copy, and two streams read with the second
+    rewritten in place (the worker pass's mix), each over 1, 2 or 4 KB of
+    each stream in flight per wave and 2 to 8 four-wave workgroups per CU.
+    None when the probe library is not built."""
+    import torch
+    try:
+        from paper_2102_02888_amd import hbm_probe
+        hbm_probe.lib()
+    except ImportError as e:
+        log("no HBM streaming ceilings: %s" % e)
+        return None
+    a = torch.zeros(nbytes // 4, dtype=torch.float32, device=dev)
+    b = torch.zeros_like(a)
+    sink = torch.zeros(1, dtype=torch.float32, device=dev)
+    rows = hbm_probe.stream_table(a, b, sink, torch.cuda.current_stream(dev))
+    del a, b, sink
+    out = hbm_probe.best(rows)
+    out["source"] = ("paper_2102_02888_amd/csrc/hbm_probe.hip over %d MiB streams, best of %d "
+                     "cases per mix" % (nbytes >> 20, len(hbm_probe.CASES)))
+    return out
+
+
 def bench_variant(args, wl, plan, st, gbytes):
     """Times one of the paper's comparison variants on the same workload."""
     import torch
@@ -561,6 +586,13 @@ def main():
     if not args.no_probe:
         del events
         result["hbm_probe_gbps"] = hbm_probe(dev)
+        ceil = hbm_ceilings(dev)
+        result["hbm_ceiling_gbps"] = ceil
+        if ceil is not None:
+            # the worker pass reads two streams and rewrites the second: the `mix`
+            result["roofline"]["measured_mix_ceiling"] = {
+                "gbps": ceil["mix"]["gbps"],
+                "frac": result["roofline"]["achieved"] / ceil["mix"]["gbps"]}
     if not args.no_cpu_baseline:
         log("timing the oracle on sampled segments ...")
         result["cpu_baseline"] = cpu_baseline(st, plan, wl)

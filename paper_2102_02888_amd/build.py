@@ -1,5 +1,5 @@
 """Builds libonebit.so (the gfx950 HIP kernels and the C ABI) in-tree, and
-the standalone HBM streaming probe lib/hbm_probe."""
+the HBM streaming probe's own library lib/libhbmprobe.so."""
 import os
 import subprocess
 import sys
@@ -9,7 +9,7 @@ ROOT = os.path.dirname(HERE)
 SOURCES = [os.path.join(HERE, "csrc", f) for f in ("onebit_kernels.hip", "onebit_abi.hip")]
 LIB = os.path.join(HERE, "lib", "libonebit.so")
 PROBE_SOURCE = os.path.join(HERE, "csrc", "hbm_probe.hip")
-PROBE = os.path.join(HERE, "lib", "hbm_probe")
+PROBE = os.path.join(HERE, "lib", "libhbmprobe.so")
 
 # -ffp-contract=off: every fp32 operation is rounded once, as the method's
 # arithmetic is specified (no fused multiply-add contraction).
@@ -42,8 +42,7 @@ def _hipcc(flags, sources, target, verbose):
 
 def build(verbose: bool = False) -> str:
     _hipcc(HIPCC_FLAGS, SOURCES, LIB, verbose)
-    probe_flags = [f for f in HIPCC_FLAGS if f not in ("-fPIC", "-shared")]
-    _hipcc(probe_flags, [PROBE_SOURCE], PROBE, verbose)
+    _hipcc(HIPCC_FLAGS, [PROBE_SOURCE], PROBE, verbose)
     return LIB
 
 

@@ -1,10 +1,11 @@
 // HBM streaming ceilings for the access mixes of the library's passes.
 //
-// A standalone program (not part of libonebit.so) that times plain streaming
-// kernels with the same load and store forms as the passes (128-bit buffer
-// loads and stores, non-temporal; workgroups renumbered so that each XCD takes
-// one contiguous eighth of the grid) and prints one line per case: the median
-// of 7 timed launches and the bytes moved per second.  The mixes:
+// A small library of its own (libhbmprobe.so, not part of libonebit.so) that
+// times plain streaming kernels with the same load and store forms as the
+// passes (128-bit buffer loads and stores, non-temporal; workgroups
+// renumbered so that each XCD takes one contiguous eighth of the grid) on
+// caller-allocated device buffers: the median of 7 timed launches after one
+// untimed one.  The mixes:
 //
 //   read     one stream read (the flat read rate of the memory system);
 //   copy     one stream read, another written;
@@ -18,14 +19,12 @@
 // For read, copy and mix, K is the number of 1 KB pieces of each stream one
 // wave keeps in flight, and lds the bytes of (unused) LDS each workgroup
 // allocates, which caps the workgroups per CU and so the bytes in flight per
-// SIMD.  Every buffer is zero-filled, so the sums are 0 and the sink store in
-// k_read never happens (it keeps the loads live).
+// SIMD.  k_read stores to its sink only for one impossible-looking sum (it
+// keeps the loads live); the caller passes a sink of at least 4 bytes anyway.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
 #include <cstdint>
-#include <cstdio>
-#include <cstdlib>
 #include <vector>
 
 namespace {
@@ -38,16 +37,6 @@ constexpr int kXcds = 8;
 constexpr int kStreamLoad = 2;        // nt
 constexpr int kStreamStore = 2 | 16;  // nt, sc1
 constexpr int kPieceFloats = 256;     // 1 KB: 64 lanes x 16 B
-constexpr double kPeakGBs = 8000.0;
-
-#define CHECK(x)                                                                          \
-    do {                                                                                  \
-        hipError_t e_ = (x);                                                              \
-        if (e_ != hipSuccess) {                                                           \
-            fprintf(stderr, "hbm_probe: %s: %s\n", #x, hipGetErrorString(e_));            \
-            exit(1);                                                                      \
-        }                                                                                 \
-    } while (0)
 
 // Buffer resource over p with the maximum range; the base goes through
 // readfirstlane so that the compiler knows it is wave-uniform.
@@ -193,137 +182,109 @@ int64_t grid_for(int64_t waves, int waves_per_block)
     return (blocks + kXcds - 1) / kXcds * kXcds;
 }
 
+// Median of 7 timed launches (after one untimed) on stream s, in *ms.
 template <class F>
-float median_ms(F launch)
+hipError_t median_ms(F launch, hipStream_t s, float *ms)
 {
-    hipEvent_t e0, e1;
-    CHECK(hipEventCreate(&e0));
-    CHECK(hipEventCreate(&e1));
-    launch();
-    CHECK(hipGetLastError());
-    CHECK(hipDeviceSynchronize());
+    hipEvent_t e0 = nullptr, e1 = nullptr;
+    hipError_t err = hipEventCreate(&e0);
+    if (err == hipSuccess) err = hipEventCreate(&e1);
     std::vector<float> ts;
-    for (int r = 0; r < 7; ++r) {
-        CHECK(hipEventRecord(e0, 0));
+    if (err == hipSuccess) {
         launch();
-        CHECK(hipEventRecord(e1, 0));
-        CHECK(hipEventSynchronize(e1));
-        float ms = 0.f;
-        CHECK(hipEventElapsedTime(&ms, e0, e1));
-        ts.push_back(ms);
+        err = hipGetLastError();
     }
-    CHECK(hipEventDestroy(e0));
-    CHECK(hipEventDestroy(e1));
+    if (err == hipSuccess) err = hipStreamSynchronize(s);
+    for (int r = 0; r < 7 && err == hipSuccess; ++r) {
+        err = hipEventRecord(e0, s);
+        if (err == hipSuccess) {
+            launch();
+            err = hipGetLastError();
+        }
+        if (err == hipSuccess) err = hipEventRecord(e1, s);
+        if (err == hipSuccess) err = hipEventSynchronize(e1);
+        float t = 0.f;
+        if (err == hipSuccess) err = hipEventElapsedTime(&t, e0, e1);
+        ts.push_back(t);
+    }
+    if (e0) (void)hipEventDestroy(e0);
+    if (e1) (void)hipEventDestroy(e1);
+    if (err != hipSuccess) return err;
     std::sort(ts.begin(), ts.end());
-    return ts[ts.size() / 2];
-}
-
-void report(const char *name, int K, int lds, int waves_per_cu, double bytes, float ms)
-{
-    const double gbs = bytes / ms / 1e6;
-    printf("%-4s K=%d lds=%5d (<= %2d waves/CU, <= %2d KB/SIMD of loads in flight)  %8.3f ms  "
-           "%6.0f GB/s  %.3f\n",
-           name, K, lds, waves_per_cu, waves_per_cu / 4 * K * (name[0] == 'm' ? 2 : 1), ms, gbs,
-           gbs / kPeakGBs);
-    fflush(stdout);
-}
-
-// Upper bound on the waves per CU of a 4-wave workgroup that allocates lds
-// bytes of LDS: the 160 KB of LDS per CU and 8 waves per SIMD (32 per CU).
-int stream_waves_per_cu(int lds)
-{
-    const int by_lds = lds > 0 ? (160 * 1024) / lds : 8;
-    return std::min(8, by_lds) * kStreamWaves;
+    *ms = ts[ts.size() / 2];
+    return hipSuccess;
 }
 
 template <int K>
-void stream_cases(float *a, float *b, float *sink, int64_t floats, int lds)
+hipError_t stream_case(int kind, const float *a, float *b, float *sink, int64_t pieces, int lds,
+                       hipStream_t s, float *ms)
 {
-    const int64_t pieces = floats / kPieceFloats;  // a multiple of every K used
-    const int64_t grid = grid_for(pieces / K, kStreamWaves);
-    const dim3 block(kStreamWaves * kWave);
-    const double stream = (double)floats * 4;
-    const int wpc = stream_waves_per_cu(lds);
-    report("read", K, lds, wpc, stream,
-           median_ms([&] { hipLaunchKernelGGL(k_read<K>, dim3(grid), block, lds, 0, a, pieces,
-                                              sink); }));
-    report("copy", K, lds, wpc, 2 * stream,
-           median_ms([&] { hipLaunchKernelGGL(k_copy<K>, dim3(grid), block, lds, 0, a, b,
-                                              pieces); }));
-    report("mix", K, lds, wpc, 3 * stream,
-           median_ms([&] { hipLaunchKernelGGL(k_mix<K>, dim3(grid), block, lds, 0, a, b,
-                                              pieces); }));
-}
-
-template <int W, int B>
-void rowsum_case(const float *g, int64_t D, int R, float *out)
-{
-    const int64_t tiles = D / kTile;
-    const int64_t grid = grid_for(tiles, W);
-    const double bytes = (double)R * D * 4 + (double)D * 4;
-    const float ms = median_ms([&] {
-        hipLaunchKernelGGL((k_rowsum<W, B>), dim3(grid), dim3(W * kWave), 0, 0, g, D, R, tiles,
-                           out);
-    });
-    printf("rowsum R=%d W=%2d B=%d  %8.3f ms  %6.0f GB/s  %.3f\n", R, W, B, ms,
-           bytes / ms / 1e6, bytes / ms / 1e6 / kPeakGBs);
-    fflush(stdout);
+    const dim3 grid((unsigned)grid_for(pieces / K, kStreamWaves)), block(kStreamWaves * kWave);
+    switch (kind) {
+    case 0:
+        return median_ms([&] { hipLaunchKernelGGL(k_read<K>, grid, block, lds, s, a, pieces,
+                                                  sink); }, s, ms);
+    case 1:
+        return median_ms([&] { hipLaunchKernelGGL(k_copy<K>, grid, block, lds, s, a, b,
+                                                  pieces); }, s, ms);
+    default:
+        return median_ms([&] { hipLaunchKernelGGL(k_mix<K>, grid, block, lds, s, a, b,
+                                                  pieces); }, s, ms);
+    }
 }
 
 }  // namespace
 
-int main()
+extern "C" {
+
+// One streaming case over device buffers a and b of `floats` floats each
+// (a multiple of 1024; a is only read, b is written by copy and mix) and a
+// 4-byte sink, on stream s.  kind: 0 read a, 1 copy a to b, 2 mix b = a + b.
+// k: 1 KB pieces per stream per wave, 1, 2 or 4.  lds: bytes of LDS per
+// 4-wave workgroup, 0 to 65536.  Writes the median time in ms to *ms.
+// Returns 0, -1 for an invalid argument, or the HIP error code.
+int hbm_probe_stream(int kind, int k, int lds, const float *a, float *b, float *sink,
+                     int64_t floats, hipStream_t s, float *ms)
 {
-    hipDeviceProp_t prop;
-    CHECK(hipGetDeviceProperties(&prop, 0));
-    printf("device %s (%s), %d CUs\n", prop.name, prop.gcnArchName, prop.multiProcessorCount);
-
-    // Streams of 4 GiB each: far beyond the 256 MB last-level cache.
-    const int64_t floats = (int64_t)1 << 30;
-    float *a = nullptr, *b = nullptr, *sink = nullptr;
-    CHECK(hipMalloc(&a, floats * 4));
-    CHECK(hipMalloc(&b, floats * 4));
-    CHECK(hipMalloc(&sink, 4));
-    CHECK(hipMemset(a, 0, floats * 4));
-    CHECK(hipMemset(b, 0, floats * 4));
-    printf("read / copy / mix over %lld MiB streams\n", (long long)(floats * 4 >> 20));
-    fflush(stdout);
-    for (int lds : {0, 40960, 65536}) {
-        stream_cases<1>(a, b, sink, floats, lds);
-        stream_cases<2>(a, b, sink, floats, lds);
-        stream_cases<4>(a, b, sink, floats, lds);
+    if (kind < 0 || kind > 2 || !a || !sink || !ms || (kind > 0 && !b) || floats <= 0 ||
+        floats % 1024 || lds < 0 || lds > 65536)
+        return -1;
+    const int64_t pieces = floats / kPieceFloats;
+    if (grid_for(pieces, kStreamWaves) > 0x7FFFFFF0) return -1;  // k = 1's grid
+    hipError_t e;
+    switch (k) {
+    case 1: e = stream_case<1>(kind, a, b, sink, pieces, lds, s, ms); break;
+    case 2: e = stream_case<2>(kind, a, b, sink, pieces, lds, s, ms); break;
+    case 4: e = stream_case<4>(kind, a, b, sink, pieces, lds, s, ms); break;
+    default: return -1;
     }
-    CHECK(hipFree(a));
-    CHECK(hipFree(b));
-    CHECK(hipFree(sink));
-
-    // The warm-up's pattern on the BERT-Large shape: 32 rows of 334,088,192 floats.
-    const int R = 32;
-    const int64_t D = 334088192;  // 326,258 tiles of 1024
-    float *g = nullptr, *out = nullptr;
-    CHECK(hipMalloc(&g, (size_t)R * D * 4));
-    CHECK(hipMalloc(&out, (size_t)D * 4));
-    CHECK(hipMemset(g, 0, (size_t)R * D * 4));
-    CHECK(hipMemset(out, 0, (size_t)D * 4));
-    printf("rowsum over %d rows of %lld floats (%.1f GB read)\n", R, (long long)D,
-           (double)R * D * 4 / 1e9);
-    fflush(stdout);
-    rowsum_case<16, 1>(g, D, R, out);
-    rowsum_case<16, 2>(g, D, R, out);
-    rowsum_case<8, 1>(g, D, R, out);
-    rowsum_case<4, 1>(g, D, R, out);
-    {
-        // the same bytes read flat
-        const int64_t fl = (int64_t)R * D, pieces = fl / kPieceFloats;
-        const float ms = median_ms([&] {
-            hipLaunchKernelGGL(k_read<4>, dim3(grid_for(pieces / 4, kStreamWaves)),
-                               dim3(kStreamWaves * kWave), 0, 0, g, pieces, out);
-        });
-        printf("flat read of the %d rows  %8.3f ms  %6.0f GB/s  %.3f\n", R, ms,
-               (double)fl * 4 / ms / 1e6, (double)fl * 4 / ms / 1e6 / kPeakGBs);
-    }
-    CHECK(hipFree(g));
-    CHECK(hipFree(out));
-    printf("done\n");
-    return 0;
+    return (int)e;
 }
+
+// The warm-up's read pattern: R rows of D floats at g (row r at g + r D; D a
+// multiple of 1024) summed per 1024-element tile in row order in fp64 and
+// written once to out (D floats), one tile per wave, w waves per workgroup
+// (4, 8 or 16) and a barrier after every b rows (1 or 2; R a multiple of
+// b), on stream s.  Writes the median time in ms to *ms.  Returns 0, -1 for
+// an invalid argument, or the HIP error code.
+int hbm_probe_rowsum(int w, int b, const float *g, int64_t D, int R, float *out, hipStream_t s,
+                     float *ms)
+{
+    if (!g || !out || !ms || D <= 0 || D % kTile || R <= 0 || (b != 1 && b != 2) || R % b)
+        return -1;
+    const int64_t tiles = D / kTile;
+    if (grid_for(tiles, w) > 0x7FFFFFF0) return -1;
+#define ROWSUM(W, B)                                                                           \
+    median_ms([&] { hipLaunchKernelGGL((k_rowsum<W, B>), dim3((unsigned)grid_for(tiles, W)),     \
+                                       dim3(W * kWave), 0, s, g, D, R, tiles, out); }, s, ms)
+    hipError_t e;
+    if (w == 16 && b == 1) e = ROWSUM(16, 1);
+    else if (w == 16 && b == 2) e = ROWSUM(16, 2);
+    else if (w == 8 && b == 1) e = ROWSUM(8, 1);
+    else if (w == 4 && b == 1) e = ROWSUM(4, 1);
+    else return -1;
+#undef ROWSUM
+    return (int)e;
+}
+
+}  // extern "C"

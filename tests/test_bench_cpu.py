@@ -60,3 +60,23 @@ def test_multi_gpu_request_is_refused():
 def test_cpu_model_is_named():
     name = bench._cpu_model()
     assert name is None or (isinstance(name, str) and name)
+
+
+def test_hbm_probe_library_rejects_bad_arguments_on_the_host():
+    """The streaming probe's library loads without a GPU and rejects invalid
+    arguments before any device call (-1)."""
+    import ctypes
+    from paper_2102_02888_amd import build, hbm_probe
+    if not os.path.exists(hbm_probe.LIB_PATH):
+        build.build()
+    L = hbm_probe.lib()
+    ms = ctypes.c_float()
+    fake = ctypes.c_void_p(4096)  # never dereferenced: every call below is rejected first
+    assert L.hbm_probe_stream(3, 1, 0, fake, fake, fake, 1024, None, ctypes.byref(ms)) == -1
+    assert L.hbm_probe_stream(0, 3, 0, fake, fake, fake, 1024, None, ctypes.byref(ms)) == -1
+    assert L.hbm_probe_stream(0, 1, 0, fake, fake, fake, 1000, None, ctypes.byref(ms)) == -1
+    assert L.hbm_probe_stream(1, 1, 0, fake, None, fake, 1024, None, ctypes.byref(ms)) == -1
+    assert L.hbm_probe_stream(2, 1, 70000, fake, fake, fake, 1024, None, ctypes.byref(ms)) == -1
+    assert L.hbm_probe_rowsum(16, 3, fake, 1024, 2, fake, None, ctypes.byref(ms)) == -1
+    assert L.hbm_probe_rowsum(16, 2, fake, 1024, 3, fake, None, ctypes.byref(ms)) == -1
+    assert L.hbm_probe_rowsum(12, 1, fake, 1024, 2, fake, None, ctypes.byref(ms)) == -1
