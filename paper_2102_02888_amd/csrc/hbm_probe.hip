@@ -270,8 +270,8 @@ int hbm_probe_stream(int kind, int k, int lds, const float *a, float *b, float *
 int hbm_probe_rowsum(int w, int b, const float *g, int64_t D, int R, float *out, hipStream_t s,
                      float *ms)
 {
-    if (!g || !out || !ms || D <= 0 || D % kTile || R <= 0 || (b != 1 && b != 2) || R % b)
-        return -1;
+    const bool shape = (w == 16 && (b == 1 || b == 2)) || ((w == 8 || w == 4) && b == 1);
+    if (!shape || !g || !out || !ms || D <= 0 || D % kTile || R <= 0 || R % b) return -1;
     const int64_t tiles = D / kTile;
     if (grid_for(tiles, w) > 0x7FFFFFF0) return -1;
 #define ROWSUM(W, B)                                                                           \

@@ -80,3 +80,5 @@ def test_hbm_probe_library_rejects_bad_arguments_on_the_host():
     assert L.hbm_probe_rowsum(16, 3, fake, 1024, 2, fake, None, ctypes.byref(ms)) == -1
     assert L.hbm_probe_rowsum(16, 2, fake, 1024, 3, fake, None, ctypes.byref(ms)) == -1
     assert L.hbm_probe_rowsum(12, 1, fake, 1024, 2, fake, None, ctypes.byref(ms)) == -1
+    assert L.hbm_probe_rowsum(0, 1, fake, 1024, 2, fake, None, ctypes.byref(ms)) == -1
+    assert L.hbm_probe_rowsum(8, 2, fake, 1024, 2, fake, None, ctypes.byref(ms)) == -1
