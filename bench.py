@@ -302,7 +302,7 @@ def bench_variant(args, wl, plan, st, gbytes):
     else:
         t0 = wl.warmup_steps
         step = lambda k: st.step_naive(wl.lr, wl.beta1, wl.beta2, wl.eps, t0 + k + 1)
-        bytes_pp = (4 + n * (gbytes + 8 + 1 / 8)) + (n / 8 + 8 + 1 / 8) + (1 / 8 + 24)
+        bytes_pp = (1 / 8 + n * (gbytes + 8 + 1 / 8)) + (n / 8 + 8 + 1 / 8) + (1 / 8 + 24)
         name = "Adam(1-bit Naive) step: gradient compressed, Adam on the decoded average"
     for k in range(args.warmup):
         step(k)

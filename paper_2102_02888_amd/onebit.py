@@ -459,11 +459,20 @@ class State:
         is error-compensated and compressed by every worker (the worker pass
         with beta1 = 0 over a zero momentum), averaged and recompressed by the
         chunk owners, and Adam updates m and v from the decoded result."""
-        if not hasattr(self, "_zero"):
-            self._zero = torch.zeros_like(self.m)
-        onebit_worker_compress(self.plan, self._zero, self.grads, self.worker_err,
+        if not hasattr(self, "_plus_bits"):
+            # With beta1 = 0 the worker's momentum term is 0 * m.  Decoded from
+            # all-ones sign words and zero scales, m is +0 everywhere, and
+            # 0 * +0 is the same +0 that a zero fp32 momentum gives, so the
+            # packed-momentum pass computes exactly what the fp32-momentum
+            # row walk would, reading 1/8 byte of m per element and row.
+            self._plus_bits = torch.full((self.plan.W,), -1, dtype=torch.int64,
+                                         device=self.x.device)
+            self._zero_scales = torch.zeros(self.plan.S, dtype=torch.float32,
+                                            device=self.x.device)
+        onebit_worker_compress(self.plan, None, self.grads, self.worker_err,
                                self.worker_bits, self.worker_scales, 0.0, self.workspace,
-                               n_local=self.n_local, stream=stream)
+                               n_local=self.n_local, m_bits=self._plus_bits,
+                               m_scales=self._zero_scales, stream=stream)
         onebit_server_reduce_compress(self.plan, 0, self.plan.n, self.worker_bits,
                                       self.worker_scales, self.server_err, self.server_bits,
                                       self.server_scales, self.workspace, stream=stream)

@@ -98,3 +98,28 @@ def test_naive_variant_free_running(ob, dev):
     check_fp("worker delta", host(st.worker_delta()), delta, mask=mask)
     check_fp("server delta", host(st.server_delta()), dbar, mask=mask)
     plan.close()
+
+
+def test_naive_worker_pass_matches_zero_fp32_momentum_bitwise(ob, dev):
+    """step_naive's worker call decodes m from all-ones sign words and zero
+    scales (+0 everywhere) to take the packed-momentum pass; with beta1 = 0
+    that is bit for bit the fp32-momentum row walk over a zero m, including
+    ragged tiles and an empty tensor, over several steps of error feedback."""
+    wl = synth.Workload(name="naive_eq", numel=[70_001, 0, 4097, 1000], n=5, warmup_steps=0,
+                        steps=3)
+    L, plan, a, x, mask = _setup(ob, dev, wl)
+    b = ob.State(plan, dev)
+    b.x.copy_(a.x)
+    zero_m = torch.zeros_like(a.m)
+    for t in range(1, wl.steps + 1):
+        gt, _ = _grads(wl, L, t, torch.float32)
+        a.grads.copy_(gt.to(dev))
+        b.grads.copy_(gt.to(dev))
+        a.step_naive(wl.lr, wl.beta1, wl.beta2, wl.eps, t)
+        ob.onebit_worker_compress(plan, zero_m, b.grads, b.worker_err, b.worker_bits,
+                                  b.worker_scales, 0.0, b.workspace)
+        torch.cuda.synchronize()
+        assert torch.equal(a.worker_bits, b.worker_bits), t
+        assert torch.equal(a.worker_scales.view(torch.int32), b.worker_scales.view(torch.int32)), t
+        assert torch.equal(a.worker_err.view(torch.int32), b.worker_err.view(torch.int32)), t
+    plan.close()
