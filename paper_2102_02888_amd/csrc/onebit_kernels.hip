@@ -317,8 +317,8 @@ __device__ __forceinline__ void warmup_update(const double (&sum)[kSubBlocks][4]
 // the "Adam(1-bit Naive)" comparison variant of Section 7.2 updates m and v
 // from the compressed gradient this way.  Loads first, then stores.
 // ---------------------------------------------------------------------------
-template <bool FULL>
-__device__ __forceinline__ void adam_message_tile(const Tile &tile, int lane,
+template <bool FULL, int SB>
+__device__ __forceinline__ void adam_message_tile(const Tile &tile, int lane, int sb0,
                                                   const uint64_t *__restrict__ bits, float s,
                                                   float *__restrict__ x, float *__restrict__ m,
                                                   float *__restrict__ v, float lr, float beta1,
@@ -327,19 +327,20 @@ __device__ __forceinline__ void adam_message_tile(const Tile &tile, int lane,
 {
     const int len = tile.len;
     const int64_t base = tile.start;
-    uint64_t word[kSubBlocks];
-    v4f xv[kSubBlocks], mv[kSubBlocks], vv[kSubBlocks];
+    uint64_t word[SB];
+    v4f xv[SB], mv[SB], vv[SB];
 #pragma unroll
-    for (int b = 0; b < kSubBlocks; ++b) {
-        const int li = b * (kWave * 4) + 4 * lane;
-        word[b] = (FULL || li < len) ? bits[(base >> 6) + 4 * b + (lane >> 4)] : 0ull;
+    for (int b = 0; b < SB; ++b) {
+        const int sb = sb0 + b;
+        const int li = sb * (kWave * 4) + 4 * lane;
+        word[b] = (FULL || li < len) ? bits[(base >> 6) + 4 * sb + (lane >> 4)] : 0ull;
         xv[b] = ld4<FULL>(x + base, li, len);
         mv[b] = ld4<FULL>(m + base, li, len);
         vv[b] = ld4<FULL>(v + base, li, len);
     }
 #pragma unroll
-    for (int b = 0; b < kSubBlocks; ++b) {
-        const int li = b * (kWave * 4) + 4 * lane;
+    for (int b = 0; b < SB; ++b) {
+        const int li = (sb0 + b) * (kWave * 4) + 4 * lane;
         const uint32_t nib = (uint32_t)(word[b] >> (4 * (lane & 15))) & 0xFu;
 #pragma unroll
         for (int c = 0; c < 4; ++c) {
@@ -367,23 +368,31 @@ __device__ __forceinline__ void adam_message_tile(const Tile &tile, int lane,
     }
 }
 
+// One 256-element sub-block per wave, four waves per tile, as in the update
+// (fewer bytes in flight per wave).
+constexpr int kAdamMessageSubBlocks = 1;
+constexpr int kAdamMessageWavesPerTile = kSubBlocks / kAdamMessageSubBlocks;
+
 __global__ __launch_bounds__(kBlock) void k_adam_message(
     const Tile *__restrict__ tiles, int64_t num_tiles, const uint64_t *__restrict__ bits,
     const float *__restrict__ scales, float *__restrict__ x, float *__restrict__ m,
     float *__restrict__ v, float lr, float beta1, float omb1, float beta2, float omb2, float eps,
     int use_bc, float bc1, float bc2)
 {
+    constexpr int SB = kAdamMessageSubBlocks;
     const int lane = threadIdx.x & (kWave - 1);
-    const int64_t t = xcd_block() * kWavesPerBlock + (threadIdx.x >> 6);
+    const int64_t w = xcd_block() * kWavesPerBlock + (threadIdx.x >> 6);
+    const int64_t t = w / kAdamMessageWavesPerTile;
+    const int sb0 = (int)(w % kAdamMessageWavesPerTile) * SB;
     if (t >= num_tiles) return;
     const Tile tile = tiles[t];
     const float s = scales[tile.seg];
     if (tile.len == kTileElems)
-        adam_message_tile<true>(tile, lane, bits, s, x, m, v, lr, beta1, omb1, beta2, omb2, eps,
-                                use_bc, bc1, bc2);
+        adam_message_tile<true, SB>(tile, lane, sb0, bits, s, x, m, v, lr, beta1, omb1, beta2,
+                                    omb2, eps, use_bc, bc1, bc2);
     else
-        adam_message_tile<false>(tile, lane, bits, s, x, m, v, lr, beta1, omb1, beta2, omb2, eps,
-                                 use_bc, bc1, bc2);
+        adam_message_tile<false, SB>(tile, lane, sb0, bits, s, x, m, v, lr, beta1, omb1, beta2,
+                                     omb2, eps, use_bc, bc1, bc2);
 }
 
 // ---------------------------------------------------------------------------
@@ -2133,7 +2142,8 @@ hipError_t launch_adam_message(const DeviceTables &tb, int64_t num_tiles, const 
                                float bc2, hipStream_t s)
 {
     const float omb1 = 1.0f - beta1, omb2 = 1.0f - beta2;
-    hipLaunchKernelGGL(k_adam_message, dim3((unsigned)blocks_for(num_tiles)), dim3(kBlock), 0, s,
+    hipLaunchKernelGGL(k_adam_message, dim3((unsigned)blocks_for(num_tiles * kAdamMessageWavesPerTile)),
+                       dim3(kBlock), 0, s,
                        tb.tiles, num_tiles, bits, scales, x, m, v, lr, beta1, omb1, beta2, omb2,
                        eps, use_bc, bc1, bc2);
     return hipGetLastError();
